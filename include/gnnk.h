@@ -1,0 +1,248 @@
+/*
+ * gnnk: generalized sparse message-passing kernels for MI355X (gfx950).
+ *
+ * C ABI of the GPU library libgnnk.so.  It implements the two primitives that
+ * Section 3 of "Deep Graph Library: A Graph-Centric, Highly-Performant Package
+ * for Graph Neural Networks" (arXiv 1909.01315) reduces message passing to:
+ *
+ *   g-SDDMM  m_e = phi(x_u, y_v, w_e)                 for every edge (u, e, v)
+ *   g-SpMM   z_v = rho{ phi(x_u, w_e) : (u, e, v) }   over the in-edges of v
+ *
+ * and their gradients, which by Theorem 1 are again a g-SDDMM on the graph
+ * (edge gradients) and g-SpMMs on the graph or on the reverse graph (node
+ * gradients).  Edge softmax and the leaky ReLU of attention layers are
+ * provided on the same graph structure.
+ *
+ * Conventions shared by every call:
+ *  - Every call returns a gnnk_status and never throws.  On failure
+ *    gnnk_last_error() describes the cause (thread-local, valid until the next
+ *    gnnk call on the same thread).
+ *  - Device pointers: all tensor and index pointers are device memory owned by
+ *    the caller; the library never frees them.  A NULL tensor pointer means
+ *    "absent" where the argument is documented nullable.
+ *  - Work is enqueued on `stream` and runs asynchronously; calls return before
+ *    the kernels finish.  Only graph_create_* and graph_validate synchronise.
+ *  - Outputs are fully overwritten, never accumulated into.  Inputs may alias
+ *    each other; outputs must not alias inputs or each other.
+ *  - Edge tensors are indexed by edge id.  Node tensors by node id.
+ *  - Index ranges are not checked on the compute path; use graph_validate.
+ *  - All floating-point tensors of one call share one dtype.  Sums and dot
+ *    products accumulate in fp64 and are rounded once to the output dtype
+ *    (bf16 outputs: to fp32, then to bf16 round-to-nearest-even).
+ *  - Calls that use the same graph handle must be ordered (one stream, or
+ *    synchronised): the handle owns the scratch space of hub-row partials.
+ */
+#ifndef GNNK_H
+#define GNNK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GNNK_OK = 0,
+    GNNK_EINVAL = 1,       /* invalid argument: enum, shape, broadcast, NULL */
+    GNNK_EUNSUPPORTED = 2, /* legal combination that is not implemented */
+    GNNK_EHIP = 3,         /* HIP runtime or launch error */
+    GNNK_ERANGE = 4,       /* graph_validate: an index is out of range */
+    GNNK_ENOMEM = 5        /* workspace too small or allocation failed */
+} gnnk_status;
+
+typedef enum { GNNK_I32 = 0, GNNK_I64 = 1 } gnnk_itype;
+typedef enum { GNNK_F32 = 0, GNNK_BF16 = 1 } gnnk_ftype;
+
+/* message functions phi: copy_u = COPY_LHS, copy_e = COPY_RHS, and the binary
+ * ops on (lhs, rhs); DOT reduces the feature dimension (g-SDDMM only). */
+typedef enum {
+    GNNK_COPY_LHS = 0,
+    GNNK_COPY_RHS = 1,
+    GNNK_ADD = 2,
+    GNNK_SUB = 3,
+    GNNK_MUL = 4,
+    GNNK_DIV = 5,
+    GNNK_DOT = 6
+} gnnk_binop;
+
+/* reduce functions rho of g-SpMM */
+typedef enum { GNNK_SUM = 0, GNNK_MEAN = 1, GNNK_MAX = 2, GNNK_MIN = 3 } gnnk_reduce;
+
+/* where a g-SDDMM operand lives: u (source node), e (edge), v (destination) */
+typedef enum { GNNK_SRC = 0, GNNK_EDGE = 1, GNNK_DST = 2 } gnnk_target;
+
+/* A dense (rows, heads, feat) tensor, row-major, with a row stride in
+ * elements (>= heads * feat).  Broadcasting (Appendix D's multi-head forms):
+ * an operand may be (H, F), (H, 1) or (1, 1) against an (H, F) message. */
+typedef struct {
+    void* data;
+    int64_t rows;
+    int32_t heads;
+    int32_t feat;
+    int64_t row_stride;
+    int32_t dtype; /* gnnk_ftype */
+    int32_t reserved;
+} gnnk_tensor;
+
+typedef struct gnnk_graph* gnnk_graph_t; /* opaque, immutable after creation */
+
+/* Host-side description of a graph handle (no GPU access). */
+typedef struct {
+    int64_t num_src, num_dst, num_edges;
+    int32_t ptr_type;       /* gnnk_itype of the CSR row offsets */
+    int32_t identity_eids;  /* 1 when edge id == in-CSR position */
+    int64_t max_in_degree, max_out_degree;
+    int64_t empty_dst_rows, empty_src_rows;
+    int64_t seg_edges;      /* edges per segment of a hub row */
+    int64_t hub_dst_rows, hub_src_rows;   /* rows longer than seg_edges */
+    int64_t segments_in, segments_out;    /* segments of those rows */
+    size_t workspace_bytes;
+} gnnk_graph_info;
+
+/* ------------------------------------------------------------------------ */
+/* Graph structure (Section 4.1: CSR for g-SpMM forward, the reverse graph's
+ * CSR for backward, edge ids kept; Appendix A, definition of the reverse
+ * graph).  A handle holds the in-CSR (rows = destinations), the out-CSR of
+ * the reverse graph (rows = sources, with the original edge ids), in- and
+ * out-degrees, rows sorted by degree for scheduling, and the segment tables
+ * of rows longer than seg_edges.  Derived arrays live in a caller-allocated
+ * device workspace of graph_workspace_bytes() bytes, which the caller keeps
+ * alive (with any borrowed index arrays) until graph_destroy.  Building is
+ * done by the host library: the index arrays are copied to the host once,
+ * which synchronises `stream`. */
+
+/* Upper bound of the workspace for a graph of this size; ptr_t is the width
+ * of the CSR row offsets the handle builds (GNNK_I64 needed when
+ * num_edges >= 2^31). */
+gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_itype ptr_t,
+                                  size_t* bytes);
+
+/* From an edge list in edge-id order: edge e goes src[e] -> dst[e] (device
+ * int32 arrays of num_edges entries, only read during the call).  Edges of a
+ * destination keep ascending edge id in the in-CSR, edges of a source keep
+ * ascending edge id in the out-CSR.  Multi-edges and self-loops are legal. */
+gnnk_status graph_create_coo(int64_t num_src, int64_t num_dst, int64_t num_edges, const int32_t* src,
+                             const int32_t* dst, gnnk_itype ptr_t, void* workspace, size_t ws_bytes,
+                             hipStream_t stream, gnnk_graph_t* out);
+
+/* From an in-CSR: indptr (num_dst + 1 entries of ptr_t), indices (num_edges
+ * int32 source ids) and eids (num_edges int32 edge ids, or NULL when the edge
+ * id is the position).  These device arrays are borrowed, not copied: keep
+ * them unchanged until graph_destroy.  Rows must be ascending in position
+ * (indptr non-decreasing, indptr[0] == 0, indptr[num_dst] == num_edges). */
+gnnk_status graph_create_csr(int64_t num_src, int64_t num_dst, int64_t num_edges, const void* indptr,
+                             gnnk_itype ptr_t, const int32_t* indices, const int32_t* eids, void* workspace,
+                             size_t ws_bytes, hipStream_t stream, gnnk_graph_t* out);
+
+/* Host-side facts about a handle. */
+gnnk_status graph_info(gnnk_graph_t g, gnnk_graph_info* info);
+
+/* In-degrees (num_dst int32) and out-degrees (num_src int32), written to
+ * caller device memory on `stream` (the batched g.in_degree of Section 4.1). */
+gnnk_status graph_in_degrees(gnnk_graph_t g, int32_t* out, hipStream_t stream);
+gnnk_status graph_out_degrees(gnnk_graph_t g, int32_t* out, hipStream_t stream);
+
+/* Copy the in-CSR (reverse = 0) or the reverse graph's CSR (reverse = 1) into
+ * caller device buffers: indptr (rows + 1 entries of the handle's ptr type),
+ * indices (num_edges int32), eids (num_edges int32; for reverse = 0 with
+ * identity ids this is 0..E-1).  Any of the three may be NULL. */
+gnnk_status graph_csr_export(gnnk_graph_t g, int reverse, void* indptr, int32_t* indices, int32_t* eids,
+                             hipStream_t stream);
+
+/* Check every stored index against its range; synchronises `stream`.
+ * Returns GNNK_ERANGE if any index is out of range. */
+gnnk_status graph_validate(gnnk_graph_t g, hipStream_t stream);
+
+/* Free the handle and any scratch it allocated (not the workspace). */
+gnnk_status graph_destroy(gnnk_graph_t g);
+
+/* ------------------------------------------------------------------------ */
+/* g-SpMM (Section 3, definition of generalized SpMM):
+ *   out[v] = reduce over in-edges (u, e, v) of op(lhs[u], rhs[e])
+ * op: COPY_LHS | COPY_RHS | ADD | SUB | MUL | DIV (not DOT).
+ * lhs: num_src rows (NULL iff op == COPY_RHS); rhs: num_edges rows (NULL iff
+ * op == COPY_LHS); out: num_dst rows of the broadcast (H, F) shape.
+ * reduce: SUM, MEAN (divides by the in-degree, multi-edges counted), MAX, MIN.
+ * A destination with no in-edge gets 0.
+ * MAX/MIN: messages are formed in fp32 and compared exactly; the smallest edge
+ * id wins a tie.  arg_lhs (source id) and arg_rhs (edge id) are nullable dense
+ * (num_dst, H, F) int32 arrays, -1 for empty destinations.
+ * Errors: GNNK_EINVAL on a bad op/reduce, shapes or dtypes; GNNK_EUNSUPPORTED
+ * for arg arrays with SUM/MEAN. */
+gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                  const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
+                  hipStream_t stream);
+
+/* g-SDDMM (Section 3, definition of generalized SDDMM):
+ *   out[e] = op(lhs[t_l(e)], rhs[t_r(e)]) for every edge (u, e, v),
+ * t(e) being u, e or v by the operand's target.  ADD/SUB/MUL/DIV are single
+ * fp32 operations; DOT is the fp64-accumulated inner product over the feature
+ * dimension, giving (E, H, 1) (the per-head attention score of Appendix D);
+ * COPY_LHS / COPY_RHS copy one operand.  out: num_edges rows. */
+gnnk_status gsddmm(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
+                   const gnnk_tensor* rhs, gnnk_target rhs_target, gnnk_tensor* out, hipStream_t stream);
+
+/* Gradients of gspmm (Theorem 1; Appendix A, the lemma on dL/dW of g-SpMM and
+ * lemma complex_dspmm_dx).  With g'_e = grad_out[v] scaled by d rho/d m_e
+ * (1 for SUM, 1/deg(v) for MEAN, for MAX/MIN 1 iff e is arg_rhs[v]):
+ *   grad_lhs[u] = sum over out-edges (u, e, v) of g'_e * d phi/d lhs   (a
+ *                 g-SpMM on the reverse graph)
+ *   grad_rhs[e] = g'_e * d phi/d rhs                                   (a
+ *                 g-SDDMM on the graph)
+ * both summed over broadcast positions when the operand is broadcast.
+ * lhs/rhs as in the forward call; grad_out: num_dst rows of the message
+ * shape.  arg_rhs is required for MAX/MIN (the edge ids written by gspmm);
+ * arg_lhs is accepted and unused.  grad_lhs / grad_rhs are nullable.  MAX/MIN
+ * run without atomics (a masked reverse g-SpMM and a masked g-SDDMM). */
+gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                           const gnnk_tensor* rhs, const int32_t* arg_lhs, const int32_t* arg_rhs,
+                           const gnnk_tensor* grad_out, gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs,
+                           hipStream_t stream);
+
+/* Gradients of gsddmm (Appendix A, the lemma on dL/dW of g-SDDMM and lemma
+ * rev): an operand on the source side collects over its node's out-edges
+ * (reverse graph), on the destination side over its in-edges, on the edge side
+ * from its own edge.  grad_out: num_edges rows of the output shape.
+ * grad_lhs / grad_rhs are nullable and take their operand's shape. */
+gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
+                            const gnnk_tensor* rhs, gnnk_target rhs_target, const gnnk_tensor* grad_out,
+                            gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs, hipStream_t stream);
+
+/* Edge softmax (the attention normalisation applied to Appendix D's edge
+ * scores): for each destination v and column c,
+ *   out[e, c] = exp(score[e, c] - max) / sum over in-edges of v of exp(. - max).
+ * score and out: num_edges rows, same shape.  Edges of a destination with one
+ * in-edge get exactly 1. */
+gnnk_status edge_softmax(gnnk_graph_t g, const gnnk_tensor* score, gnnk_tensor* out, hipStream_t stream);
+
+/* grad_score[e] = out[e] * (grad_out[e] - sum over in-edges e' of dst(e) of
+ * out[e'] * grad_out[e']), where out is the softmax result. */
+gnnk_status edge_softmax_backward(gnnk_graph_t g, const gnnk_tensor* out, const gnnk_tensor* grad_out,
+                                  gnnk_tensor* grad_score, hipStream_t stream);
+
+/* Leaky ReLU on an edge (or any) tensor: y = x > 0 ? x : slope * x (one fp32
+ * operation), and its backward dx = x > 0 ? dy : slope * dy. */
+gnnk_status edge_leaky_relu(const gnnk_tensor* x, gnnk_tensor* y, float slope, hipStream_t stream);
+gnnk_status edge_leaky_relu_backward(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* dx, float slope,
+                                     hipStream_t stream);
+
+/* ------------------------------------------------------------------------ */
+/* Tuning knobs, for schedule comparisons (forcing node- or edge-balanced
+ * schedules; the paper's Table 1 states both are valid for commutative and
+ * associative reducers).  Process-wide; "seg_edges" applies to graphs created
+ * afterwards, the others to calls issued afterwards.  Keys:
+ *   "seg_edges"   edges per hub-row segment (>= 32; default 2048)
+ *   "no_split"    1: never split a row across waves (hub rows run whole)
+ *   "small_deg"   rows of at most this in-degree share a wave (-1 = auto)
+ * Returns GNNK_EINVAL for an unknown key or value. */
+gnnk_status gnnk_set_option(const char* key, int64_t value);
+
+const char* gnnk_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GNNK_H */

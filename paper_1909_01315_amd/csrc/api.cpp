@@ -1,0 +1,590 @@
+// C ABI of the gnnk operators: argument checks, the geometry of a call
+// (broadcast pattern, vector width, lanes per edge), the schedule over the
+// degree-sorted rows, and the kernel launches.
+//
+// Theorem 1 of the paper drives the backward entry points: every gradient is
+// one more pass of the same row engine, a g-SpMM over the in-CSR or the
+// reverse graph's CSR, or a g-SDDMM over the in-CSR, with the message of the
+// corresponding lemma.
+#include <algorithm>
+#include <vector>
+
+#include "host.h"
+
+namespace gnnk {
+namespace {
+
+enum Kind { K_FULL = 0, K_HEADS = 1, K_SCALAR = 2, K_BAD = 3 };
+
+bool tensor_ok(const gnnk_tensor* t) {
+    return t && t->heads >= 1 && t->feat >= 1 && (t->dtype == GNNK_F32 || t->dtype == GNNK_BF16) &&
+           t->row_stride >= (int64_t)t->heads * t->feat && t->rows >= 0 && (t->data || t->rows == 0);
+}
+
+// shape of a tensor against an (H, F) message
+Kind kind_of(const gnnk_tensor* t, int H, int F) {
+    if (t->heads == H && t->feat == F) return K_FULL;
+    if (H == 1 && t->heads == 1 && t->feat == F) return K_FULL;
+    if (t->heads == H && t->feat == 1) return K_HEADS;
+    if (t->heads == 1 && t->feat == 1) return K_SCALAR;
+    return K_BAD;
+}
+
+struct Member {
+    const gnnk_tensor* t;
+    Kind kind;
+};
+
+struct Geo {
+    int H = 1, F = 1, vec = 1, NV = 1, L = 1, log2L = 0, G = 64, nchunk = 1;
+    bool merged = false;
+    int64_t D = 1;
+};
+
+int pow2ceil(int x) {
+    int p = 1;
+    while (p < x) p <<= 1;
+    return p;
+}
+
+// Choose the canonical geometry of an (Hm, Fm) message read and written by
+// `ms`.  When no tensor broadcasts over features only, heads and features
+// merge into one row of Hm * Fm columns.
+gnnk_status choose_geo(int Hm, int Fm, std::vector<Member>& ms, const std::vector<const void*>& int_arrays, Geo& g) {
+    for (auto& m : ms) {
+        m.kind = kind_of(m.t, Hm, Fm);
+        if (m.kind == K_BAD)
+            return fail(GNNK_EINVAL, "tensor (%d, %d) does not broadcast against the (%d, %d) message", m.t->heads,
+                        m.t->feat, Hm, Fm);
+    }
+    bool any_heads = false;
+    for (auto& m : ms) any_heads = any_heads || (m.kind == K_HEADS);
+    g.merged = !any_heads;
+    g.H = g.merged ? 1 : Hm;
+    g.F = g.merged ? Hm * Fm : Fm;
+    g.D = (int64_t)Hm * Fm;
+    const int es = ms.empty() ? 4 : (ms[0].t->dtype == GNNK_BF16 ? 2 : 4);
+    int cand[4] = {8, 4, 2, 1};
+    g.vec = 1;
+    for (int v : cand) {
+        if (v == 8 && es == 4) continue;
+        if (g.F % v) continue;
+        bool ok = true;
+        for (auto& m : ms) {
+            if (m.kind != K_FULL) continue;
+            if ((uintptr_t)m.t->data % (size_t)(v * es) || m.t->row_stride % v) ok = false;
+        }
+        for (const void* p : int_arrays)
+            if (p && (uintptr_t)p % (size_t)std::min(16, v * 4)) ok = false;
+        if (ok) {
+            g.vec = v;
+            break;
+        }
+    }
+    g.NV = (int)(g.D / g.vec);
+    if (g.NV > 64) {
+        g.L = 64;
+        g.nchunk = (g.NV + 63) / 64;
+    } else {
+        g.L = pow2ceil(g.NV);
+        g.nchunk = 1;
+    }
+    g.log2L = 0;
+    while ((1 << g.log2L) < g.L) ++g.log2L;
+    g.G = 64 / g.L;
+    return GNNK_OK;
+}
+
+OperandDev operand(const gnnk_tensor* t, Kind k, int32_t target) {
+    OperandDev o{};
+    if (!t) return o;
+    o.data = t->data;
+    o.stride = t->row_stride;
+    o.target = target;
+    o.full = k == K_FULL;
+    o.hmul = k == K_HEADS ? 1 : 0;
+    return o;
+}
+
+// output reduction over broadcast positions
+gnnk_status out_desc(const gnnk_tensor* t, Kind k, const Geo& g, OutDev& o) {
+    o.data = t->data;
+    o.stride = t->row_stride;
+    if (k == K_FULL) {
+        o.reduce = 0;
+        o.red = 1;
+        o.per_head = 0;
+        return GNNK_OK;
+    }
+    o.reduce = 1;
+    if (g.nchunk > 1) return fail(GNNK_EUNSUPPORTED, "reduced outputs need D / vec <= 64");
+    if (k == K_HEADS) {
+        o.red = g.F / g.vec;
+        o.per_head = 1;
+    } else {
+        o.red = g.NV;
+        o.per_head = 0;
+    }
+    return GNNK_OK;
+}
+
+CsrDev csr_of(const gnnk_graph* g, const Dir& d) {
+    CsrDev c{};
+    c.ptr = d.ptr;
+    c.idx = d.idx;
+    c.eid = d.eid;
+    c.perm = d.perm;
+    c.seg = d.seg;
+    c.hub_off = d.hub_off;
+    c.ptr64 = g->ptr64;
+    return c;
+}
+
+SchedDev schedule(const Dir& d, const Geo& geo, bool fill_empty) {
+    SchedDev s{};
+    const Options& o = options();
+    const bool split = o.no_split == 0;
+    const int64_t n_hub = split ? d.n_hub : 0;
+    const int64_t n_seg = split ? d.n_seg : 0;
+    int64_t T = o.small_deg >= 0 ? o.small_deg : (geo.G > 1 ? geo.G : 0);
+    int64_t n_big = std::max(d.count_above(T), n_hub);
+    n_big = std::min(n_big, d.n_nz);
+    const int fr = 4;
+    s.n_seg = (int32_t)n_seg;
+    s.n_hub = (int32_t)n_hub;
+    s.n_big = (int32_t)n_big;
+    s.n_nz = (int32_t)d.n_nz;
+    s.n_rows = (int32_t)d.n_rows;
+    s.w_big_end = (int32_t)(n_seg + (n_big - n_hub));
+    s.w_small_end = (int32_t)(s.w_big_end + (d.n_nz - n_big + geo.G - 1) / geo.G);
+    s.fill_rows_per_group = fr;
+    int64_t fill_waves = fill_empty ? (d.n_rows - d.n_nz + (int64_t)geo.G * fr - 1) / ((int64_t)geo.G * fr) : 0;
+    s.w_total = (int32_t)(s.w_small_end + fill_waves);
+    return s;
+}
+
+void set_geo(EngineArgs& A, const Geo& g) {
+    A.geo.F = g.F;
+    A.geo.NV = g.NV;
+    A.geo.L = g.L;
+    A.geo.log2L = g.log2L;
+    A.geo.G = g.G;
+    A.geo.nchunk = g.nchunk;
+}
+
+int dtype_code(const gnnk_tensor* t) { return t->dtype == GNNK_BF16 ? 1 : 0; }
+
+bool same_dtype(std::initializer_list<const gnnk_tensor*> ts) {
+    int d = -1;
+    for (auto t : ts) {
+        if (!t) continue;
+        if (d < 0) d = t->dtype;
+        else if (t->dtype != d) return false;
+    }
+    return true;
+}
+
+int64_t rows_of_target(const gnnk_graph* g, int t) {
+    return t == GNNK_SRC ? g->n_src : (t == GNNK_DST ? g->n_dst : g->n_edges);
+}
+
+gnnk_status launch_status(hipError_t e, const char* what) { return e == hipSuccess ? GNNK_OK : hip_fail(e, what); }
+
+// A row-reduction (g-SpMM) pass: sums, with hub partials and their combine.
+gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& geo, int dtype, int opk,
+                         hipStream_t s) {
+    A.csr = csr_of(g, d);
+    set_geo(A, geo);
+    A.sch = schedule(d, geo, true);
+    A.partial_stride = geo.D;
+    if (A.sch.n_seg > 0) {
+        A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 8);
+        if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
+    }
+    gnnk_status st = launch_status(launch_spmm(A, dtype, geo.vec, false, opk, s), "g-SpMM launch");
+    if (st == GNNK_OK && A.sch.n_hub > 0)
+        st = launch_status(launch_spmm_combine(A, dtype, geo.vec, false, s), "g-SpMM combine launch");
+    return st;
+}
+
+gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, int opk, hipStream_t s) {
+    A.csr = csr_of(g, g->in);
+    set_geo(A, geo);
+    A.sch = schedule(g->in, geo, false);
+    return launch_status(launch_sddmm(A, dtype, geo.vec, opk, s), "g-SDDMM launch");
+}
+
+int32_t tgt_in(int t) { return t == GNNK_SRC ? T_NBR : (t == GNNK_EDGE ? T_EDGE : T_SELF); }   // in-CSR walk
+int32_t tgt_out(int t) { return t == GNNK_SRC ? T_SELF : (t == GNNK_EDGE ? T_EDGE : T_NBR); }  // reverse walk
+
+}  // namespace
+}  // namespace gnnk
+
+using namespace gnnk;
+
+extern "C" {
+
+gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                  const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
+                  hipStream_t stream) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (op < GNNK_COPY_LHS || op > GNNK_DIV) return fail(GNNK_EINVAL, "gspmm op must be COPY_LHS..DIV");
+    if (reduce < GNNK_SUM || reduce > GNNK_MIN) return fail(GNNK_EINVAL, "bad reduce");
+    const bool use_l = op != GNNK_COPY_RHS, use_r = op != GNNK_COPY_LHS;
+    if (use_l != (lhs != nullptr) || use_r != (rhs != nullptr))
+        return fail(GNNK_EINVAL, "lhs is required unless COPY_RHS and rhs unless COPY_LHS (and absent otherwise)");
+    if ((use_l && !tensor_ok(lhs)) || (use_r && !tensor_ok(rhs)) || !tensor_ok(out))
+        return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({lhs, rhs, out})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
+    if ((use_l && lhs->rows != g->n_src) || (use_r && rhs->rows != g->n_edges) || out->rows != g->n_dst)
+        return fail(GNNK_EINVAL, "row counts must be num_src (lhs), num_edges (rhs), num_dst (out)");
+    const bool cmp = reduce == GNNK_MAX || reduce == GNNK_MIN;
+    if (!cmp && (arg_lhs || arg_rhs)) return fail(GNNK_EUNSUPPORTED, "arg arrays are only produced by MAX/MIN");
+    int Hm, Fm;
+    if (!use_r) { Hm = lhs->heads; Fm = lhs->feat; }
+    else if (!use_l) { Hm = rhs->heads; Fm = rhs->feat; }
+    else { Hm = std::max(lhs->heads, rhs->heads); Fm = std::max(lhs->feat, rhs->feat); }
+    if (out->heads != Hm || out->feat != Fm) return fail(GNNK_EINVAL, "out must have the message shape (%d, %d)", Hm, Fm);
+    std::vector<Member> ms;
+    if (use_l) ms.push_back({lhs, K_FULL});
+    if (use_r) ms.push_back({rhs, K_FULL});
+    ms.push_back({out, K_FULL});
+    Geo geo;
+    gnnk_status st = choose_geo(Hm, Fm, ms, {arg_lhs, arg_rhs}, geo);
+    if (st != GNNK_OK) return st;
+    if (g->n_dst == 0) return GNNK_OK;
+    EngineArgs A{};
+    size_t k = 0;
+    OperandDev ol = use_l ? operand(lhs, ms[k++].kind, T_NBR) : OperandDev{};
+    OperandDev orr = use_r ? operand(rhs, ms[k++].kind, T_EDGE) : OperandDev{};
+    int opk;
+    if (op == GNNK_COPY_LHS) { A.a = ol; opk = 0; }
+    else if (op == GNNK_COPY_RHS) { A.a = orr; opk = 0; }
+    else {
+        A.a = ol;
+        A.b = orr;
+        opk = op == GNNK_MUL ? 1 : 2;
+        A.op = op == GNNK_ADD ? M_ADD : (op == GNNK_SUB ? M_SUB : (op == GNNK_MUL ? M_MUL : M_DIV));
+    }
+    A.out.data = out->data;
+    A.out.stride = out->row_stride;
+    A.out.red = 1;
+    A.out.reduce = 0;
+    A.flags = (reduce == GNNK_MEAN ? F_OWN_MEAN : 0) | (reduce == GNNK_MIN ? F_IS_MIN : 0);
+    if (!cmp) return run_spmm_sum(g, g->in, A, geo, dtype_code(out), opk, stream);
+    A.arg_nbr = arg_lhs;
+    A.arg_edge = arg_rhs;
+    A.csr = csr_of(g, g->in);
+    set_geo(A, geo);
+    A.sch = schedule(g->in, geo, true);
+    if (A.sch.n_seg > 0) {
+        A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 12);
+        if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
+    }
+    st = launch_status(launch_spmm(A, dtype_code(out), geo.vec, true, opk, stream), "g-SpMM launch");
+    if (st == GNNK_OK && A.sch.n_hub > 0)
+        st = launch_status(launch_spmm_combine(A, dtype_code(out), geo.vec, true, stream), "g-SpMM combine launch");
+    return st;
+}
+
+gnnk_status gsddmm(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
+                   const gnnk_tensor* rhs, gnnk_target rhs_target, gnnk_tensor* out, hipStream_t stream) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (op < GNNK_COPY_LHS || op > GNNK_DOT) return fail(GNNK_EINVAL, "bad op");
+    if (lhs_target < GNNK_SRC || lhs_target > GNNK_DST || rhs_target < GNNK_SRC || rhs_target > GNNK_DST)
+        return fail(GNNK_EINVAL, "bad target");
+    const bool use_l = op != GNNK_COPY_RHS, use_r = op != GNNK_COPY_LHS;
+    if (use_l != (lhs != nullptr) || use_r != (rhs != nullptr))
+        return fail(GNNK_EINVAL, "lhs is required unless COPY_RHS and rhs unless COPY_LHS (and absent otherwise)");
+    if ((use_l && !tensor_ok(lhs)) || (use_r && !tensor_ok(rhs)) || !tensor_ok(out))
+        return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({lhs, rhs, out})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
+    if ((use_l && lhs->rows != rows_of_target(g, lhs_target)) || (use_r && rhs->rows != rows_of_target(g, rhs_target)) ||
+        out->rows != g->n_edges)
+        return fail(GNNK_EINVAL, "row counts do not match the targets / num_edges");
+    int Hm, Fm;
+    if (!use_r) { Hm = lhs->heads; Fm = lhs->feat; }
+    else if (!use_l) { Hm = rhs->heads; Fm = rhs->feat; }
+    else { Hm = std::max(lhs->heads, rhs->heads); Fm = std::max(lhs->feat, rhs->feat); }
+    if (op == GNNK_DOT) {
+        if (out->heads != Hm || out->feat != 1) return fail(GNNK_EINVAL, "dot output must be (E, %d, 1)", Hm);
+    } else if (out->heads != Hm || out->feat != Fm) {
+        return fail(GNNK_EINVAL, "out must have the message shape (%d, %d)", Hm, Fm);
+    }
+    std::vector<Member> ms;
+    if (use_l) ms.push_back({lhs, K_FULL});
+    if (use_r) ms.push_back({rhs, K_FULL});
+    ms.push_back({out, K_FULL});
+    Geo geo;
+    gnnk_status st = choose_geo(Hm, Fm, ms, {}, geo);
+    if (st != GNNK_OK) return st;
+    if (g->n_edges == 0) return GNNK_OK;
+    EngineArgs A{};
+    size_t k = 0;
+    OperandDev ol = use_l ? operand(lhs, ms[k++].kind, tgt_in(lhs_target)) : OperandDev{};
+    OperandDev orr = use_r ? operand(rhs, ms[k++].kind, tgt_in(rhs_target)) : OperandDev{};
+    st = out_desc(out, ms[k].kind, geo, A.out);
+    if (st != GNNK_OK) return st;
+    int opk;
+    if (op == GNNK_COPY_LHS) { A.a = ol; opk = 0; }
+    else if (op == GNNK_COPY_RHS) { A.a = orr; opk = 0; }
+    else {
+        A.a = ol;
+        A.b = orr;
+        opk = (op == GNNK_MUL || op == GNNK_DOT) ? 1 : 2;
+        A.op = op == GNNK_ADD ? M_ADD : (op == GNNK_SUB ? M_SUB : (op == GNNK_DIV ? M_DIV : M_MUL));
+    }
+    return run_sddmm(g, A, geo, dtype_code(out), opk, stream);
+}
+
+gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                           const gnnk_tensor* rhs, const int32_t* arg_lhs, const int32_t* arg_rhs,
+                           const gnnk_tensor* grad_out, gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs,
+                           hipStream_t stream) {
+    clear_error();
+    (void)arg_lhs;
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (op < GNNK_COPY_LHS || op > GNNK_DIV) return fail(GNNK_EINVAL, "gspmm op must be COPY_LHS..DIV");
+    if (reduce < GNNK_SUM || reduce > GNNK_MIN) return fail(GNNK_EINVAL, "bad reduce");
+    const bool use_l = op != GNNK_COPY_RHS, use_r = op != GNNK_COPY_LHS;
+    const bool cmp = reduce == GNNK_MAX || reduce == GNNK_MIN;
+    if (use_l != (lhs != nullptr) || use_r != (rhs != nullptr))
+        return fail(GNNK_EINVAL, "lhs is required unless COPY_RHS and rhs unless COPY_LHS (and absent otherwise)");
+    if ((grad_lhs && !use_l) || (grad_rhs && !use_r)) return fail(GNNK_EINVAL, "gradient of an unused operand");
+    if ((use_l && !tensor_ok(lhs)) || (use_r && !tensor_ok(rhs)) || !tensor_ok(grad_out) ||
+        (grad_lhs && !tensor_ok(grad_lhs)) || (grad_rhs && !tensor_ok(grad_rhs)))
+        return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({lhs, rhs, grad_out, grad_lhs, grad_rhs})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
+    if ((use_l && lhs->rows != g->n_src) || (use_r && rhs->rows != g->n_edges) || grad_out->rows != g->n_dst)
+        return fail(GNNK_EINVAL, "row counts must be num_src (lhs), num_edges (rhs), num_dst (grad_out)");
+    if (cmp && !arg_rhs) return fail(GNNK_EINVAL, "MAX/MIN backward needs arg_rhs (edge ids)");
+    int Hm, Fm;
+    if (!use_r) { Hm = lhs->heads; Fm = lhs->feat; }
+    else if (!use_l) { Hm = rhs->heads; Fm = rhs->feat; }
+    else { Hm = std::max(lhs->heads, rhs->heads); Fm = std::max(lhs->feat, rhs->feat); }
+    if (grad_out->heads != Hm || grad_out->feat != Fm) return fail(GNNK_EINVAL, "grad_out must have the message shape");
+    if (grad_lhs && (grad_lhs->rows != g->n_src || grad_lhs->heads != lhs->heads || grad_lhs->feat != lhs->feat))
+        return fail(GNNK_EINVAL, "grad_lhs must have lhs's shape");
+    if (grad_rhs && (grad_rhs->rows != g->n_edges || grad_rhs->heads != rhs->heads || grad_rhs->feat != rhs->feat))
+        return fail(GNNK_EINVAL, "grad_rhs must have rhs's shape");
+    const int dt = dtype_code(grad_out);
+    const int32_t scale_flags = (reduce == GNNK_MEAN ? F_SCALE_A_DEG : 0) | (cmp ? F_MASK_A : 0);
+
+    if (grad_lhs && g->n_src > 0) {
+        // Lemma complex_dspmm_dx: a g-SpMM on the reverse graph, message dZ[v] * d phi / d x
+        std::vector<Member> ms{{grad_out, K_FULL}};
+        if (op == GNNK_MUL || op == GNNK_DIV) ms.push_back({rhs, K_FULL});
+        ms.push_back({grad_lhs, K_FULL});
+        Geo geo;
+        gnnk_status st = choose_geo(Hm, Fm, ms, {arg_rhs}, geo);
+        if (st != GNNK_OK) return st;
+        EngineArgs A{};
+        A.a = operand(grad_out, ms[0].kind, T_NBR);
+        int opk = 0;
+        if (op == GNNK_MUL || op == GNNK_DIV) {
+            A.b = operand(rhs, ms[1].kind, T_EDGE);
+            opk = op == GNNK_MUL ? 1 : 2;
+            A.op = op == GNNK_MUL ? M_MUL : M_DIV;
+        }
+        st = out_desc(grad_lhs, ms.back().kind, geo, A.out);
+        if (st != GNNK_OK) return st;
+        A.flags = scale_flags;
+        A.deg = g->in.deg;
+        A.mask_arg = arg_rhs;
+        A.mask_ld = geo.D;
+        st = run_spmm_sum(g, g->out, A, geo, dt, opk, stream);
+        if (st != GNNK_OK) return st;
+    }
+    if (grad_rhs && g->n_edges > 0) {
+        // the lemma on dL/dW of g-SpMM: a g-SDDMM, message dZ[v] * d phi / d w
+        std::vector<Member> ms{{grad_out, K_FULL}};
+        if (op == GNNK_MUL || op == GNNK_DIV) ms.push_back({lhs, K_FULL});
+        if (op == GNNK_DIV) ms.push_back({rhs, K_FULL});
+        ms.push_back({grad_rhs, K_FULL});
+        Geo geo;
+        gnnk_status st = choose_geo(Hm, Fm, ms, {arg_rhs}, geo);
+        if (st != GNNK_OK) return st;
+        EngineArgs A{};
+        A.a = operand(grad_out, ms[0].kind, T_SELF);
+        int opk = 0;
+        if (op == GNNK_MUL) {
+            A.b = operand(lhs, ms[1].kind, T_NBR);
+            opk = 1;
+            A.op = M_MUL;
+        } else if (op == GNNK_DIV) {
+            A.b = operand(lhs, ms[1].kind, T_NBR);
+            A.c = operand(rhs, ms[2].kind, T_EDGE);
+            opk = 2;
+            A.op = M_NEGDIV2;
+        }
+        st = out_desc(grad_rhs, ms.back().kind, geo, A.out);
+        if (st != GNNK_OK) return st;
+        A.flags = scale_flags | (op == GNNK_SUB ? F_NEGATE : 0);
+        A.deg = g->in.deg;
+        A.mask_arg = arg_rhs;
+        A.mask_ld = geo.D;
+        st = run_sddmm(g, A, geo, dt, opk, stream);
+        if (st != GNNK_OK) return st;
+    }
+    return GNNK_OK;
+}
+
+gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
+                            const gnnk_tensor* rhs, gnnk_target rhs_target, const gnnk_tensor* grad_out,
+                            gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs, hipStream_t stream) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (op < GNNK_COPY_LHS || op > GNNK_DOT) return fail(GNNK_EINVAL, "bad op");
+    if (lhs_target < GNNK_SRC || lhs_target > GNNK_DST || rhs_target < GNNK_SRC || rhs_target > GNNK_DST)
+        return fail(GNNK_EINVAL, "bad target");
+    const bool use_l = op != GNNK_COPY_RHS, use_r = op != GNNK_COPY_LHS;
+    const bool binary = use_l && use_r;
+    if (use_l != (lhs != nullptr) || use_r != (rhs != nullptr))
+        return fail(GNNK_EINVAL, "lhs is required unless COPY_RHS and rhs unless COPY_LHS (and absent otherwise)");
+    if ((grad_lhs && !use_l) || (grad_rhs && !use_r)) return fail(GNNK_EINVAL, "gradient of an unused operand");
+    if ((use_l && !tensor_ok(lhs)) || (use_r && !tensor_ok(rhs)) || !tensor_ok(grad_out) ||
+        (grad_lhs && !tensor_ok(grad_lhs)) || (grad_rhs && !tensor_ok(grad_rhs)))
+        return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({lhs, rhs, grad_out, grad_lhs, grad_rhs})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
+    if ((use_l && lhs->rows != rows_of_target(g, lhs_target)) || (use_r && rhs->rows != rows_of_target(g, rhs_target)) ||
+        grad_out->rows != g->n_edges)
+        return fail(GNNK_EINVAL, "row counts do not match the targets / num_edges");
+    int Hm, Fm;
+    if (!use_r) { Hm = lhs->heads; Fm = lhs->feat; }
+    else if (!use_l) { Hm = rhs->heads; Fm = rhs->feat; }
+    else { Hm = std::max(lhs->heads, rhs->heads); Fm = std::max(lhs->feat, rhs->feat); }
+    if (grad_out->heads != Hm || grad_out->feat != (op == GNNK_DOT ? 1 : Fm))
+        return fail(GNNK_EINVAL, "grad_out must have the output shape");
+    if (grad_lhs && (grad_lhs->rows != lhs->rows || grad_lhs->heads != lhs->heads || grad_lhs->feat != lhs->feat))
+        return fail(GNNK_EINVAL, "grad_lhs must have lhs's shape");
+    if (grad_rhs && (grad_rhs->rows != rhs->rows || grad_rhs->heads != rhs->heads || grad_rhs->feat != rhs->feat))
+        return fail(GNNK_EINVAL, "grad_rhs must have rhs's shape");
+    const int dt = dtype_code(grad_out);
+
+    for (int which = 0; which < 2; ++which) {
+        gnnk_tensor* gx = which == 0 ? grad_lhs : grad_rhs;
+        if (!gx || gx->rows == 0) continue;
+        const int tx = which == 0 ? lhs_target : rhs_target;
+        // the other operand enters the derivative of mul / div / dot
+        std::vector<Member> ms{{grad_out, K_FULL}};
+        EngineArgs A{};
+        int opk = 0;
+        int32_t flags = 0;
+        auto tg = [&](int t) { return tx == GNNK_EDGE || tx == GNNK_DST ? tgt_in(t) : tgt_out(t); };
+        const bool muldot = op == GNNK_MUL || op == GNNK_DOT;
+        // operands b and c of the derivative message, with their own targets
+        const gnnk_tensor* bt = nullptr;
+        const gnnk_tensor* ct = nullptr;
+        int b_target = 0, c_target = 0;
+        if (which == 0) {
+            if (binary && (muldot || op == GNNK_DIV)) {
+                bt = rhs; b_target = rhs_target;
+                opk = muldot ? 1 : 2;
+                A.op = muldot ? M_MUL : M_DIV;
+            }
+        } else {
+            if (binary && muldot) {
+                bt = lhs; b_target = lhs_target;
+                opk = 1;
+                A.op = M_MUL;
+            } else if (op == GNNK_DIV) {
+                bt = lhs; b_target = lhs_target;
+                ct = rhs; c_target = rhs_target;
+                opk = 2;
+                A.op = M_NEGDIV2;
+            } else if (op == GNNK_SUB) {
+                flags |= F_NEGATE;
+            }
+        }
+        if (bt) ms.push_back({bt, K_FULL});
+        if (ct) ms.push_back({ct, K_FULL});
+        ms.push_back({gx, K_FULL});
+        Geo geo;
+        gnnk_status st = choose_geo(Hm, Fm, ms, {}, geo);
+        if (st != GNNK_OK) return st;
+        A.a = operand(grad_out, ms[0].kind, tg(GNNK_EDGE));
+        if (bt) A.b = operand(bt, ms[1].kind, tg(b_target));
+        if (ct) A.c = operand(ct, ms[2].kind, tg(c_target));
+        st = out_desc(gx, ms.back().kind, geo, A.out);
+        if (st != GNNK_OK) return st;
+        A.flags = flags;
+        if (tx == GNNK_EDGE) st = run_sddmm(g, A, geo, dt, opk, stream);
+        else st = run_spmm_sum(g, tx == GNNK_SRC ? g->out : g->in, A, geo, dt, opk, stream);
+        if (st != GNNK_OK) return st;
+    }
+    return GNNK_OK;
+}
+
+static gnnk_status softmax_common(gnnk_graph_t g, const gnnk_tensor* a, const gnnk_tensor* b, gnnk_tensor* out,
+                                  bool backward, hipStream_t stream) {
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (!tensor_ok(a) || (b && !tensor_ok(b)) || !tensor_ok(out)) return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({a, b, out})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
+    for (const gnnk_tensor* t : {a, b, (const gnnk_tensor*)out}) {
+        if (!t) continue;
+        if (t->rows != g->n_edges || t->heads != a->heads || t->feat != a->feat)
+            return fail(GNNK_EINVAL, "edge tensors must be (num_edges, H, F) of one shape");
+    }
+    std::vector<Member> ms{{a, K_FULL}, {out, K_FULL}};
+    if (b) ms.push_back({b, K_FULL});
+    Geo geo;
+    gnnk_status st = choose_geo(a->heads, a->feat, ms, {}, geo);
+    if (st != GNNK_OK) return st;
+    if (g->n_edges == 0) return GNNK_OK;
+    EngineArgs A{};
+    A.a = operand(a, K_FULL, T_EDGE);
+    if (b) A.b = operand(b, K_FULL, T_EDGE);
+    A.out.data = out->data;
+    A.out.stride = out->row_stride;
+    A.out.red = 1;
+    A.out.reduce = 0;
+    A.csr = csr_of(g, g->in);
+    set_geo(A, geo);
+    A.sch = schedule(g->in, geo, false);
+    if (A.sch.n_seg > 0) {
+        A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 16);
+        if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
+    }
+    return launch_status(launch_softmax(A, dtype_code(a), geo.vec, backward, stream), "edge softmax launch");
+}
+
+gnnk_status edge_softmax(gnnk_graph_t g, const gnnk_tensor* score, gnnk_tensor* out, hipStream_t stream) {
+    clear_error();
+    return softmax_common(g, score, nullptr, out, false, stream);
+}
+
+gnnk_status edge_softmax_backward(gnnk_graph_t g, const gnnk_tensor* out, const gnnk_tensor* grad_out,
+                                  gnnk_tensor* grad_score, hipStream_t stream) {
+    clear_error();
+    if (!grad_out) return fail(GNNK_EINVAL, "grad_out is NULL");
+    return softmax_common(g, out, grad_out, grad_score, true, stream);
+}
+
+static gnnk_status leaky_common(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* y, float slope,
+                                bool backward, hipStream_t stream) {
+    if (!tensor_ok(x) || (backward && !tensor_ok(dy)) || !tensor_ok(y)) return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({x, dy, y})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
+    if (y->rows != x->rows || y->heads != x->heads || y->feat != x->feat ||
+        (dy && (dy->rows != x->rows || dy->heads != x->heads || dy->feat != x->feat)))
+        return fail(GNNK_EINVAL, "tensors must have one shape");
+    hipError_t e = launch_leaky(x->data, dy ? dy->data : nullptr, y->data, x->rows, x->heads * x->feat,
+                                x->row_stride, dy ? dy->row_stride : 0, y->row_stride, slope, dtype_code(x), backward,
+                                stream);
+    return launch_status(e, "leaky relu launch");
+}
+
+gnnk_status edge_leaky_relu(const gnnk_tensor* x, gnnk_tensor* y, float slope, hipStream_t stream) {
+    clear_error();
+    return leaky_common(x, nullptr, y, slope, false, stream);
+}
+
+gnnk_status edge_leaky_relu_backward(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* dx, float slope,
+                                     hipStream_t stream) {
+    clear_error();
+    if (!dy) return fail(GNNK_EINVAL, "dy is NULL");
+    return leaky_common(x, dy, dx, slope, true, stream);
+}
+
+}  // extern "C"

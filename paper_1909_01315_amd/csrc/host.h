@@ -1,0 +1,64 @@
+// Host-side state of the gnnk library: graph handles, options, errors.
+#pragma once
+
+#include <stdarg.h>
+#include <stdint.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/gnnk.h"
+#include "internal.h"
+
+namespace gnnk {
+
+// One traversal direction: the in-CSR (rows = destinations) or the reverse
+// graph's CSR (rows = sources).
+struct Dir {
+    int64_t n_rows = 0;
+    const void* ptr = nullptr;     // device row offsets (graph ptr type)
+    const int32_t* idx = nullptr;  // device neighbour ids
+    const int32_t* eid = nullptr;  // device edge ids, nullptr = identity
+    int32_t* deg = nullptr;        // device degree per row
+    int32_t* perm = nullptr;       // device rows by descending degree
+    int4* seg = nullptr;           // device segments of hub rows
+    int32_t* hub_off = nullptr;    // device first segment per hub row (n_hub + 1)
+    int64_t n_seg = 0, n_hub = 0, n_nz = 0, max_deg = 0;
+    std::vector<int32_t> sorted_deg;  // host, descending (bin boundaries by binary search)
+    int64_t count_above(int64_t t) const;  // rows with degree > t
+};
+
+}  // namespace gnnk
+
+struct gnnk_graph {
+    int64_t n_src = 0, n_dst = 0, n_edges = 0;
+    int ptr64 = 0;
+    int identity_eids = 1;
+    int64_t seg_edges = 2048;
+    gnnk::Dir in, out;
+    int32_t* flag = nullptr;  // device word for graph_validate
+    size_t ws_used = 0;
+    // scratch for hub-row partials, owned by the handle and grown on demand
+    void* scratch = nullptr;
+    size_t scratch_bytes = 0;
+    std::mutex scratch_mu;
+};
+
+namespace gnnk {
+
+struct Options {
+    int64_t seg_edges = 2048;
+    int64_t no_split = 0;
+    int64_t small_deg = -1;
+};
+Options& options();
+
+gnnk_status fail(gnnk_status st, const char* fmt, ...);
+gnnk_status hip_fail(hipError_t e, const char* what);
+void clear_error();
+
+// scratch of at least `bytes` bytes owned by g (nullptr on failure)
+void* graph_scratch(gnnk_graph* g, size_t bytes);
+
+}  // namespace gnnk

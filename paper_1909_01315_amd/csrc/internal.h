@@ -1,0 +1,134 @@
+// Internal declarations of the gnnk GPU library (host and device side).
+//
+// Geometry of a call.  A message row of D = H * F columns is split into
+// vectors of VEC consecutive columns (VEC divides F, so a vector never spans
+// two heads); NV = D / VEC vectors.  L = lanes per edge (power of two, at most
+// 64, L >= NV unless the row is processed in chunks of 64 vectors), and a
+// 64-lane wavefront holds G = 64 / L lane groups, each working on one edge at
+// a time.
+//
+// Schedule of a row traversal (an in-CSR or the reverse graph's CSR).  Rows
+// are kept sorted by descending degree (perm).  A call splits them into:
+//   hub rows   degree > seg_edges: cut into segments of seg_edges edges, one
+//              wavefront per segment, partial results combined afterwards in
+//              segment order;
+//   big rows   one wavefront per row, the G lane groups striding its edges;
+//   small rows degree <= small_deg: each lane group owns one row;
+//   empty rows degree 0: filled with the empty-reduction value.
+// Every role sits in one launch; block b takes the roles of its wavefronts in
+// that order, so the longest work items start first.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace gnnk {
+
+enum OperandTarget : int32_t { T_NBR = 0, T_EDGE = 1, T_SELF = 2 };
+
+// message kinds (fused op of up to three operands a, b, c)
+enum MsgOp : int32_t {
+    M_COPY_A = 0,   // a
+    M_ADD = 1,      // a + b
+    M_SUB = 2,      // a - b
+    M_MUL = 3,      // a * b
+    M_DIV = 4,      // a / b
+    M_NEGDIV2 = 5,  // -(a * b) / (c * c)   (gradient of a division w.r.t. its divisor)
+    M_RSUB = 6,     // b - a
+};
+
+struct OperandDev {
+    const void* data;   // nullptr when absent
+    int64_t stride;     // row stride, elements
+    int32_t hmul;       // element offset per head for a broadcast-over-feature operand (1 or 0)
+    int32_t full;       // 1: operand has the message feature extent (per-lane vector load)
+    int32_t target;     // OperandTarget
+    int32_t pad;
+};
+
+struct OutDev {
+    void* data;
+    int64_t stride;
+    int32_t reduce;     // 1: the output is summed over broadcast positions (operand of shape (H,1) or (1,1))
+    int32_t red;        // lanes summed into one output element (after each lane sums its VEC columns)
+    int32_t per_head;   // with reduce: 1 -> one value per head, 0 -> one value per row
+    int32_t pad;
+};
+
+struct CsrDev {
+    const void* ptr;        // row offsets (int32 or int64)
+    const int32_t* idx;     // neighbour of each position
+    const int32_t* eid;     // edge id of each position, nullptr = identity
+    const int32_t* perm;    // rows by descending degree
+    const int4* seg;        // {row, begin, end, hub index} per segment of a hub row
+    const int32_t* hub_off; // first segment of each hub row (hub rows = perm[0, n_hub)), n_hub + 1 entries
+    int32_t ptr64;
+    int32_t pad;
+};
+
+struct SchedDev {
+    int32_t n_seg;          // waves of segments
+    int32_t n_hub;          // hub rows (perm[0, n_hub))
+    int32_t n_big;          // rows with one wavefront each end at perm[n_big)
+    int32_t n_nz;           // non-empty rows end at perm[n_nz)
+    int32_t n_rows;
+    int32_t w_big_end;      // wave index where big rows end
+    int32_t w_small_end;    // wave index where small rows end
+    int32_t w_total;        // total waves
+    int32_t fill_rows_per_group;
+    int32_t pad;
+};
+
+struct GeomDev {
+    int32_t F;       // feature extent of the message (canonical)
+    int32_t NV;      // vectors per message row
+    int32_t L;       // lanes per edge
+    int32_t log2L;
+    int32_t G;       // lane groups per wavefront
+    int32_t nchunk;  // chunks of 64 vectors (NV > 64)
+};
+
+// flags of a row-engine call
+enum : int32_t {
+    F_MASK_A = 1,       // a is zeroed unless arg[row of a][col] == edge id
+    F_SCALE_A_DEG = 2,  // a is divided by the degree of a's row (mean backward)
+    F_OWN_MEAN = 4,     // the reduced value is divided by the row's own degree
+    F_NEGATE = 8,       // the output is negated
+    F_IS_MIN = 16,      // max/min reductions: minimum
+    F_PARTIAL = 32,     // internal: write hub-row partials
+};
+
+struct EngineArgs {
+    CsrDev csr;
+    SchedDev sch;
+    GeomDev geo;
+    OperandDev a, b, c;
+    OutDev out;
+    int32_t* arg_nbr;        // max/min: neighbour id of the winner (nullable)
+    int32_t* arg_edge;       // max/min: edge id of the winner (nullable)
+    const int32_t* mask_arg; // F_MASK_A: edge-id array (rows of a's target, D columns)
+    const int32_t* deg;      // F_SCALE_A_DEG: degree per row of a's target
+    void* partial;           // hub-row partials (fp64 sums, or fp32 value + int32 edge + int32 nbr)
+    int64_t partial_stride;  // elements per segment row (D)
+    int32_t op;              // MsgOp
+    int32_t flags;
+    int64_t mask_ld;         // row stride of mask_arg
+};
+
+// ----- host-side launchers (engine.hip) -----
+enum class Family { SPMM_SUM, SPMM_MAXMIN, SDDMM, SOFTMAX, SOFTMAX_BWD };
+
+// dtype: 0 fp32, 1 bf16; opk: 0 copy-a, 1 mul-ab, 2 generic
+hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, hipStream_t s);
+hipError_t launch_spmm_combine(const EngineArgs& a, int dtype, int vec, bool maxmin, hipStream_t s);
+hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, hipStream_t s);
+hipError_t launch_softmax(const EngineArgs& a, int dtype, int vec, bool backward, hipStream_t s);
+hipError_t launch_leaky(const void* x, const void* dy, void* y, int64_t rows, int32_t cols, int64_t sx,
+                        int64_t sdy, int64_t sy, float slope, int dtype, bool backward, hipStream_t s);
+hipError_t launch_validate(const int32_t* idx, int64_t n, int64_t bound, int32_t* flag, hipStream_t s);
+hipError_t launch_validate_ptr(const void* ptr, int ptr64, int64_t n_rows, int64_t n_edges, int32_t* flag,
+                               hipStream_t s);
+hipError_t launch_iota(int32_t* out, int64_t n, hipStream_t s);
+hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int64_t n, hipStream_t s);
+
+}  // namespace gnnk

@@ -1,0 +1,64 @@
+"""The C-ABI library: it loads, exports every entry point include/gnnk.h
+declares, and rejects bad arguments on the host before touching the GPU
+(CPU only: no call here launches work)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_1909_01315_amd import gnnk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gnnk.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:gnnk_status|const char\s*\*)\s+(\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(gnnk.LIB_PATH):
+        pytest.fail("libgnnk.so is not built: run __graft_entry__.build()")
+    return gnnk.load()
+
+
+def test_header_declares_the_operator_set():
+    names = declared_functions()
+    for n in ("graph_create_csr", "graph_create_coo", "gspmm", "gsddmm", "edge_softmax", "gspmm_backward",
+              "gsddmm_backward", "edge_softmax_backward", "edge_leaky_relu", "edge_leaky_relu_backward",
+              "graph_validate", "graph_destroy", "gnnk_last_error"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    raw = ctypes.CDLL(gnnk.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(raw, n)]
+    assert not missing, f"not exported: {missing}"
+    assert set(declared_functions()) == set(gnnk.SYMBOLS), "binding and header list the same entry points"
+
+
+def test_host_side_errors(lib):
+    # none of these reach the GPU: the arguments are rejected first
+    assert lib.gspmm(None, 4, 0, None, None, None, None, None, None) == gnnk.EINVAL
+    assert b"NULL graph" in lib.gnnk_last_error()
+    assert lib.gsddmm(None, 6, None, 0, None, 2, None, None) == gnnk.EINVAL
+    assert lib.edge_softmax(None, None, None, None) == gnnk.EINVAL
+    assert lib.graph_destroy(None) == gnnk.EINVAL
+    assert lib.graph_validate(None, None) == gnnk.EINVAL
+    assert lib.gnnk_set_option(b"no_such_option", 1) == gnnk.EINVAL
+    assert b"unknown option" in lib.gnnk_last_error()
+    assert lib.gnnk_set_option(b"seg_edges", 1) == gnnk.EINVAL
+    assert lib.edge_leaky_relu(None, None, ctypes.c_float(0.2), None) == gnnk.EINVAL
+
+
+def test_workspace_bound_grows_with_size(lib):
+    b1, b2 = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.graph_workspace_bytes(1000, 1000, 10000, gnnk.I32, ctypes.byref(b1)) == gnnk.OK
+    assert lib.graph_workspace_bytes(1000, 1000, 20000, gnnk.I64, ctypes.byref(b2)) == gnnk.OK
+    assert b2.value > b1.value >= 10000 * 4 * 4
+    assert lib.graph_workspace_bytes(-1, 10, 10, gnnk.I32, ctypes.byref(b1)) == gnnk.EINVAL
+    assert lib.graph_workspace_bytes(10, 10, 10, 7, ctypes.byref(b1)) == gnnk.EINVAL
