@@ -1,0 +1,405 @@
+// Device-side building blocks shared by the gnnk kernels (gfx950, wave64):
+// vector IO of fp32/bf16 rows, cross-lane reductions, operand fetch and the
+// message arithmetic, edge batches, and the row output.
+//
+// Conventions that keep every kernel deterministic and branch-free in its
+// edge loop: a lane holds VEC consecutive columns of the message row; edge
+// batches read clamped (always in-bounds) positions and drop the extra slots
+// with selects; inactive lanes read column 0 and never write.
+#pragma once
+
+#include "internal.h"
+
+namespace gnnk {
+
+constexpr int WAVE = 64;
+constexpr int WPB = 4;  // wavefronts per block
+constexpr int UNR = 4;  // edges in flight per lane group
+
+typedef uint16_t bf16_t;
+
+__device__ __forceinline__ int64_t row_ptr(const CsrDev& c, int64_t r) {
+    return c.ptr64 ? reinterpret_cast<const int64_t*>(c.ptr)[r] : (int64_t) reinterpret_cast<const int32_t*>(c.ptr)[r];
+}
+
+// ---------------------------------------------------------------------------
+// element IO: VEC consecutive elements <-> float registers
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ uint32_t f2bf(float f) {
+    uint32_t b = __float_as_uint(f);
+    b += 0x7FFFu + ((b >> 16) & 1u);  // round to nearest, ties to even (finite inputs)
+    return b >> 16;
+}
+
+template <typename T, int VEC>
+struct IO;
+
+template <int VEC>
+struct IO<float, VEC> {
+    static __device__ __forceinline__ void load(const float* p, float* v) {
+        if constexpr (VEC == 4) {
+            float4 x = *reinterpret_cast<const float4*>(p);
+            v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+        } else if constexpr (VEC == 2) {
+            float2 x = *reinterpret_cast<const float2*>(p);
+            v[0] = x.x; v[1] = x.y;
+        } else {
+            v[0] = *p;
+        }
+    }
+    static __device__ __forceinline__ float load1(const float* p) { return *p; }
+    static __device__ __forceinline__ void store(float* p, const float* v) {
+        if constexpr (VEC == 4) {
+            *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+        } else if constexpr (VEC == 2) {
+            *reinterpret_cast<float2*>(p) = make_float2(v[0], v[1]);
+        } else {
+            *p = v[0];
+        }
+    }
+    static __device__ __forceinline__ void store1(float* p, float v) { *p = v; }
+};
+
+template <int VEC>
+struct IO<bf16_t, VEC> {
+    static __device__ __forceinline__ void load(const bf16_t* p, float* v) {
+        if constexpr (VEC == 8) {
+            uint4 x = *reinterpret_cast<const uint4*>(p);
+            v[0] = bf_lo(x.x); v[1] = bf_hi(x.x); v[2] = bf_lo(x.y); v[3] = bf_hi(x.y);
+            v[4] = bf_lo(x.z); v[5] = bf_hi(x.z); v[6] = bf_lo(x.w); v[7] = bf_hi(x.w);
+        } else if constexpr (VEC == 4) {
+            uint2 x = *reinterpret_cast<const uint2*>(p);
+            v[0] = bf_lo(x.x); v[1] = bf_hi(x.x); v[2] = bf_lo(x.y); v[3] = bf_hi(x.y);
+        } else if constexpr (VEC == 2) {
+            uint32_t x = *reinterpret_cast<const uint32_t*>(p);
+            v[0] = bf_lo(x); v[1] = bf_hi(x);
+        } else {
+            v[0] = bf_lo(*p);
+        }
+    }
+    static __device__ __forceinline__ float load1(const bf16_t* p) { return bf_lo(*p); }
+    static __device__ __forceinline__ void store(bf16_t* p, const float* v) {
+        if constexpr (VEC == 8) {
+            uint4 x;
+            x.x = f2bf(v[0]) | (f2bf(v[1]) << 16); x.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+            x.z = f2bf(v[4]) | (f2bf(v[5]) << 16); x.w = f2bf(v[6]) | (f2bf(v[7]) << 16);
+            *reinterpret_cast<uint4*>(p) = x;
+        } else if constexpr (VEC == 4) {
+            uint2 x;
+            x.x = f2bf(v[0]) | (f2bf(v[1]) << 16); x.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+            *reinterpret_cast<uint2*>(p) = x;
+        } else if constexpr (VEC == 2) {
+            *reinterpret_cast<uint32_t*>(p) = f2bf(v[0]) | (f2bf(v[1]) << 16);
+        } else {
+            *p = (bf16_t)f2bf(v[0]);
+        }
+    }
+    static __device__ __forceinline__ void store1(bf16_t* p, float v) { *p = (bf16_t)f2bf(v); }
+};
+
+template <int VEC>
+__device__ __forceinline__ void load_i32(const int32_t* p, int32_t* v) {
+    if constexpr (VEC >= 4 && VEC % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+            int4 x = reinterpret_cast<const int4*>(p)[q];
+            v[4 * q] = x.x; v[4 * q + 1] = x.y; v[4 * q + 2] = x.z; v[4 * q + 3] = x.w;
+        }
+    } else if constexpr (VEC == 2) {
+        int2 x = *reinterpret_cast<const int2*>(p);
+        v[0] = x.x; v[1] = x.y;
+    } else {
+        v[0] = *p;
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_i32(int32_t* p, const int32_t* v) {
+    if constexpr (VEC >= 4 && VEC % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q)
+            reinterpret_cast<int4*>(p)[q] = make_int4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    } else if constexpr (VEC == 2) {
+        *reinterpret_cast<int2*>(p) = make_int2(v[0], v[1]);
+    } else {
+        *p = v[0];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// cross-lane helpers (64-bit values move as two 32-bit shuffles)
+
+__device__ __forceinline__ double shfl_xor_d(double x, int m) {
+    int2 v = *reinterpret_cast<int2*>(&x);
+    v.x = __shfl_xor(v.x, m, WAVE);
+    v.y = __shfl_xor(v.y, m, WAVE);
+    return *reinterpret_cast<double*>(&v);
+}
+
+__device__ __forceinline__ double shfl_d(double x, int src) {
+    int2 v = *reinterpret_cast<int2*>(&x);
+    v.x = __shfl(v.x, src, WAVE);
+    v.y = __shfl(v.y, src, WAVE);
+    return *reinterpret_cast<double*>(&v);
+}
+
+// Sum over aligned runs of `red` consecutive lanes starting at multiples of
+// `red` within each lane group; the first lane of a run gets the total (the
+// other lanes hold partial sums).  Every lane must call it.
+__device__ __forceinline__ double seg_sum(double v, int lane_in_group, int red) {
+    const int pos = lane_in_group % red;
+    const int lane = __lane_id();
+    for (int s = 1; s < red; s <<= 1) {
+        double o = shfl_d(v, lane + s < WAVE ? lane + s : lane);
+        v += ((pos & (2 * s - 1)) == 0 && pos + s < red) ? o : 0.0;
+    }
+    return v;
+}
+
+// ---------------------------------------------------------------------------
+// operands and messages
+
+__device__ __forceinline__ int32_t row_of(int32_t target, int32_t nb, int32_t ed, int32_t self) {
+    return target == T_NBR ? nb : (target == T_EDGE ? ed : self);
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void load_operand(const OperandDev& o, int32_t row, int col0, int h, float* v) {
+    const T* base = reinterpret_cast<const T*>(o.data) + (int64_t)row * o.stride;
+    if (o.full) {
+        IO<T, VEC>::load(base + col0, v);
+    } else {
+        const float x = IO<T, VEC>::load1(base + h * o.hmul);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = x;
+    }
+}
+
+// EXT: extra treatment of operand a in backward passes
+enum : int { EXT_NONE = 0, EXT_SCALE = 1 /* a / deg(row of a) */, EXT_MASK = 2 /* a where arg == edge */ };
+
+// Raw operand values of one edge for this lane's VEC columns (loaded first,
+// combined after the loads of a whole batch are in flight).
+template <int VEC>
+struct Raw {
+    float a[VEC];
+    float b[VEC];
+    float c[VEC];
+    int32_t k[VEC];
+    int32_t dg;
+};
+
+// OPK: 0 message = a; 1 message = a * b; 2 any MsgOp (runtime)
+template <typename T, int VEC, int OPK, int EXT>
+__device__ __forceinline__ void fetch(const EngineArgs& A, int32_t nb, int32_t ed, int32_t self, int col0, int h,
+                                      Raw<VEC>& r) {
+    const int32_t ar = row_of(A.a.target, nb, ed, self);
+    load_operand<T, VEC>(A.a, ar, col0, h, r.a);
+    if constexpr (OPK >= 1) load_operand<T, VEC>(A.b, row_of(A.b.target, nb, ed, self), col0, h, r.b);
+    if constexpr (OPK == 2) {
+        if (A.op == M_NEGDIV2) load_operand<T, VEC>(A.c, row_of(A.c.target, nb, ed, self), col0, h, r.c);
+    }
+    if constexpr (EXT == EXT_SCALE) r.dg = A.deg[ar];
+    if constexpr (EXT == EXT_MASK) load_i32<VEC>(A.mask_arg + (int64_t)ar * A.mask_ld + col0, r.k);
+}
+
+// message in fp64 (sums and g-SDDMM); single operations are exact in fp64
+// before the final rounding
+template <int VEC, int OPK, int EXT>
+__device__ __forceinline__ void combine_f64(const EngineArgs& A, const Raw<VEC>& r, int32_t ed, double* m) {
+    double ad[VEC];
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) ad[i] = r.a[i];
+    if constexpr (EXT == EXT_SCALE) {
+        const double inv = 1.0 / (double)r.dg;  // one division per edge, not per column
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) ad[i] = ad[i] * inv;
+    }
+    if constexpr (EXT == EXT_MASK) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) ad[i] = (r.k[i] == ed) ? ad[i] : 0.0;
+    }
+    if constexpr (OPK == 0) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) m[i] = ad[i];
+    } else if constexpr (OPK == 1) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) m[i] = ad[i] * (double)r.b[i];
+    } else {
+        switch (A.op) {
+            case M_ADD:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = ad[i] + (double)r.b[i];
+                break;
+            case M_SUB:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = ad[i] - (double)r.b[i];
+                break;
+            case M_RSUB:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = (double)r.b[i] - ad[i];
+                break;
+            case M_MUL:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = ad[i] * (double)r.b[i];
+                break;
+            case M_DIV:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = ad[i] / (double)r.b[i];
+                break;
+            case M_NEGDIV2:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = -ad[i] * (double)r.b[i] / ((double)r.c[i] * (double)r.c[i]);
+                break;
+            default:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = ad[i];
+        }
+    }
+}
+
+// message for max/min: one fp32 operation, as a message tensor would hold it
+template <int VEC, int OPK>
+__device__ __forceinline__ void combine_f32(const EngineArgs& A, const Raw<VEC>& r, float* m) {
+    if constexpr (OPK == 0) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) m[i] = r.a[i];
+    } else {
+        const int op = OPK == 1 ? (int)M_MUL : A.op;
+        switch (op) {
+            case M_ADD:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = r.a[i] + r.b[i];
+                break;
+            case M_SUB:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = r.a[i] - r.b[i];
+                break;
+            case M_MUL:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = r.a[i] * r.b[i];
+                break;
+            case M_DIV:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = r.a[i] / r.b[i];
+                break;
+            default:
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) m[i] = r.a[i];
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// edge batches: positions p0 + u * stride, u < UNR.  Slots past the row end
+// read the row's first position (always in bounds); ok[] drops them later.
+
+__device__ __forceinline__ void batch_ids(const CsrDev& C, int64_t b, int64_t e, int64_t p0, int64_t stride,
+                                          bool* ok, int32_t* nb, int32_t* ed) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        const int64_t p = p0 + (int64_t)u * stride;
+        ok[u] = p < e;
+        const int64_t pc = ok[u] ? p : b;
+        nb[u] = C.idx[pc];
+        ed[u] = C.eid ? C.eid[pc] : (int32_t)pc;
+    }
+}
+
+// candidate (m, e) replaces (best, be): strictly better, or equal with a
+// smaller edge id, or nothing recorded yet.  Bitwise operators keep it
+// branch-free.
+__device__ __forceinline__ bool better(float m, int32_t e, float best, int32_t be, bool is_min) {
+    const bool strict = is_min ? (m < best) : (m > best);
+    const bool tie = (m == best) & (e < be);
+    return (be < 0) | strict | tie;
+}
+
+// ---------------------------------------------------------------------------
+// output of one reduced row (sums)
+
+template <typename T, int VEC>
+__device__ __forceinline__ void write_sum_row(const EngineArgs& A, int64_t row, bool active, int lig, int col0,
+                                              int h, double* acc, int64_t deg, bool write_lane) {
+    if (A.flags & F_OWN_MEAN) {
+        const double d = deg > 0 ? (double)deg : 1.0;
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc[i] = acc[i] / d;
+    }
+    if (A.flags & F_NEGATE) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc[i] = -acc[i];
+    }
+    if (!A.out.reduce) {
+        if (active && write_lane && row >= 0) {
+            float v[VEC];
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[i] = (float)acc[i];
+            IO<T, VEC>::store(reinterpret_cast<T*>(A.out.data) + row * A.out.stride + col0, v);
+        }
+    } else {
+        double s = 0.0;
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) s += acc[i];
+        s = seg_sum(active ? s : 0.0, lig, A.out.red);
+        if (active && write_lane && row >= 0 && (lig % A.out.red) == 0) {
+            const int64_t o = A.out.per_head ? h : 0;
+            IO<T, VEC>::store1(reinterpret_cast<T*>(A.out.data) + row * A.out.stride + o, (float)s);
+        }
+    }
+}
+
+// lane-group geometry of one wavefront
+struct Lanes {
+    int g;    // lane group
+    int lig;  // lane in group
+};
+
+__device__ __forceinline__ Lanes lanes_of(const GeomDev& geo) {
+    const int lane = threadIdx.x & (WAVE - 1);
+    return Lanes{lane >> geo.log2L, lane & (geo.L - 1)};
+}
+
+__device__ __forceinline__ int wave_id() { return blockIdx.x * WPB + (threadIdx.x >> 6); }
+
+// ---------------------------------------------------------------------------
+// template dispatch of the launchers
+
+#define GNNK_VEC_DISPATCH_F32(VEC_, ...)                      \
+    switch (VEC_) {                                           \
+        case 4: { constexpr int V = 4; __VA_ARGS__; } break;  \
+        case 2: { constexpr int V = 2; __VA_ARGS__; } break;  \
+        default: { constexpr int V = 1; __VA_ARGS__; } break; \
+    }
+
+#define GNNK_VEC_DISPATCH_BF16(VEC_, ...)                     \
+    switch (VEC_) {                                           \
+        case 8: { constexpr int V = 8; __VA_ARGS__; } break;  \
+        case 4: { constexpr int V = 4; __VA_ARGS__; } break;  \
+        case 2: { constexpr int V = 2; __VA_ARGS__; } break;  \
+        default: { constexpr int V = 1; __VA_ARGS__; } break; \
+    }
+
+#define GNNK_OPK_DISPATCH(OPK_, ...)                          \
+    switch (OPK_) {                                           \
+        case 0: { constexpr int K = 0; __VA_ARGS__; } break;  \
+        case 1: { constexpr int K = 1; __VA_ARGS__; } break;  \
+        default: { constexpr int K = 2; __VA_ARGS__; } break; \
+    }
+
+#define GNNK_EXT_DISPATCH(EXT_, ...)                                  \
+    switch (EXT_) {                                                   \
+        case EXT_SCALE: { constexpr int X = EXT_SCALE; __VA_ARGS__; } break; \
+        case EXT_MASK: { constexpr int X = EXT_MASK; __VA_ARGS__; } break;   \
+        default: { constexpr int X = EXT_NONE; __VA_ARGS__; } break;         \
+    }
+
+inline int ext_of(int32_t flags) {
+    return (flags & F_MASK_A) ? EXT_MASK : ((flags & F_SCALE_A_DEG) ? EXT_SCALE : EXT_NONE);
+}
+
+inline unsigned blocks_for_waves(int64_t waves) { return (unsigned)((waves + WPB - 1) / WPB); }
+
+}  // namespace gnnk

@@ -95,7 +95,6 @@ enum : int32_t {
     F_OWN_MEAN = 4,     // the reduced value is divided by the row's own degree
     F_NEGATE = 8,       // the output is negated
     F_IS_MIN = 16,      // max/min reductions: minimum
-    F_PARTIAL = 32,     // internal: write hub-row partials
 };
 
 struct EngineArgs {
@@ -115,9 +114,7 @@ struct EngineArgs {
     int64_t mask_ld;         // row stride of mask_arg
 };
 
-// ----- host-side launchers (engine.hip) -----
-enum class Family { SPMM_SUM, SPMM_MAXMIN, SDDMM, SOFTMAX, SOFTMAX_BWD };
-
+// ----- host-side launchers (spmm.hip, sddmm.hip, softmax.hip, misc.hip) -----
 // dtype: 0 fp32, 1 bf16; opk: 0 copy-a, 1 mul-ab, 2 generic
 hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, hipStream_t s);
 hipError_t launch_spmm_combine(const EngineArgs& a, int dtype, int vec, bool maxmin, hipStream_t s);

@@ -1,0 +1,116 @@
+// Elementwise and structural kernels: leaky ReLU and its backward, index
+// validation, and small helpers of the graph handle.
+#include "device.h"
+
+namespace gnnk {
+
+static inline unsigned grid_1d(int64_t n) {
+    int64_t b = (n + 255) / 256;
+    if (b > 65536) b = 65536;
+    return (unsigned)(b > 0 ? b : 1);
+}
+
+template <typename T, bool BWD>
+__global__ void leaky_kernel(const T* x, const T* dy, T* y, int64_t rows, int32_t cols, int64_t sx, int64_t sdy,
+                             int64_t sy, float slope) {
+    const int64_t n = rows * (int64_t)cols;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int64_t r = i / cols, c = i - r * cols;
+        float xv = IO<T, 1>::load1(x + r * sx + c);
+        float out;
+        if (BWD) {
+            float d = IO<T, 1>::load1(dy + r * sdy + c);
+            out = xv > 0.0f ? d : slope * d;
+        } else {
+            out = xv > 0.0f ? xv : slope * xv;
+        }
+        IO<T, 1>::store1(y + r * sy + c, out);
+    }
+}
+
+__global__ void validate_kernel(const int32_t* idx, int64_t n, int64_t bound, int32_t* flag) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        int32_t v = idx[i];
+        if (v < 0 || v >= bound) atomicOr(flag, 1);
+    }
+}
+
+template <typename P>
+__global__ void validate_ptr_kernel(const P* ptr, int64_t n_rows, int64_t n_edges, int32_t* flag) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i <= n_rows;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t v = ptr[i];
+        bool bad = v < 0 || v > n_edges || (i == 0 && v != 0) || (i == n_rows && v != n_edges) ||
+                   (i < n_rows && ptr[i + 1] < v);
+        if (bad) atomicOr(flag, 2);
+    }
+}
+
+__global__ void iota_kernel(int32_t* out, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        out[i] = (int32_t)i;
+}
+
+__global__ void copy_ptr_kernel(const void* src, int src64, void* dst, int dst64, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        int64_t v = src64 ? reinterpret_cast<const int64_t*>(src)[i] : reinterpret_cast<const int32_t*>(src)[i];
+        if (dst64) reinterpret_cast<int64_t*>(dst)[i] = v;
+        else reinterpret_cast<int32_t*>(dst)[i] = (int32_t)v;
+    }
+}
+
+
+hipError_t launch_leaky(const void* x, const void* dy, void* y, int64_t rows, int32_t cols, int64_t sx,
+                        int64_t sdy, int64_t sy, float slope, int dtype, bool backward, hipStream_t s) {
+    int64_t n = rows * (int64_t)cols;
+    if (n <= 0) return hipSuccess;
+    dim3 grid(grid_1d(n)), block(256);
+    if (dtype == 0) {
+        if (backward)
+            hipLaunchKernelGGL((leaky_kernel<float, true>), grid, block, 0, s, (const float*)x, (const float*)dy,
+                               (float*)y, rows, cols, sx, sdy, sy, slope);
+        else
+            hipLaunchKernelGGL((leaky_kernel<float, false>), grid, block, 0, s, (const float*)x, (const float*)dy,
+                               (float*)y, rows, cols, sx, sdy, sy, slope);
+    } else {
+        if (backward)
+            hipLaunchKernelGGL((leaky_kernel<bf16_t, true>), grid, block, 0, s, (const bf16_t*)x,
+                               (const bf16_t*)dy, (bf16_t*)y, rows, cols, sx, sdy, sy, slope);
+        else
+            hipLaunchKernelGGL((leaky_kernel<bf16_t, false>), grid, block, 0, s, (const bf16_t*)x,
+                               (const bf16_t*)dy, (bf16_t*)y, rows, cols, sx, sdy, sy, slope);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_validate(const int32_t* idx, int64_t n, int64_t bound, int32_t* flag, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(validate_kernel, dim3(grid_1d(n)), dim3(256), 0, s, idx, n, bound, flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_validate_ptr(const void* ptr, int ptr64, int64_t n_rows, int64_t n_edges, int32_t* flag,
+                               hipStream_t s) {
+    dim3 grid(grid_1d(n_rows + 1)), block(256);
+    if (ptr64)
+        hipLaunchKernelGGL((validate_ptr_kernel<int64_t>), grid, block, 0, s, (const int64_t*)ptr, n_rows, n_edges,
+                           flag);
+    else
+        hipLaunchKernelGGL((validate_ptr_kernel<int32_t>), grid, block, 0, s, (const int32_t*)ptr, n_rows, n_edges,
+                           flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_iota(int32_t* out, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(iota_kernel, dim3(grid_1d(n)), dim3(256), 0, s, out, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(copy_ptr_kernel, dim3(grid_1d(n)), dim3(256), 0, s, src, src64, dst, dst64, n);
+    return hipGetLastError();
+}
+
+}  // namespace gnnk

@@ -1,0 +1,206 @@
+// Edge softmax over the in-edges of each destination, per column (the
+// attention normalisation applied to the per-edge scores of Appendix D), and
+// its backward.  Forward: max, then the sum of exp(s - max) in fp64, then
+// a = exp(s - max) / sum.  Backward: S = sum of a * g in fp64, then
+// ds = a * (g - S).  Rows use the degree-sorted schedule; hub rows leave
+// per-segment (max, sum) or S partials and a second launch combines them in
+// segment order and writes the segment's edges.
+#include "device.h"
+
+namespace gnnk {
+
+template <typename T, int VEC>
+__device__ __forceinline__ void ld_edge(const OperandDev& o, int64_t ed, int col0, float* v) {
+    IO<T, VEC>::load(reinterpret_cast<const T*>(o.data) + ed * o.stride + col0, v);
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void softmax_pass_max(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
+                                                 int col0, float* mx) {
+    for (int64_t p = b + start; p < e; p += stride) {
+        const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
+        float s[VEC];
+        ld_edge<T, VEC>(A.a, ed, col0, s);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], s[i]);
+    }
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void softmax_pass_sum(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
+                                                 int col0, const float* mx, double* sum, bool backward) {
+    for (int64_t p = b + start; p < e; p += stride) {
+        const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
+        float s[VEC];
+        ld_edge<T, VEC>(A.a, ed, col0, s);
+        if (backward) {
+            float gg[VEC];
+            ld_edge<T, VEC>(A.b, ed, col0, gg);
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) sum[i] += (double)s[i] * (double)gg[i];
+        } else {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) sum[i] += (double)expf(s[i] - mx[i]);
+        }
+    }
+}
+
+template <typename T, int VEC>
+__device__ __forceinline__ void softmax_pass_write(const EngineArgs& A, int64_t b, int64_t e, int start,
+                                                   int stride, int col0, bool active, const float* mx,
+                                                   const double* sum, bool backward) {
+    for (int64_t p = b + start; p < e; p += stride) {
+        const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
+        float s[VEC], v[VEC];
+        ld_edge<T, VEC>(A.a, ed, col0, s);
+        if (backward) {
+            float gg[VEC];
+            ld_edge<T, VEC>(A.b, ed, col0, gg);
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[i] = (float)((double)s[i] * ((double)gg[i] - sum[i]));
+        } else {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[i] = (float)((double)expf(s[i] - mx[i]) / sum[i]);
+        }
+        if (active) IO<T, VEC>::store(reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0, v);
+    }
+}
+
+template <typename T, int VEC, bool BWD>
+__global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
+    const int w = wave_id();
+    if (w >= A.sch.w_small_end) return;
+    const GeomDev& geo = A.geo;
+    const Lanes ln = lanes_of(geo);
+    const int g = ln.g, lig = ln.lig;
+    const int64_t D = (int64_t)geo.NV * VEC;
+    bool coop = w < A.sch.w_big_end;
+    int64_t r = -1, b = 0, e = 0;
+    int slot = -1;
+    if (coop) {
+        if (w < A.sch.n_seg) {
+            int4 s = A.csr.seg[w];
+            r = s.x; b = s.y; e = s.z; slot = w;
+        } else {
+            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
+            b = row_ptr(A.csr, r);
+            e = row_ptr(A.csr, r + 1);
+        }
+    } else {
+        const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + g;
+        if (k < A.sch.n_nz) {
+            r = A.csr.perm[k];
+            b = row_ptr(A.csr, r);
+            e = row_ptr(A.csr, r + 1);
+        }
+    }
+    const int start = coop ? g : 0, stride = coop ? geo.G : 1;
+    for (int ch = 0; ch < geo.nchunk; ++ch) {
+        const int j = ch * geo.L + lig;
+        const bool active = j < geo.NV && r >= 0;
+        const int col0 = j < geo.NV ? j * VEC : 0;
+        float mx[VEC];
+        double sum[VEC];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) { mx[i] = -INFINITY; sum[i] = 0.0; }
+        if (!BWD) {
+            softmax_pass_max<T, VEC>(A, b, e, start, stride, col0, mx);
+            if (coop)
+                for (int s = geo.L; s < WAVE; s <<= 1)
+#pragma unroll
+                    for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], __shfl_xor(mx[i], s, WAVE));
+        }
+        softmax_pass_sum<T, VEC>(A, b, e, start, stride, col0, mx, sum, BWD);
+        if (coop)
+            for (int s = geo.L; s < WAVE; s <<= 1)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) sum[i] += shfl_xor_d(sum[i], s);
+        if (slot >= 0) {
+            if (g == 0 && active) {
+                double* P = reinterpret_cast<double*>(A.partial) + (int64_t)slot * 2 * D;
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) {
+                    P[col0 + i] = (double)mx[i];
+                    P[D + col0 + i] = sum[i];
+                }
+            }
+        } else {
+            softmax_pass_write<T, VEC>(A, b, e, start, stride, col0, active, mx, sum, BWD);
+        }
+    }
+}
+
+// hub rows: combine the segment partials of the row, then write this segment
+template <typename T, int VEC, bool BWD>
+__global__ __launch_bounds__(256) void softmax_finish_kernel(EngineArgs A) {
+    const int w = wave_id();
+    if (w >= A.sch.n_seg) return;
+    const GeomDev& geo = A.geo;
+    const Lanes ln = lanes_of(geo);
+    const int g = ln.g, lig = ln.lig;
+    const int64_t D = (int64_t)geo.NV * VEC;
+    const int4 sg = A.csr.seg[w];
+    const int s0 = A.csr.hub_off[sg.w], s1 = A.csr.hub_off[sg.w + 1];
+    for (int ch = 0; ch < geo.nchunk; ++ch) {
+        const int j = ch * geo.L + lig;
+        const bool active = j < geo.NV;
+        const int col0 = active ? j * VEC : 0;
+        float mx[VEC];
+        double sum[VEC];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) { mx[i] = -INFINITY; sum[i] = 0.0; }
+        const double* P = reinterpret_cast<const double*>(A.partial);
+        if (!BWD) {
+            for (int s = s0; s < s1; ++s)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], (float)P[(int64_t)s * 2 * D + col0 + i]);
+        }
+        for (int s = s0; s < s1; ++s) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) {
+                double part = P[(int64_t)s * 2 * D + D + col0 + i];
+                if (!BWD) {
+                    const float ms = (float)P[(int64_t)s * 2 * D + col0 + i];
+                    part *= (double)expf(ms - mx[i]);  // rescale the segment's sum to the row maximum
+                }
+                sum[i] += part;
+            }
+        }
+        softmax_pass_write<T, VEC>(A, sg.y, sg.z, g, geo.G, col0, active, mx, sum, BWD);
+    }
+}
+
+
+hipError_t launch_softmax(const EngineArgs& a, int dtype, int vec, bool backward, hipStream_t s) {
+    if (a.sch.w_small_end <= 0) return hipSuccess;
+    dim3 grid(blocks_for_waves(a.sch.w_small_end)), block(WAVE * WPB);
+    dim3 fgrid(blocks_for_waves(a.sch.n_seg));
+    if (dtype == 0) {
+        GNNK_VEC_DISPATCH_F32(vec, {
+            if (backward) {
+                hipLaunchKernelGGL((softmax_kernel<float, V, true>), grid, block, 0, s, a);
+                if (a.sch.n_seg > 0)
+                    hipLaunchKernelGGL((softmax_finish_kernel<float, V, true>), fgrid, block, 0, s, a);
+            } else {
+                hipLaunchKernelGGL((softmax_kernel<float, V, false>), grid, block, 0, s, a);
+                if (a.sch.n_seg > 0)
+                    hipLaunchKernelGGL((softmax_finish_kernel<float, V, false>), fgrid, block, 0, s, a);
+            }
+        })
+    } else {
+        GNNK_VEC_DISPATCH_BF16(vec, {
+            if (backward) {
+                hipLaunchKernelGGL((softmax_kernel<bf16_t, V, true>), grid, block, 0, s, a);
+                if (a.sch.n_seg > 0)
+                    hipLaunchKernelGGL((softmax_finish_kernel<bf16_t, V, true>), fgrid, block, 0, s, a);
+            } else {
+                hipLaunchKernelGGL((softmax_kernel<bf16_t, V, false>), grid, block, 0, s, a);
+                if (a.sch.n_seg > 0)
+                    hipLaunchKernelGGL((softmax_finish_kernel<bf16_t, V, false>), fgrid, block, 0, s, a);
+            }
+        })
+    }
+    return hipGetLastError();
+}
+
+}  // namespace gnnk

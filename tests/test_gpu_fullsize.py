@@ -1,0 +1,245 @@
+"""GPU parity at the full workload sizes (c3: 114.6M-edge R-MAT, c4: 61.9M-edge
+R-MAT with int64 row offsets, fp32 and bf16; c5: the relational bipartite
+graph), in the launch configuration bench.py times (default schedule).  The
+oracle computes sampled rows / edges one by one: the largest hub rows, random
+rows of every degree class, empty rows, and their edges.  Tolerances are in
+tests/_gpu.py."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as orc
+from paper_1909_01315_amd import gnnk, synth
+from _gpu import assert_close, assert_exact, dev, host
+
+pytestmark = pytest.mark.gpu
+
+
+def log(msg):
+    print(f"[fullsize] {msg}", flush=True)
+
+
+def sample_rows(deg, seed, n_top=4, n_rand=96, n_empty=8):
+    """the n_top largest rows, random non-empty rows, and empty rows"""
+    rng = np.random.default_rng(seed)
+    order = np.argsort(-deg, kind="stable")
+    top = order[:n_top]
+    nz = np.nonzero(deg > 0)[0]
+    rnd = rng.choice(nz, size=min(n_rand, nz.size), replace=False)
+    ez = np.nonzero(deg == 0)[0]
+    emp = rng.choice(ez, size=min(n_empty, ez.size), replace=False) if ez.size else np.zeros(0, np.int64)
+    return np.unique(np.concatenate([top, rnd, emp])).astype(np.int64)
+
+
+def edges_of_rows(indptr, rows, cap=200000):
+    parts = [np.arange(indptr[r], indptr[r + 1]) for r in rows]
+    e = np.concatenate(parts) if parts else np.zeros(0, np.int64)
+    return e[:cap]
+
+
+def argmax_scatter_check(w, X, dm, ae_gpu, dXm_gpu, kind, name, seed=7):
+    """The masked reverse g-SpMM of max backward, checked on sampled sources.
+    The oracle's own arg edges are computed for every destination those
+    sources' out-edges reach (the only ones the backward reads)."""
+    rng = np.random.default_rng(seed)
+    cand = np.nonzero((w.outdeg > 0) & (w.outdeg <= 16))[0]
+    srcs = np.sort(rng.choice(cand, size=min(12, cand.size), replace=False)).astype(np.int64)
+    dsts = np.unique(w.sg.dst[np.isin(w.sg.src, srcs)]).astype(np.int64)
+    _, _, ae_rows = orc.gspmm(w.o, "copy_lhs", "max", X, rows=dsts)
+    assert_exact(host(ae_gpu)[dsts], ae_rows, f"{name} arg edges")
+    ae_full = np.full((w.sg.n_dst,) + ae_rows.shape[1:], -1, np.int32)
+    ae_full[dsts] = ae_rows
+    gl, _ = orc.gspmm_backward(w.o, "copy_lhs", "max", X, None, dm, arg_e=ae_full, sel=srcs)
+    assert_close(host(dXm_gpu)[srcs], gl, kind=kind, name=name)
+
+
+class Workload:
+    def __init__(self, sg, ptr64=False):
+        log(f"{sg.name}: building handle for N={sg.n_dst} E={sg.n_edges}")
+        self.sg = sg
+        self.o = orc.OGraph.of(sg)
+        self.g = gnnk.Graph.from_coo(dev(sg.src), dev(sg.dst), sg.n_src, sg.n_dst, ptr64=ptr64)
+        torch.cuda.synchronize()
+        self.indeg = np.bincount(sg.dst, minlength=sg.n_dst)
+        self.outdeg = np.bincount(sg.src, minlength=sg.n_src)
+        # in-CSR positions = edge ids (edges are sorted by destination)
+        self.indptr = np.concatenate([[0], np.cumsum(self.indeg)])
+        self.rows = sample_rows(self.indeg, 1)
+        self.srows = sample_rows(self.outdeg, 2)
+        self.edges = np.unique(np.concatenate([edges_of_rows(self.indptr, self.rows[:20], 30000),
+                                               np.random.default_rng(3).integers(0, sg.n_edges, 20000)]))
+
+
+@pytest.fixture(scope="module")
+def c3():
+    return Workload(synth.graph_c3())
+
+
+@pytest.fixture(scope="module")
+def c4():
+    return Workload(synth.graph_c4(), ptr64=True)
+
+
+# ---------------------------------------------------------------------------
+# c3: 114.6M-edge R-MAT, D=128 (GAT 8 x 16, SAGE mean)
+
+
+def test_c3_graph_formats(c3):
+    log("c3 formats")
+    info = c3.g.info()
+    assert info["max_in_degree"] == c3.indeg.max()
+    assert info["empty_dst_rows"] == int((c3.indeg == 0).sum())
+    assert info["hub_dst_rows"] > 0
+    ip, ii, ie = orc.csr(c3.o, reverse=True)
+    hp, hi, he = c3.g.csr_export(reverse=True)
+    assert np.array_equal(host(hp).astype(np.int64), ip)
+    assert np.array_equal(host(hi), ii)
+    assert np.array_equal(host(he), ie)
+    del ip, ii, ie, hp, hi, he
+    gp, gi, ge = c3.g.csr_export(reverse=False)
+    assert np.array_equal(host(gp).astype(np.int64), c3.indptr)
+    assert np.array_equal(host(gi), c3.sg.src)
+    assert_exact(c3.g.in_degrees(), c3.indeg.astype(np.int32))
+    assert_exact(c3.g.out_degrees(), c3.outdeg.astype(np.int32))
+
+
+def test_c3_gat_spmm_and_sddmm(c3):
+    N, E = c3.sg.n_dst, c3.sg.n_edges
+    fs = synth.feat_seed(3)
+    X = synth.normal(fs, "X", (N, 8, 16))
+    log("c3 attention weights (E,8,1)")
+    a = synth.uniform(fs, "alpha", (E, 8, 1), 0.0, 1.0)
+    Xd, ad = dev(X), dev(a)
+    Z = host(gnnk.gspmm(c3.g, "mul", "sum", Xd, ad))
+    log("c3 u_mul_e/sum oracle on sampled rows")
+    assert_close(Z[c3.rows], orc.gspmm(c3.o, "mul", "sum", X, a, rows=c3.rows), name="c3 u_mul_e/sum")
+    del Z
+    M = host(gnnk.gsddmm(c3.g, "dot", Xd, "u", Xd, "v"))
+    log("c3 u_dot_v oracle on sampled edges")
+    assert_close(M[c3.edges], orc.gsddmm(c3.o, "dot", X, "u", X, "v", edges=c3.edges), name="c3 u_dot_v")
+    del M
+    dZ = synth.normal(synth.grad_seed(3), "dZ", (N, 8, 16))
+    dX, da = gnnk.gspmm_backward(c3.g, "mul", "sum", Xd, ad, dev(dZ))
+    log("c3 u_mul_e/sum backward oracle")
+    gl, _ = orc.gspmm_backward(c3.o, "mul", "sum", X, a, dZ, want_rhs=False, sel=c3.srows)
+    assert_close(host(dX)[c3.srows], gl, name="c3 dX (reverse graph)")
+    _, gr = orc.gspmm_backward(c3.o, "mul", "sum", X, a, dZ, want_lhs=False, sel=c3.edges)
+    assert_close(host(da)[c3.edges], gr, name="c3 d attention")
+
+
+def test_c3_gat_scores_softmax(c3):
+    N, E = c3.sg.n_dst, c3.sg.n_edges
+    fs = synth.feat_seed(3)
+    el = synth.normal(fs, "el", (N, 8, 1))
+    er = synth.normal(fs, "er", (N, 8, 1))
+    s = gnnk.gsddmm(c3.g, "add", dev(el), "u", dev(er), "v")
+    sh = host(s)
+    log("c3 u_add_v bit-exact on sampled edges")
+    assert_exact(sh[c3.edges], orc.gsddmm(c3.o, "add", el, "u", er, "v", edges=c3.edges))
+    s2 = gnnk.edge_leaky_relu(s, 0.2)
+    assert_exact(host(s2)[c3.edges], orc.leaky_relu(sh[c3.edges], 0.2))
+    # softmax on oracle-made scores (inputs never come from the GPU path)
+    score = orc.leaky_relu(orc.gsddmm(c3.o, "add", el, "u", er, "v"), 0.2)
+    a = host(gnnk.edge_softmax(c3.g, dev(score)))
+    ref, eids = orc.edge_softmax(c3.o, score, rows=c3.rows)
+    log("c3 edge softmax on sampled rows (hub rows included)")
+    assert_close(a[eids], ref, name="c3 edge_softmax")
+    a_ref = synth.uniform(fs, "a_in", (E, 8, 1), 0.0, 1.0)
+    gout = synth.normal(synth.grad_seed(3), "g_a", (E, 8, 1))
+    ds = host(gnnk.edge_softmax_backward(c3.g, dev(a_ref), dev(gout)))
+    ref, eids = orc.edge_softmax_backward(c3.o, a_ref, gout, rows=c3.rows)
+    assert_close(ds[eids], ref, name="c3 edge_softmax_backward")
+    dl, dr = gnnk.gsddmm_backward(c3.g, "add", dev(el), "u", dev(er), "v", dev(gout))
+    gl, _ = orc.gsddmm_backward(c3.o, "add", el, "u", er, "v", gout, want_rhs=False, sel=c3.srows)
+    assert_close(host(dl)[c3.srows], gl, name="c3 d_el")
+    _, gr = orc.gsddmm_backward(c3.o, "add", el, "u", er, "v", gout, want_lhs=False, sel=c3.rows)
+    assert_close(host(dr)[c3.rows], gr, name="c3 d_er")
+
+
+def test_c3_sage_mean_and_max(c3):
+    N = c3.sg.n_dst
+    X = synth.normal(synth.feat_seed(3), "X", (N, 1, 128))
+    Xd = dev(X)
+    h = host(gnnk.gspmm(c3.g, "copy_lhs", "mean", Xd))
+    assert_close(h[c3.rows], orc.gspmm(c3.o, "copy_lhs", "mean", X, rows=c3.rows), name="c3 copy_u/mean")
+    dh = synth.normal(synth.grad_seed(3), "dh", (N, 1, 128))
+    dX, _ = gnnk.gspmm_backward(c3.g, "copy_lhs", "mean", Xd, None, dev(dh))
+    gl, _ = orc.gspmm_backward(c3.o, "copy_lhs", "mean", X, None, dh, sel=c3.srows)
+    assert_close(host(dX)[c3.srows], gl, name="c3 mean backward")
+    m, au, ae = gnnk.gspmm(c3.g, "copy_lhs", "max", Xd, want_args=True)
+    rm, rau, rae = orc.gspmm(c3.o, "copy_lhs", "max", X, rows=c3.rows)
+    assert_exact(host(m)[c3.rows], rm, "c3 max value")
+    assert_exact(host(ae)[c3.rows], rae, "c3 arg edge")
+    assert_exact(host(au)[c3.rows], rau, "c3 arg node")
+    dm = synth.normal(synth.grad_seed(3), "dm", (N, 1, 128))
+    dXm, _ = gnnk.gspmm_backward(c3.g, "copy_lhs", "max", Xd, None, dev(dm), arg_rhs=ae)
+    argmax_scatter_check(c3, X, dm, ae, dXm, "f32", "c3 argmax scatter")
+
+
+def test_c3_sum_of_ones_is_in_degree(c3):
+    ones = torch.ones((c3.sg.n_src, 1, 4), device="cuda")
+    out = gnnk.gspmm(c3.g, "copy_lhs", "sum", ones)
+    assert_exact(out[:, 0, 0], c3.indeg.astype(np.float32), "in-degree")
+
+
+# ---------------------------------------------------------------------------
+# c4: 61.9M-edge R-MAT, 42% empty rows, int64 row offsets, D=100 fp32 and bf16
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_c4_forward_backward(c4, dtype):
+    N = c4.sg.n_dst
+    kind = "f32" if dtype == "f32" else "bf16"
+    X = synth.normal(synth.feat_seed(4), "X", (N, 1, 100))
+    Y = synth.normal(synth.feat_seed(4), "Y", (N, 1, 100))
+    if dtype == "bf16":
+        X, Y = synth.to_bf16_bits(X), synth.to_bf16_bits(Y)
+    Xd, Yd = dev(X), dev(Y)
+    log(f"c4 {dtype} copy_u/sum")
+    s = host(gnnk.gspmm(c4.g, "copy_lhs", "sum", Xd))
+    assert_close(s[c4.rows], orc.gspmm(c4.o, "copy_lhs", "sum", X, rows=c4.rows), kind=kind, name="c4 sum")
+    m, au, ae = gnnk.gspmm(c4.g, "copy_lhs", "max", Xd, want_args=True)
+    rm, rau, rae = orc.gspmm(c4.o, "copy_lhs", "max", X, rows=c4.rows)
+    assert_exact(host(m)[c4.rows], rm, "c4 max")
+    assert_exact(host(ae)[c4.rows], rae, "c4 arg edge")
+    assert_exact(host(au)[c4.rows], rau, "c4 arg node")
+    M = host(gnnk.gsddmm(c4.g, "dot", Xd, "u", Yd, "v"))
+    assert_close(M[c4.edges], orc.gsddmm(c4.o, "dot", X, "u", Y, "v", edges=c4.edges), kind=kind, name="c4 dot")
+    dZ = synth.normal(synth.grad_seed(4), "dZ", (N, 1, 100))
+    if dtype == "bf16":
+        dZ = synth.to_bf16_bits(dZ)
+    dX, _ = gnnk.gspmm_backward(c4.g, "copy_lhs", "sum", Xd, None, dev(dZ))
+    gl, _ = orc.gspmm_backward(c4.o, "copy_lhs", "sum", X, None, dZ, sel=c4.srows)
+    assert_close(host(dX)[c4.srows], gl, kind=kind, name="c4 sum backward")
+    dXm, _ = gnnk.gspmm_backward(c4.g, "copy_lhs", "max", Xd, None, dev(dZ), arg_rhs=ae)
+    argmax_scatter_check(c4, X, dZ, ae, dXm, kind, "c4 argmax scatter")
+    dM = synth.normal(synth.grad_seed(4), "dM", (c4.sg.n_edges, 1, 1))
+    if dtype == "bf16":
+        dM = synth.to_bf16_bits(dM)
+    dx, dy = gnnk.gsddmm_backward(c4.g, "dot", Xd, "u", Yd, "v", dev(dM))
+    gl, _ = orc.gsddmm_backward(c4.o, "dot", X, "u", Y, "v", dM, want_rhs=False, sel=c4.srows)
+    assert_close(host(dx)[c4.srows], gl, kind=kind, name="c4 dot dX")
+    _, gr = orc.gsddmm_backward(c4.o, "dot", X, "u", Y, "v", dM, want_lhs=False, sel=c4.rows)
+    assert_close(host(dy)[c4.rows], gr, kind=kind, name="c4 dot dY")
+
+
+# ---------------------------------------------------------------------------
+# c5: relational graph (etype * N + src -> dst), D=64, compared in full
+
+
+def test_c5_relational_full():
+    sg = synth.graph_c5()
+    log("c5 relational graph")
+    o = orc.OGraph.of(sg)
+    g = gnnk.Graph.from_coo(dev(sg.src), dev(sg.dst), sg.n_src, sg.n_dst)
+    X = synth.normal(synth.feat_seed(5), "Xrel", (sg.n_src, 1, 64))
+    W = sg.extra["norm"].reshape(-1, 1, 1)
+    Z = gnnk.gspmm(g, "mul", "sum", dev(X), dev(W))
+    assert_close(Z, orc.gspmm(o, "mul", "sum", X, W), name="c5 u_mul_e/sum")
+    dZ = synth.normal(synth.grad_seed(5), "dZ", (sg.n_dst, 1, 64))
+    dW = gnnk.gsddmm(g, "dot", dev(X), "u", dev(dZ), "v")
+    assert_close(dW, orc.gsddmm(o, "dot", X, "u", dZ, "v"), name="c5 dW as u_dot_v")
+    _, gw = gnnk.gspmm_backward(g, "mul", "sum", dev(X), dev(W), dev(dZ), want_lhs=False)
+    _, rw = orc.gspmm_backward(o, "mul", "sum", X, W, dZ, want_lhs=False)
+    assert_close(gw, rw, name="c5 dW via gspmm_backward")
+    g.destroy()
