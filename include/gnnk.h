@@ -237,6 +237,8 @@ gnnk_status edge_leaky_relu_backward(const gnnk_tensor* x, const gnnk_tensor* dy
  *   "seg_edges"   edges per hub-row segment (>= 32; default 2048)
  *   "no_split"    1: never split a row across waves (hub rows run whole)
  *   "small_deg"   rows of at most this in-degree share a wave (-1 = auto)
+ *   "no_fast"     1: run every call on the kernels that read operand layouts
+ *                 at run time (no compile-time specialised walks)
  * Returns GNNK_EINVAL for an unknown key or value. */
 gnnk_status gnnk_set_option(const char* key, int64_t value);
 

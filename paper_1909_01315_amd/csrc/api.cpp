@@ -190,6 +190,79 @@ int64_t rows_of_target(const gnnk_graph* g, int t) {
 
 gnnk_status launch_status(hipError_t e, const char* what) { return e == hipSuccess ? GNNK_OK : hip_fail(e, what); }
 
+// A node table addressed with 32-bit byte offsets by the fast kernels.
+bool fits32(const OperandDev& o, int64_t rows, int es) {
+    if (!o.data) return false;
+    const uint64_t rb = (uint64_t)o.stride * (uint64_t)es;
+    return rows < (1 << 24) && rb < (1u << 24) && (uint64_t)rows * rb <= 0xFFFFFFFFull;
+}
+
+// rows of the table an operand reads during a walk over `d`
+int64_t table_rows(const gnnk_graph* g, const Dir& d, int32_t target) {
+    const bool in = &d == &g->in;
+    if (target == T_EDGE) return g->n_edges;
+    if (target == T_NBR) return in ? g->n_src : g->n_dst;
+    return in ? g->n_dst : g->n_src;
+}
+
+struct Pick {
+    int spec = SP_DYN;
+    int gc = 0;
+};
+
+bool fast_geo(const Geo& geo, int dtype) {
+    return (geo.G == 1 || geo.G == 2 || geo.G == 4) && fast_vec(dtype, geo.vec);
+}
+
+// the compile-time layout of a g-SpMM call, when one matches
+Pick pick_spmm(const gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& geo, int dtype, int opk, bool maxmin) {
+    Pick p;
+    if (options().no_fast || !fast_geo(geo, dtype)) return p;
+    const int es = dtype == 1 ? 2 : 4;
+    const int64_t nrows = table_rows(g, d, T_NBR);
+    if (A.a.target != T_NBR || !A.a.full || !fits32(A.a, nrows, es)) return p;
+    const int ext = ext_of(A.flags);
+    if (ext == EXT_MASK) {
+        OperandDev m{};
+        m.data = A.mask_arg;
+        m.stride = A.mask_ld;
+        if (!fits32(m, nrows, 4)) return p;
+    }
+    if (opk == 0) {
+        p.spec = SP_CU;
+        p.gc = geo.G;
+        return p;
+    }
+    if (maxmin || opk != 1 || A.op != M_MUL || ext != EXT_NONE || A.b.target != T_EDGE || A.b.full) return p;
+    const bool head = A.b.hmul != 0;
+    const int hb = head ? geo.H : 1;
+    const bool cb = d.eid == nullptr && (hb & (hb - 1)) == 0 && geo.G * ENGINE_UNR * hb <= 64;
+    int lg = 0;
+    while ((1 << lg) < hb) ++lg;
+    A.log2hb = lg;
+    p.spec = head ? (cb ? SP_UE_H_CB : SP_UE_H) : (cb ? SP_UE_R_CB : SP_UE_R);
+    p.gc = geo.G;
+    return p;
+}
+
+// the compile-time layout of a g-SDDMM call (walks the in-CSR)
+Pick pick_sddmm(const gnnk_graph* g, const EngineArgs& A, const Geo& geo, int dtype, int opk) {
+    Pick p;
+    if (options().no_fast || !fast_geo(geo, dtype) || ext_of(A.flags) != EXT_NONE || opk == 0) return p;
+    if (!A.a.full || !A.b.full) return p;
+    const int es = dtype == 1 ? 2 : 4;
+    if (A.a.target == T_NBR && A.b.target == T_SELF && fits32(A.a, g->n_src, es) && fits32(A.b, g->n_dst, es) &&
+        (opk == 1 || A.op != M_NEGDIV2)) {
+        p.spec = SP_UV;
+        p.gc = geo.G;
+    } else if (A.a.target == T_SELF && A.b.target == T_NBR && opk == 1 && fits32(A.a, g->n_dst, es) &&
+               fits32(A.b, g->n_src, es)) {
+        p.spec = SP_VU;
+        p.gc = geo.G;
+    }
+    return p;
+}
+
 // A row-reduction (g-SpMM) pass: sums, with hub partials and their combine.
 gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& geo, int dtype, int opk,
                          hipStream_t s) {
@@ -201,7 +274,8 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
         A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 8);
         if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
     }
-    gnnk_status st = launch_status(launch_spmm(A, dtype, geo.vec, false, opk, s), "g-SpMM launch");
+    const Pick pk = pick_spmm(g, d, A, geo, dtype, opk, false);
+    gnnk_status st = launch_status(launch_spmm(A, dtype, geo.vec, false, opk, pk.spec, pk.gc, s), "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
         st = launch_status(launch_spmm_combine(A, dtype, geo.vec, false, s), "g-SpMM combine launch");
     return st;
@@ -211,7 +285,8 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
     A.csr = csr_of(g, g->in);
     set_geo(A, geo);
     A.sch = schedule(g->in, geo, false);
-    return launch_status(launch_sddmm(A, dtype, geo.vec, opk, s), "g-SDDMM launch");
+    const Pick pk = pick_sddmm(g, A, geo, dtype, opk);
+    return launch_status(launch_sddmm(A, dtype, geo.vec, opk, pk.spec, pk.gc, s), "g-SDDMM launch");
 }
 
 int32_t tgt_in(int t) { return t == GNNK_SRC ? T_NBR : (t == GNNK_EDGE ? T_EDGE : T_SELF); }   // in-CSR walk
@@ -282,7 +357,8 @@ gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_
         A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 12);
         if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
     }
-    st = launch_status(launch_spmm(A, dtype_code(out), geo.vec, true, opk, stream), "g-SpMM launch");
+    const Pick pk = pick_spmm(g, g->in, A, geo, dtype_code(out), opk, true);
+    st = launch_status(launch_spmm(A, dtype_code(out), geo.vec, true, opk, pk.spec, pk.gc, stream), "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
         st = launch_status(launch_spmm_combine(A, dtype_code(out), geo.vec, true, stream), "g-SpMM combine launch");
     return st;

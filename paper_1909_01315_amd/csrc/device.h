@@ -14,7 +14,7 @@ namespace gnnk {
 
 constexpr int WAVE = 64;
 constexpr int WPB = 4;  // wavefronts per block
-constexpr int UNR = 4;  // edges in flight per lane group
+constexpr int UNR = ENGINE_UNR;  // edges in flight per lane group
 
 typedef uint16_t bf16_t;
 
@@ -145,6 +145,32 @@ __device__ __forceinline__ double shfl_d(double x, int src) {
     return *reinterpret_cast<double*>(&v);
 }
 
+// fp64 lane moves through DPP (two 32-bit halves); CTRL is a dpp_ctrl code
+template <int CTRL>
+__device__ __forceinline__ double dpp_d(double x) {
+    int2 v = *reinterpret_cast<int2*>(&x);
+    v.x = __builtin_amdgcn_mov_dpp(v.x, CTRL, 0xF, 0xF, false);
+    v.y = __builtin_amdgcn_mov_dpp(v.y, CTRL, 0xF, 0xF, false);
+    return *reinterpret_cast<double*>(&v);
+}
+
+constexpr int DPP_QUAD_1032 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int DPP_QUAD_2301 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int DPP_ROR4 = 0x124;      // row_ror:4 (within 16 lanes)
+constexpr int DPP_ROR8 = 0x128;      // row_ror:8
+
+// Sum over aligned runs of `red` lanes (a power of two), correct in the first
+// lane of each run: DPP within 16-lane rows, swizzles beyond.
+__device__ __forceinline__ double run_sum(double v, int red) {
+    if (red >= 2) v += dpp_d<DPP_QUAD_1032>(v);
+    if (red >= 4) v += dpp_d<DPP_QUAD_2301>(v);
+    if (red >= 8) v += dpp_d<DPP_ROR4>(v);
+    if (red >= 16) v += dpp_d<DPP_ROR8>(v);
+    if (red >= 32) v += shfl_xor_d(v, 16);
+    if (red >= 64) v += shfl_xor_d(v, 32);
+    return v;
+}
+
 // Sum over aligned runs of `red` consecutive lanes starting at multiples of
 // `red` within each lane group; the first lane of a run gets the total (the
 // other lanes hold partial sums).  Every lane must call it.
@@ -160,25 +186,65 @@ __device__ __forceinline__ double seg_sum(double v, int lane_in_group, int red) 
 
 // ---------------------------------------------------------------------------
 // operands and messages
+//
+// An operand's layout can be fixed at compile time (Spec): its target (the
+// neighbour, the edge, or the row itself) and its kind (a full vector per
+// lane, one value per head, one value per row).  DYN reads both from the
+// runtime descriptor.  Fast specs address node operands with 32-bit byte
+// offsets (the host checks that the table fits), which the compiler turns
+// into scalar-base loads with one 32-bit vector offset.
+
+enum : int { DYN = -1 };
+enum : int { OK_FULL = 0, OK_HEAD = 1, OK_ROW = 2 };
+
+template <int AT_, int AK_, int BT_, int BK_, int GC_, bool CB_>
+struct Spec {
+    static constexpr int AT = AT_, AK = AK_, BT = BT_, BK = BK_;
+    static constexpr int GC = GC_;    // lane groups per wavefront, 0 = runtime (no scalar id batches)
+    static constexpr bool CB = CB_;   // b is read with one coalesced load per batch (identity edge ids)
+    static constexpr bool FAST = GC_ > 0;
+};
+using SpecDyn = Spec<DYN, DYN, DYN, DYN, 0, false>;
 
 __device__ __forceinline__ int32_t row_of(int32_t target, int32_t nb, int32_t ed, int32_t self) {
     return target == T_NBR ? nb : (target == T_EDGE ? ed : self);
 }
 
-template <typename T, int VEC>
-__device__ __forceinline__ void load_operand(const OperandDev& o, int32_t row, int col0, int h, float* v) {
-    const T* base = reinterpret_cast<const T*>(o.data) + (int64_t)row * o.stride;
-    if (o.full) {
-        IO<T, VEC>::load(base + col0, v);
-    } else {
-        const float x = IO<T, VEC>::load1(base + h * o.hmul);
+template <typename T, int VEC, int TGT, int KIND, bool FAST>
+__device__ __forceinline__ void ld_opd(const OperandDev& o, int32_t nb, int32_t ed, int32_t self, int col0, int h,
+                                       float* v) {
+    const int32_t row = row_of(TGT == DYN ? o.target : TGT, nb, ed, self);
+    if constexpr (FAST && TGT != DYN && TGT != T_EDGE && KIND != DYN) {
+        const uint32_t rb = (uint32_t)o.stride * (uint32_t)sizeof(T);
+        const uint32_t c = KIND == OK_FULL ? (uint32_t)col0 : (KIND == OK_HEAD ? (uint32_t)h : 0u);
+        const uint32_t off = __umul24((uint32_t)row, rb) + c * (uint32_t)sizeof(T);
+        const T* p = reinterpret_cast<const T*>(reinterpret_cast<const char*>(o.data) + off);
+        if constexpr (KIND == OK_FULL) {
+            IO<T, VEC>::load(p, v);
+        } else {
+            const float x = IO<T, VEC>::load1(p);
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) v[i] = x;
+            for (int i = 0; i < VEC; ++i) v[i] = x;
+        }
+    } else {
+        const T* base = reinterpret_cast<const T*>(o.data) + (int64_t)row * o.stride;
+        const bool full = KIND == DYN ? (o.full != 0) : KIND == OK_FULL;
+        if (full) {
+            IO<T, VEC>::load(base + col0, v);
+        } else {
+            const int hm = KIND == DYN ? o.hmul : (KIND == OK_HEAD ? 1 : 0);
+            const float x = IO<T, VEC>::load1(base + h * hm);
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) v[i] = x;
+        }
     }
 }
 
-// EXT: extra treatment of operand a in backward passes
-enum : int { EXT_NONE = 0, EXT_SCALE = 1 /* a / deg(row of a) */, EXT_MASK = 2 /* a where arg == edge */ };
+// the runtime-descriptor load (softmax and other generic callers)
+template <typename T, int VEC>
+__device__ __forceinline__ void load_operand(const OperandDev& o, int32_t row, int col0, int h, float* v) {
+    ld_opd<T, VEC, DYN, DYN, false>(o, row, row, row, col0, h, v);
+}
 
 // Raw operand values of one edge for this lane's VEC columns (loaded first,
 // combined after the loads of a whole batch are in flight).
@@ -191,18 +257,55 @@ struct Raw {
     int32_t dg;
 };
 
-// OPK: 0 message = a; 1 message = a * b; 2 any MsgOp (runtime)
-template <typename T, int VEC, int OPK, int EXT>
+// Values of an operand that targets the row itself, loaded once per row.
+template <int VEC>
+struct Pre {
+    float a[VEC];
+    float b[VEC];
+};
+
+// OPK: 0 message = a; 1 message = a * b; 2 any MsgOp (runtime).
+// An operand that targets the row itself under a fast spec comes from `pre`;
+// with S::CB the caller fills b from the batch's coalesced load.
+template <typename T, int VEC, int OPK, int EXT, class S>
 __device__ __forceinline__ void fetch(const EngineArgs& A, int32_t nb, int32_t ed, int32_t self, int col0, int h,
-                                      Raw<VEC>& r) {
-    const int32_t ar = row_of(A.a.target, nb, ed, self);
-    load_operand<T, VEC>(A.a, ar, col0, h, r.a);
-    if constexpr (OPK >= 1) load_operand<T, VEC>(A.b, row_of(A.b.target, nb, ed, self), col0, h, r.b);
-    if constexpr (OPK == 2) {
-        if (A.op == M_NEGDIV2) load_operand<T, VEC>(A.c, row_of(A.c.target, nb, ed, self), col0, h, r.c);
+                                      const Pre<VEC>& pre, Raw<VEC>& r) {
+    constexpr bool F = S::FAST;
+    if constexpr (F && S::AT == T_SELF) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) r.a[i] = pre.a[i];
+    } else {
+        ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a);
     }
+    if constexpr (OPK >= 1) {
+        if constexpr (F && S::BT == T_SELF) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) r.b[i] = pre.b[i];
+        } else if constexpr (!S::CB) {
+            ld_opd<T, VEC, S::BT, S::BK, F>(A.b, nb, ed, self, col0, h, r.b);
+        }
+    }
+    if constexpr (OPK == 2) {
+        if (A.op == M_NEGDIV2) ld_opd<T, VEC, DYN, DYN, false>(A.c, nb, ed, self, col0, h, r.c);
+    }
+    const int32_t ar = row_of(S::AT == DYN ? A.a.target : S::AT, nb, ed, self);
     if constexpr (EXT == EXT_SCALE) r.dg = A.deg[ar];
-    if constexpr (EXT == EXT_MASK) load_i32<VEC>(A.mask_arg + (int64_t)ar * A.mask_ld + col0, r.k);
+    if constexpr (EXT == EXT_MASK) {
+        if constexpr (F) {
+            const uint32_t off = __umul24((uint32_t)ar, (uint32_t)A.mask_ld * 4u) + (uint32_t)col0 * 4u;
+            load_i32<VEC>(reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(A.mask_arg) + off), r.k);
+        } else {
+            load_i32<VEC>(A.mask_arg + (int64_t)ar * A.mask_ld + col0, r.k);
+        }
+    }
+}
+
+// the operands of a fast spec that target the row itself
+template <typename T, int VEC, int OPK, class S>
+__device__ __forceinline__ void load_pre(const EngineArgs& A, int32_t self, int col0, int h, Pre<VEC>& pre) {
+    if constexpr (S::FAST && S::AT == T_SELF) ld_opd<T, VEC, T_SELF, S::AK, true>(A.a, 0, 0, self, col0, h, pre.a);
+    if constexpr (S::FAST && OPK >= 1 && S::BT == T_SELF)
+        ld_opd<T, VEC, T_SELF, S::BK, true>(A.b, 0, 0, self, col0, h, pre.b);
 }
 
 // message in fp64 (sums and g-SDDMM); single operations are exact in fp64
@@ -213,7 +316,11 @@ __device__ __forceinline__ void combine_f64(const EngineArgs& A, const Raw<VEC>&
 #pragma unroll
     for (int i = 0; i < VEC; ++i) ad[i] = r.a[i];
     if constexpr (EXT == EXT_SCALE) {
-        const double inv = 1.0 / (double)r.dg;  // one division per edge, not per column
+        // one reciprocal per edge, not one division per column: the hardware
+        // estimate refined by one Newton step (within an ulp of 1/deg in fp64)
+        const double d = (double)r.dg;
+        double inv = __builtin_amdgcn_rcp(d);
+        inv = fma(inv, fma(-d, inv, 1.0), inv);
 #pragma unroll
         for (int i = 0; i < VEC; ++i) ad[i] = ad[i] * inv;
     }
@@ -293,20 +400,7 @@ __device__ __forceinline__ void combine_f32(const EngineArgs& A, const Raw<VEC>&
 }
 
 // ---------------------------------------------------------------------------
-// edge batches: positions p0 + u * stride, u < UNR.  Slots past the row end
-// read the row's first position (always in bounds); ok[] drops them later.
-
-__device__ __forceinline__ void batch_ids(const CsrDev& C, int64_t b, int64_t e, int64_t p0, int64_t stride,
-                                          bool* ok, int32_t* nb, int32_t* ed) {
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-        const int64_t p = p0 + (int64_t)u * stride;
-        ok[u] = p < e;
-        const int64_t pc = ok[u] ? p : b;
-        nb[u] = C.idx[pc];
-        ed[u] = C.eid ? C.eid[pc] : (int32_t)pc;
-    }
-}
+// max / min
 
 // candidate (m, e) replaces (best, be): strictly better, or equal with a
 // smaller edge id, or nothing recorded yet.  Bitwise operators keep it
@@ -322,7 +416,8 @@ __device__ __forceinline__ bool better(float m, int32_t e, float best, int32_t b
 
 template <typename T, int VEC>
 __device__ __forceinline__ void write_sum_row(const EngineArgs& A, int64_t row, bool active, int lig, int col0,
-                                              int h, double* acc, int64_t deg, bool write_lane) {
+                                              int h, double* acc, int64_t deg, bool write_lane,
+                                              bool may_reduce = true) {
     if (A.flags & F_OWN_MEAN) {
         const double d = deg > 0 ? (double)deg : 1.0;
 #pragma unroll
@@ -332,7 +427,7 @@ __device__ __forceinline__ void write_sum_row(const EngineArgs& A, int64_t row, 
 #pragma unroll
         for (int i = 0; i < VEC; ++i) acc[i] = -acc[i];
     }
-    if (!A.out.reduce) {
+    if (!may_reduce || !A.out.reduce) {
         if (active && write_lane && row >= 0) {
             float v[VEC];
 #pragma unroll
@@ -362,7 +457,38 @@ __device__ __forceinline__ Lanes lanes_of(const GeomDev& geo) {
     return Lanes{lane >> geo.log2L, lane & (geo.L - 1)};
 }
 
-__device__ __forceinline__ int wave_id() { return blockIdx.x * WPB + (threadIdx.x >> 6); }
+// with the lane-group count fixed at compile time (GC > 0)
+template <int GC>
+__device__ __forceinline__ Lanes lanes_of(const GeomDev& geo) {
+    if constexpr (GC > 0) {
+        constexpr int L = WAVE / GC;
+        const int lane = threadIdx.x & (WAVE - 1);
+        return Lanes{lane / L, lane % L};
+    } else {
+        return lanes_of(geo);
+    }
+}
+
+// sum over the lane groups of a wavefront (each lane keeps its columns)
+template <int GC, int VEC>
+__device__ __forceinline__ void sum_groups(const GeomDev& geo, double* acc) {
+    const int L = GC > 0 ? WAVE / GC : geo.L;
+    for (int s = L; s < WAVE; s <<= 1)
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) acc[i] += shfl_xor_d(acc[i], s);
+}
+
+// a wave-uniform value, moved to scalar registers
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+    const int32_t lo = __builtin_amdgcn_readfirstlane((int32_t)(uint64_t)x);
+    const int32_t hi = __builtin_amdgcn_readfirstlane((int32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+}
+
+// wave index within the grid, in a scalar register
+__device__ __forceinline__ int wave_id() {
+    return __builtin_amdgcn_readfirstlane((int)(blockIdx.x * WPB + (threadIdx.x >> 6)));
+}
 
 // ---------------------------------------------------------------------------
 // template dispatch of the launchers
@@ -396,9 +522,6 @@ __device__ __forceinline__ int wave_id() { return blockIdx.x * WPB + (threadIdx.
         default: { constexpr int X = EXT_NONE; __VA_ARGS__; } break;         \
     }
 
-inline int ext_of(int32_t flags) {
-    return (flags & F_MASK_A) ? EXT_MASK : ((flags & F_SCALE_A_DEG) ? EXT_SCALE : EXT_NONE);
-}
 
 inline unsigned blocks_for_waves(int64_t waves) { return (unsigned)((waves + WPB - 1) / WPB); }
 

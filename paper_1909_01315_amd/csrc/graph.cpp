@@ -486,6 +486,9 @@ gnnk_status gnnk_set_option(const char* key, int64_t value) {
     } else if (k == "small_deg") {
         if (value < -1 || value > 4096) return fail(GNNK_EINVAL, "small_deg must be in [-1, 4096]");
         options().small_deg = value;
+    } else if (k == "no_fast") {
+        if (value != 0 && value != 1) return fail(GNNK_EINVAL, "no_fast is 0 or 1");
+        options().no_fast = value;
     } else {
         return fail(GNNK_EINVAL, "unknown option '%s'", key);
     }

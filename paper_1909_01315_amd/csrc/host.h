@@ -51,6 +51,7 @@ struct Options {
     int64_t seg_edges = 2048;
     int64_t no_split = 0;
     int64_t small_deg = -1;
+    int64_t no_fast = 0;  // 1: every call uses the runtime-layout kernels
 };
 Options& options();
 

@@ -26,6 +26,8 @@ namespace gnnk {
 
 enum OperandTarget : int32_t { T_NBR = 0, T_EDGE = 1, T_SELF = 2 };
 
+constexpr int ENGINE_UNR = 4;  // edges in flight per lane group and batch
+
 // message kinds (fused op of up to three operands a, b, c)
 enum MsgOp : int32_t {
     M_COPY_A = 0,   // a
@@ -97,6 +99,13 @@ enum : int32_t {
     F_IS_MIN = 16,      // max/min reductions: minimum
 };
 
+// EXT: extra treatment of operand a in backward passes
+enum : int { EXT_NONE = 0, EXT_SCALE = 1 /* a / deg(row of a) */, EXT_MASK = 2 /* a where arg == edge */ };
+
+inline int ext_of(int32_t flags) {
+    return (flags & F_MASK_A) ? EXT_MASK : ((flags & F_SCALE_A_DEG) ? EXT_SCALE : EXT_NONE);
+}
+
 struct EngineArgs {
     CsrDev csr;
     SchedDev sch;
@@ -112,13 +121,32 @@ struct EngineArgs {
     int32_t op;              // MsgOp
     int32_t flags;
     int64_t mask_ld;         // row stride of mask_arg
+    int32_t log2hb;          // coalesced b: log2 of the values per edge (heads, or 1 per row)
+    int32_t pad2;
+};
+
+// Operand layouts with kernels specialised at compile time (the host picks
+// one when a call matches it and the lane-group count is 1, 2 or 4; SP_DYN
+// reads every layout from the descriptors).
+enum SpecId : int32_t {
+    SP_DYN = 0,
+    SP_CU = 1,       // a: neighbour row, full                 (copy_u, and dZ in node gradients)
+    SP_UE_H = 2,     // a: neighbour row; b: edge, one per head (u_mul_e with attention weights)
+    SP_UE_H_CB = 3,  //   the same, b read coalesced (identity edge ids)
+    SP_UE_R = 4,     // a: neighbour row; b: edge, one per row  (u_mul_e with a scalar edge weight)
+    SP_UE_R_CB = 5,  //   the same, b read coalesced
+    SP_UV = 6,       // a: neighbour row; b: own row            (g-SDDMM u_op_v)
+    SP_VU = 7,       // a: own row; b: neighbour row            (edge gradient dZ[v] . X[u])
 };
 
 // ----- host-side launchers (spmm.hip, sddmm.hip, softmax.hip, misc.hip) -----
-// dtype: 0 fp32, 1 bf16; opk: 0 copy-a, 1 mul-ab, 2 generic
-hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, hipStream_t s);
+// dtype: 0 fp32, 1 bf16; opk: 0 copy-a, 1 mul-ab, 2 generic; gc: lane groups
+// of a fast spec
+bool fast_vec(int dtype, int vec);
+hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, int spec, int gc,
+                       hipStream_t s);
 hipError_t launch_spmm_combine(const EngineArgs& a, int dtype, int vec, bool maxmin, hipStream_t s);
-hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, hipStream_t s);
+hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, int spec, int gc, hipStream_t s);
 hipError_t launch_softmax(const EngineArgs& a, int dtype, int vec, bool backward, hipStream_t s);
 hipError_t launch_leaky(const void* x, const void* dy, void* y, int64_t rows, int32_t cols, int64_t sx,
                         int64_t sdy, int64_t sy, float slope, int dtype, bool backward, hipStream_t s);

@@ -6,70 +6,75 @@
 // g-SpMM (the lemma on dL/dW of g-SpMM) and of g-SDDMM.  Elementwise ops are
 // single fp32 operations (computed in fp64, rounded once); dot products and
 // sums over broadcast positions accumulate in fp64.
-#include "device.h"
+#include "walk.h"
 
 namespace gnnk {
 
+// Output of one edge: VEC columns, or the sum over the lanes of a head (dot)
+// or of the row, computed with DPP within 16-lane rows when the run length is
+// a power of two.
 template <typename T, int VEC, int OPK, int EXT>
-__device__ __forceinline__ void sddmm_edges(const EngineArgs& A, int32_t self, int64_t b, int64_t e, int64_t n_iter,
-                                            int start, int stride, int lig, int col0, int h, bool active) {
-    const CsrDev& C = A.csr;
-    // n_iter is uniform over the wavefront so the lane reductions line up
-    for (int64_t it = 0; it < n_iter; it += UNR) {
-        int32_t nb[UNR], ed[UNR];
-        bool ok[UNR];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            const int64_t p = b + start + (it + u) * (int64_t)stride;
-            ok[u] = ((it + u) < n_iter) & (p < e);
-            const int64_t pc = ok[u] ? p : b;
-            nb[u] = C.idx[pc];
-            ed[u] = C.eid ? C.eid[pc] : (int32_t)pc;
-        }
-        Raw<VEC> r[UNR];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT>(A, nb[u], ed[u], self, col0, h, r[u]);
+struct SddmmSink {
+    const EngineArgs& A;
+    int lig, col0, h;
+    bool active;
+    __device__ __forceinline__ void operator()(const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
+        double m[VEC];
+        combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
+        const bool neg = (A.flags & F_NEGATE) != 0;
         if (!A.out.reduce) {
+            if (ok & active) {
+                float v[VEC];
 #pragma unroll
-            for (int u = 0; u < UNR; ++u) {
-                double m[VEC];
-                combine_f64<VEC, OPK, EXT>(A, r[u], ed[u], m);
-                if (ok[u] & active) {
-                    float v[VEC];
-#pragma unroll
-                    for (int i = 0; i < VEC; ++i) v[i] = (float)((A.flags & F_NEGATE) ? -m[i] : m[i]);
-                    IO<T, VEC>::store(reinterpret_cast<T*>(A.out.data) + (int64_t)ed[u] * A.out.stride + col0, v);
-                }
+                for (int i = 0; i < VEC; ++i) v[i] = (float)(neg ? -m[i] : m[i]);
+                IO<T, VEC>::store(reinterpret_cast<T*>(A.out.data) + (int64_t)ed * A.out.stride + col0, v);
             }
         } else {
+            double s = 0.0;
 #pragma unroll
-            for (int u = 0; u < UNR; ++u) {
-                double m[VEC];
-                combine_f64<VEC, OPK, EXT>(A, r[u], ed[u], m);
-                double s = 0.0;
-#pragma unroll
-                for (int i = 0; i < VEC; ++i) s += m[i];
-                s = seg_sum(active ? s : 0.0, lig, A.out.red);
-                if (ok[u] & active & ((lig % A.out.red) == 0)) {
-                    if (A.flags & F_NEGATE) s = -s;
-                    const int64_t o = A.out.per_head ? h : 0;
-                    IO<T, VEC>::store1(reinterpret_cast<T*>(A.out.data) + (int64_t)ed[u] * A.out.stride + o,
-                                       (float)s);
-                }
+            for (int i = 0; i < VEC; ++i) s += m[i];
+            const int red = A.out.red;
+            s = active ? s : 0.0;
+            s = (red & (red - 1)) == 0 ? run_sum(s, red) : seg_sum(s, lig, red);
+            if (ok & active & ((lig % red) == 0)) {
+                const int64_t o = A.out.per_head ? h : 0;
+                IO<T, VEC>::store1(reinterpret_cast<T*>(A.out.data) + (int64_t)ed * A.out.stride + o,
+                                   (float)(neg ? -s : s));
             }
         }
     }
+};
+
+// the edges of one row: by the whole wavefront (WAVE_ROW, uniform bounds) or
+// by this lane group alone
+template <typename T, int VEC, int OPK, int EXT, class S, bool WAVE_ROW>
+__device__ __forceinline__ void sddmm_row(const EngineArgs& A, const Lanes& ln, int G, int L, int64_t r, int64_t b,
+                                          int64_t e) {
+    const GeomDev& geo = A.geo;
+    const int32_t self = r >= 0 ? (int32_t)r : 0;
+    for (int ch = 0; ch < geo.nchunk; ++ch) {
+        const int j = ch * L + ln.lig;
+        const bool active = j < geo.NV;
+        const int col0 = active ? j * VEC : 0;
+        const int h = col0 / geo.F;
+        Pre<VEC> pre;
+        if (r >= 0) load_pre<T, VEC, OPK, S>(A, self, col0, h, pre);
+        SddmmSink<T, VEC, OPK, EXT> sink{A, ln.lig, col0, h, active};
+        if constexpr (WAVE_ROW) walk_row<T, VEC, OPK, EXT, S>(A, self, b, e, ln.g, G, col0, h, pre, sink);
+        else walk_lane<T, VEC, OPK, EXT, S>(A, self, b, e, col0, h, pre, sink);
+    }
 }
 
-template <typename T, int VEC, int OPK, int EXT>
+template <typename T, int VEC, int OPK, int EXT, class S>
 __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
     const int w = wave_id();
     if (w >= A.sch.w_small_end) return;
     const GeomDev& geo = A.geo;
-    const Lanes ln = lanes_of(geo);
-    int64_t r, b, e, n_iter;
-    int start, stride;
+    const Lanes ln = lanes_of<S::GC>(geo);
+    const int G = S::GC > 0 ? S::GC : geo.G;
+    const int L = WAVE / G;
     if (w < A.sch.w_big_end) {
+        int64_t r, b, e;
         if (w < A.sch.n_seg) {
             const int4 s = A.csr.seg[w];
             r = s.x; b = s.y; e = s.z;
@@ -78,46 +83,75 @@ __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        start = ln.g;
-        stride = geo.G;
-        n_iter = (e - b + geo.G - 1) / geo.G;
+        sddmm_row<T, VEC, OPK, EXT, S, true>(A, ln, G, L, uniform64(r), uniform64(b), uniform64(e));
     } else {
-        const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + ln.g;
-        r = -1; b = 0; e = 0;
+        int64_t r = -1, b = 0, e = 0;
+        const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * G + ln.g;
         if (k < A.sch.n_nz) {
             r = A.csr.perm[k];
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        start = 0;
-        stride = 1;
-        // the first group of the wave has the longest row (rows sorted by degree)
-        const int64_t k0 = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G;
-        const int64_t r0 = A.csr.perm[k0];
-        n_iter = row_ptr(A.csr, r0 + 1) - row_ptr(A.csr, r0);
-    }
-    for (int ch = 0; ch < geo.nchunk; ++ch) {
-        const int j = ch * geo.L + ln.lig;
-        const bool active = j < geo.NV;
-        const int col0 = active ? j * VEC : 0;
-        const int h = col0 / geo.F;
-        sddmm_edges<T, VEC, OPK, EXT>(A, r >= 0 ? (int32_t)r : 0, b, e, n_iter, start, stride, ln.lig, col0, h,
-                                      active);
+        sddmm_row<T, VEC, OPK, EXT, S, false>(A, ln, G, L, r, b, e);
     }
 }
 
-hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, hipStream_t s) {
+namespace {
+
+template <typename T, int V>
+void launch_sddmm_t(const EngineArgs& a, int opk, int ext, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
+    if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
+        if (spec == SP_UV || spec == SP_VU) {
+            switch (gc) {
+                case 1: {
+                    constexpr int C = 1;
+                    if (spec == SP_VU) {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    } else if (opk == 1) {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    } else {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    }
+                } break;
+                case 2: {
+                    constexpr int C = 2;
+                    if (spec == SP_VU) {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    } else if (opk == 1) {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    } else {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    }
+                } break;
+                default: {
+                    constexpr int C = 4;
+                    if (spec == SP_VU) {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    } else if (opk == 1) {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    } else {
+                        hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
+                    }
+                } break;
+            }
+            return;
+        }
+    }
+    GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
+        hipLaunchKernelGGL((sddmm_kernel<T, V, K, X, SpecDyn>), grid, block, 0, s, a);
+    }))
+}
+
+}  // namespace
+
+hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, int spec, int gc, hipStream_t s) {
     if (a.sch.w_small_end <= 0) return hipSuccess;
     const dim3 grid(blocks_for_waves(a.sch.w_small_end)), block(WAVE * WPB);
     const int ext = ext_of(a.flags);
     if (dtype == 0) {
-        GNNK_VEC_DISPATCH_F32(vec, GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
-            hipLaunchKernelGGL((sddmm_kernel<float, V, K, X>), grid, block, 0, s, a);
-        })))
+        GNNK_VEC_DISPATCH_F32(vec, launch_sddmm_t<float, V>(a, opk, ext, spec, gc, grid, block, s))
     } else {
-        GNNK_VEC_DISPATCH_BF16(vec, GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
-            hipLaunchKernelGGL((sddmm_kernel<bf16_t, V, K, X>), grid, block, 0, s, a);
-        })))
+        GNNK_VEC_DISPATCH_BF16(vec, launch_sddmm_t<bf16_t, V>(a, opk, ext, spec, gc, grid, block, s))
     }
     return hipGetLastError();
 }

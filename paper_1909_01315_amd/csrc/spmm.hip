@@ -9,50 +9,21 @@
 // and min compare fp32 messages and break ties toward the smaller edge id.
 // The edge loop loads the next batch's indices while the current batch's
 // gathers are in flight.
-#include "device.h"
+#include "walk.h"
 
 namespace gnnk {
 
 // ---------------------------------------------------------------------------
 // sums
 
-template <typename T, int VEC, int OPK, int EXT>
-__device__ __forceinline__ void spmm_sum_edges(const EngineArgs& A, int32_t self, int64_t b, int64_t e, int start,
-                                               int stride, int col0, int h, double* acc) {
-    const int64_t step = (int64_t)stride * UNR;
-    int64_t p0 = b + start;
-    if (p0 >= e) return;
-    int32_t nb[UNR], ed[UNR];
-    bool ok[UNR];
-    batch_ids(A.csr, b, e, p0, stride, ok, nb, ed);
-    for (; p0 < e; p0 += step) {
-        Raw<VEC> r[UNR];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT>(A, nb[u], ed[u], self, col0, h, r[u]);
-        bool okc[UNR];
-        int32_t edc[UNR];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            okc[u] = ok[u];
-            edc[u] = ed[u];
-        }
-        batch_ids(A.csr, b, e, p0 + step, stride, ok, nb, ed);  // next batch, overlapping the gathers
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            double m[VEC];
-            combine_f64<VEC, OPK, EXT>(A, r[u], edc[u], m);
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) acc[i] += okc[u] ? m[i] : 0.0;
-        }
-    }
-}
-
-template <typename T, int VEC, int OPK, int EXT>
+template <typename T, int VEC, int OPK, int EXT, class S>
 __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
     const int w = wave_id();
     if (w >= A.sch.w_total) return;
     const GeomDev& geo = A.geo;
-    const Lanes ln = lanes_of(geo);
+    const Lanes ln = lanes_of<S::GC>(geo);
+    const int G = S::GC > 0 ? S::GC : geo.G;
+    const int L = WAVE / G;
 
     if (w < A.sch.w_big_end) {
         // one wavefront: a segment of a hub row, or a whole big row
@@ -66,18 +37,27 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
+        r = uniform64(r);
+        b = uniform64(b);
+        e = uniform64(e);
         for (int ch = 0; ch < geo.nchunk; ++ch) {
-            const int j = ch * geo.L + ln.lig;
+            const int j = ch * L + ln.lig;
             const bool active = j < geo.NV;
             const int col0 = active ? j * VEC : 0;
             const int h = col0 / geo.F;
             double acc[VEC];
 #pragma unroll
             for (int i = 0; i < VEC; ++i) acc[i] = 0.0;
-            spmm_sum_edges<T, VEC, OPK, EXT>(A, (int32_t)r, b, e, ln.g, geo.G, col0, h, acc);
-            for (int s = geo.L; s < WAVE; s <<= 1)
+            Pre<VEC> pre;
+            load_pre<T, VEC, OPK, S>(A, (int32_t)r, col0, h, pre);
+            auto sink = [&](const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
+                double m[VEC];
+                combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) acc[i] += shfl_xor_d(acc[i], s);
+                for (int i = 0; i < VEC; ++i) acc[i] += ok ? m[i] : 0.0;
+            };
+            walk_row<T, VEC, OPK, EXT, S>(A, (int32_t)r, b, e, ln.g, G, col0, h, pre, sink);
+            sum_groups<S::GC, VEC>(geo, acc);
             if (slot >= 0) {
                 if (ln.g == 0 && active) {
                     double* P = reinterpret_cast<double*>(A.partial) + (int64_t)slot * A.partial_stride + col0;
@@ -85,42 +65,51 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
                     for (int i = 0; i < VEC; ++i) P[i] = acc[i];
                 }
             } else {
-                write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, ln.g == 0);
+                write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, ln.g == 0, !S::FAST);
             }
         }
     } else if (w < A.sch.w_small_end) {
         // small rows: each lane group owns one row
-        const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + ln.g;
+        const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * G + ln.g;
         int64_t r = -1, b = 0, e = 0;
         if (k < A.sch.n_nz) {
             r = A.csr.perm[k];
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
+        const int32_t self = r >= 0 ? (int32_t)r : 0;
         for (int ch = 0; ch < geo.nchunk; ++ch) {
-            const int j = ch * geo.L + ln.lig;
+            const int j = ch * L + ln.lig;
             const bool active = j < geo.NV;
             const int col0 = active ? j * VEC : 0;
             const int h = col0 / geo.F;
             double acc[VEC];
 #pragma unroll
             for (int i = 0; i < VEC; ++i) acc[i] = 0.0;
-            spmm_sum_edges<T, VEC, OPK, EXT>(A, r >= 0 ? (int32_t)r : 0, b, e, 0, 1, col0, h, acc);
-            write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, true);
+            Pre<VEC> pre;
+            load_pre<T, VEC, OPK, S>(A, self, col0, h, pre);
+            auto sink = [&](const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
+                double m[VEC];
+                combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) acc[i] += ok ? m[i] : 0.0;
+            };
+            walk_lane<T, VEC, OPK, EXT, S>(A, self, b, e, col0, h, pre, sink);
+            write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, true, !S::FAST);
         }
     } else {
         // empty rows: the empty reduction is 0 (no mean, no negation)
         const int64_t k0 = A.sch.n_nz +
-                           ((int64_t)(w - A.sch.w_small_end) * geo.G + ln.g) * A.sch.fill_rows_per_group;
+                           ((int64_t)(w - A.sch.w_small_end) * G + ln.g) * A.sch.fill_rows_per_group;
         for (int q = 0; q < A.sch.fill_rows_per_group; ++q) {
             const int64_t k = k0 + q;
             const int64_t r = k < A.sch.n_rows ? A.csr.perm[k] : -1;
             for (int ch = 0; ch < geo.nchunk; ++ch) {
-                const int j = ch * geo.L + ln.lig;
+                const int j = ch * L + ln.lig;
                 const bool active = j < geo.NV;
                 const int col0 = active ? j * VEC : 0;
                 const int h = col0 / geo.F;
-                if (!A.out.reduce) {
+                if (S::FAST || !A.out.reduce) {
                     if (active && r >= 0) {
                         float v[VEC];
 #pragma unroll
@@ -169,45 +158,6 @@ __global__ __launch_bounds__(256) void spmm_sum_combine_kernel(EngineArgs A) {
 // ---------------------------------------------------------------------------
 // max / min with the winning edge and neighbour
 
-template <typename T, int VEC, int OPK>
-__device__ __forceinline__ void spmm_cmp_edges(const EngineArgs& A, int32_t self, int64_t b, int64_t e, int start,
-                                               int stride, int col0, int h, float* best, int32_t* be,
-                                               int32_t* bn) {
-    const bool is_min = (A.flags & F_IS_MIN) != 0;
-    const int64_t step = (int64_t)stride * UNR;
-    int64_t p0 = b + start;
-    if (p0 >= e) return;
-    int32_t nb[UNR], ed[UNR];
-    bool ok[UNR];
-    batch_ids(A.csr, b, e, p0, stride, ok, nb, ed);
-    for (; p0 < e; p0 += step) {
-        Raw<VEC> r[UNR];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT_NONE>(A, nb[u], ed[u], self, col0, h, r[u]);
-        bool okc[UNR];
-        int32_t edc[UNR], nbc[UNR];
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            okc[u] = ok[u];
-            edc[u] = ed[u];
-            nbc[u] = nb[u];
-        }
-        batch_ids(A.csr, b, e, p0 + step, stride, ok, nb, ed);
-#pragma unroll
-        for (int u = 0; u < UNR; ++u) {
-            float m[VEC];
-            combine_f32<VEC, OPK>(A, r[u], m);
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) {
-                const bool upd = okc[u] & better(m[i], edc[u], best[i], be[i], is_min);
-                best[i] = upd ? m[i] : best[i];
-                be[i] = upd ? edc[u] : be[i];
-                bn[i] = upd ? nbc[u] : bn[i];
-            }
-        }
-    }
-}
-
 template <typename T, int VEC>
 __device__ __forceinline__ void write_cmp_row(const EngineArgs& A, int64_t row, bool active, int col0,
                                               const float* best, const int32_t* be, const int32_t* bn) {
@@ -221,37 +171,69 @@ __device__ __forceinline__ void write_cmp_row(const EngineArgs& A, int64_t row, 
     if (A.arg_nbr) store_i32<VEC>(A.arg_nbr + row * D + col0, bn);
 }
 
-template <typename T, int VEC, int OPK>
-__global__ __launch_bounds__(256) void spmm_cmp_kernel(EngineArgs A) {
-    const int w = wave_id();
-    if (w >= A.sch.w_total) return;
+// Running max/min of one lane group.  The group sees its edges in ascending
+// position, which is ascending edge id when the CSR has identity ids or
+// rows kept in id order; TIES = true adds the explicit smaller-id test for
+// any other order.
+template <int VEC, int OPK, bool TIES>
+struct CmpSink {
+    const EngineArgs& A;
+    bool is_min;
+    float best[VEC];
+    int32_t be[VEC], bn[VEC];
+    __device__ __forceinline__ void operator()(const Raw<VEC>& rw, int32_t ed, int32_t nb, bool ok) {
+        float m[VEC];
+        combine_f32<VEC, OPK>(A, rw, m);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            bool upd;
+            if constexpr (TIES) upd = better(m[i], ed, best[i], be[i], is_min);
+            else upd = (be[i] < 0) | (is_min ? (m[i] < best[i]) : (m[i] > best[i]));
+            upd = upd & ok;
+            best[i] = upd ? m[i] : best[i];
+            be[i] = upd ? ed : be[i];
+            bn[i] = upd ? nb : bn[i];
+        }
+    }
+};
+
+// max/min over the edges of one row: by the whole wavefront (WAVE_ROW,
+// uniform bounds; hub segments leave partials) or by this lane group alone
+template <typename T, int VEC, int OPK, class S, bool WAVE_ROW>
+__device__ __forceinline__ void cmp_row(const EngineArgs& A, const Lanes& ln, int G, int L, int64_t r, int64_t b,
+                                        int64_t e, int slot) {
     const GeomDev& geo = A.geo;
-    const Lanes ln = lanes_of(geo);
     const int64_t D = (int64_t)geo.NV * VEC;
     const bool is_min = (A.flags & F_IS_MIN) != 0;
-
-    if (w < A.sch.w_big_end) {
-        int64_t r, b, e;
-        int slot = -1;
-        if (w < A.sch.n_seg) {
-            const int4 s = A.csr.seg[w];
-            r = s.x; b = s.y; e = s.z; slot = w;
-        } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
-        }
-        for (int ch = 0; ch < geo.nchunk; ++ch) {
-            const int j = ch * geo.L + ln.lig;
-            const bool active = j < geo.NV;
-            const int col0 = active ? j * VEC : 0;
-            const int h = col0 / geo.F;
-            float best[VEC];
-            int32_t be[VEC], bn[VEC];
+    const bool ties = A.csr.eid != nullptr;
+    const int32_t self = r >= 0 ? (int32_t)r : 0;
+    for (int ch = 0; ch < geo.nchunk; ++ch) {
+        const int j = ch * L + ln.lig;
+        const bool active = j < geo.NV;
+        const int col0 = active ? j * VEC : 0;
+        const int h = col0 / geo.F;
+        float best[VEC];
+        int32_t be[VEC], bn[VEC];
+        Pre<VEC> pre;
+        auto run = [&](auto& sk) {
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) { best[i] = 0.0f; be[i] = -1; bn[i] = -1; }
-            spmm_cmp_edges<T, VEC, OPK>(A, (int32_t)r, b, e, ln.g, geo.G, col0, h, best, be, bn);
-            for (int s = geo.L; s < WAVE; s <<= 1) {
+            for (int i = 0; i < VEC; ++i) { sk.best[i] = 0.0f; sk.be[i] = -1; sk.bn[i] = -1; }
+            if constexpr (WAVE_ROW) walk_row<T, VEC, OPK, EXT_NONE, S>(A, self, b, e, ln.g, G, col0, h, pre, sk);
+            else walk_lane<T, VEC, OPK, EXT_NONE, S>(A, self, b, e, col0, h, pre, sk);
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) { best[i] = sk.best[i]; be[i] = sk.be[i]; bn[i] = sk.bn[i]; }
+        };
+        if (ties) {
+            CmpSink<VEC, OPK, true> sk{A, is_min, {}, {}, {}};
+            run(sk);
+        } else {
+            CmpSink<VEC, OPK, false> sk{A, is_min, {}, {}, {}};
+            run(sk);
+        }
+        if constexpr (!WAVE_ROW) {
+            write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn);
+        } else {
+            for (int s = L; s < WAVE; s <<= 1) {
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) {
                     const float ob = __shfl_xor(best[i], s, WAVE);
@@ -276,34 +258,47 @@ __global__ __launch_bounds__(256) void spmm_cmp_kernel(EngineArgs A) {
                 write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn);
             }
         }
+    }
+}
+
+template <typename T, int VEC, int OPK, class S>
+__global__ __launch_bounds__(256) void spmm_cmp_kernel(EngineArgs A) {
+    const int w = wave_id();
+    if (w >= A.sch.w_total) return;
+    const GeomDev& geo = A.geo;
+    const Lanes ln = lanes_of<S::GC>(geo);
+    const int G = S::GC > 0 ? S::GC : geo.G;
+    const int L = WAVE / G;
+
+    if (w < A.sch.w_big_end) {
+        int64_t r, b, e;
+        int slot = -1;
+        if (w < A.sch.n_seg) {
+            const int4 s = A.csr.seg[w];
+            r = s.x; b = s.y; e = s.z; slot = w;
+        } else {
+            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
+            b = row_ptr(A.csr, r);
+            e = row_ptr(A.csr, r + 1);
+        }
+        cmp_row<T, VEC, OPK, S, true>(A, ln, G, L, uniform64(r), uniform64(b), uniform64(e), slot);
     } else if (w < A.sch.w_small_end) {
-        const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + ln.g;
+        const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * G + ln.g;
         int64_t r = -1, b = 0, e = 0;
         if (k < A.sch.n_nz) {
             r = A.csr.perm[k];
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        for (int ch = 0; ch < geo.nchunk; ++ch) {
-            const int j = ch * geo.L + ln.lig;
-            const bool active = j < geo.NV;
-            const int col0 = active ? j * VEC : 0;
-            const int h = col0 / geo.F;
-            float best[VEC];
-            int32_t be[VEC], bn[VEC];
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) { best[i] = 0.0f; be[i] = -1; bn[i] = -1; }
-            spmm_cmp_edges<T, VEC, OPK>(A, r >= 0 ? (int32_t)r : 0, b, e, 0, 1, col0, h, best, be, bn);
-            write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn);
-        }
+        cmp_row<T, VEC, OPK, S, false>(A, ln, G, L, r, b, e, -1);
     } else {
         const int64_t k0 = A.sch.n_nz +
-                           ((int64_t)(w - A.sch.w_small_end) * geo.G + ln.g) * A.sch.fill_rows_per_group;
+                           ((int64_t)(w - A.sch.w_small_end) * G + ln.g) * A.sch.fill_rows_per_group;
         for (int q = 0; q < A.sch.fill_rows_per_group; ++q) {
             const int64_t k = k0 + q;
             const int64_t r = k < A.sch.n_rows ? A.csr.perm[k] : -1;
             for (int ch = 0; ch < geo.nchunk; ++ch) {
-                const int j = ch * geo.L + ln.lig;
+                const int j = ch * L + ln.lig;
                 const bool active = j < geo.NV;
                 float best[VEC];
                 int32_t be[VEC], bn[VEC];
@@ -358,29 +353,86 @@ __global__ __launch_bounds__(256) void spmm_cmp_combine_kernel(EngineArgs A) {
 // ---------------------------------------------------------------------------
 // launchers
 
-hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, hipStream_t s) {
+bool fast_vec(int dtype, int vec) { return dtype == 0 ? vec == 4 : (vec == 4 || vec == 8); }
+
+namespace {
+
+template <int GC, bool CB>
+using SpUEH = Spec<T_NBR, OK_FULL, T_EDGE, OK_HEAD, GC, CB>;
+template <int GC, bool CB>
+using SpUER = Spec<T_NBR, OK_FULL, T_EDGE, OK_ROW, GC, CB>;
+template <int GC>
+using SpCU = Spec<T_NBR, OK_FULL, DYN, DYN, GC, false>;
+
+#define GNNK_GC_DISPATCH(GC_, ...)                               \
+    switch (GC_) {                                               \
+        case 1: { constexpr int C = 1; __VA_ARGS__; } break;     \
+        case 2: { constexpr int C = 2; __VA_ARGS__; } break;     \
+        default: { constexpr int C = 4; __VA_ARGS__; } break;    \
+    }
+
+template <typename T, int V>
+void launch_sum_t(const EngineArgs& a, int opk, int ext, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
+    if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
+        if (spec != SP_DYN) {
+            GNNK_GC_DISPATCH(gc, {
+                switch (spec) {
+                    case SP_CU:
+                        GNNK_EXT_DISPATCH(ext, {
+                            hipLaunchKernelGGL((spmm_sum_kernel<T, V, 0, X, SpCU<C>>), grid, block, 0, s, a);
+                        })
+                        break;
+                    case SP_UE_H:
+                        hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUEH<C, false>>), grid, block, 0, s, a);
+                        break;
+                    case SP_UE_H_CB:
+                        hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUEH<C, true>>), grid, block, 0, s, a);
+                        break;
+                    case SP_UE_R:
+                        hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUER<C, false>>), grid, block, 0, s, a);
+                        break;
+                    default:
+                        hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUER<C, true>>), grid, block, 0, s, a);
+                        break;
+                }
+            })
+            return;
+        }
+    }
+    GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
+        hipLaunchKernelGGL((spmm_sum_kernel<T, V, K, X, SpecDyn>), grid, block, 0, s, a);
+    }))
+}
+
+template <typename T, int V>
+void launch_cmp_t(const EngineArgs& a, int opk, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
+    if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
+        if (spec == SP_CU) {
+            GNNK_GC_DISPATCH(gc, { hipLaunchKernelGGL((spmm_cmp_kernel<T, V, 0, SpCU<C>>), grid, block, 0, s, a); })
+            return;
+        }
+    }
+    GNNK_OPK_DISPATCH(opk, { hipLaunchKernelGGL((spmm_cmp_kernel<T, V, K, SpecDyn>), grid, block, 0, s, a); })
+}
+
+}  // namespace
+
+hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, int spec, int gc,
+                       hipStream_t s) {
     if (a.sch.w_total <= 0) return hipSuccess;
     const dim3 grid(blocks_for_waves(a.sch.w_total)), block(WAVE * WPB);
     const int ext = ext_of(a.flags);
     if (maxmin) {
         if (dtype == 0) {
-            GNNK_VEC_DISPATCH_F32(vec, GNNK_OPK_DISPATCH(opk, {
-                hipLaunchKernelGGL((spmm_cmp_kernel<float, V, K>), grid, block, 0, s, a);
-            }))
+            GNNK_VEC_DISPATCH_F32(vec, launch_cmp_t<float, V>(a, opk, spec, gc, grid, block, s))
         } else {
-            GNNK_VEC_DISPATCH_BF16(vec, GNNK_OPK_DISPATCH(opk, {
-                hipLaunchKernelGGL((spmm_cmp_kernel<bf16_t, V, K>), grid, block, 0, s, a);
-            }))
+            GNNK_VEC_DISPATCH_BF16(vec, launch_cmp_t<bf16_t, V>(a, opk, spec, gc, grid, block, s))
         }
     } else {
         if (dtype == 0) {
-            GNNK_VEC_DISPATCH_F32(vec, GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
-                hipLaunchKernelGGL((spmm_sum_kernel<float, V, K, X>), grid, block, 0, s, a);
-            })))
+            GNNK_VEC_DISPATCH_F32(vec, launch_sum_t<float, V>(a, opk, ext, spec, gc, grid, block, s))
         } else {
-            GNNK_VEC_DISPATCH_BF16(vec, GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
-                hipLaunchKernelGGL((spmm_sum_kernel<bf16_t, V, K, X>), grid, block, 0, s, a);
-            })))
+            GNNK_VEC_DISPATCH_BF16(vec, launch_sum_t<bf16_t, V>(a, opk, ext, spec, gc, grid, block, s))
         }
     }
     return hipGetLastError();

@@ -1,0 +1,236 @@
+// Edge walks of the row engine.
+//
+// walk_row(): the whole wavefront works on the positions [b, e) of one CSR
+// row (a hub segment or a big row).  Lane group g takes the positions
+// b + g, b + g + G, ...; a batch is UNR consecutive positions per group, so
+// G * UNR consecutive positions per wavefront.
+//
+// Under a fast spec (G known at compile time) full batches are software
+// pipelined: the neighbour and edge ids of a batch come from scalar loads
+// issued two batches ahead (waited on through the scalar counter, so they
+// never wait behind the vector gathers), the gathers of batch i + 1 are in
+// flight while batch i is combined, and a per-edge head or row value of b
+// (the attention weights) is read with one coalesced load per batch and
+// moved to its lanes with ds_bpermute.  The last, partial batch and every
+// batch of a runtime-G call read their ids per lane, clamp positions past
+// the row end to the row start (always in bounds) and drop those slots.
+//
+// walk_lane(): one lane group walks its own row (the small-row role).
+//
+// Both call consume(const Raw& r, int32_t edge_id, int32_t nbr_id, bool ok)
+// for every edge of the lane group in ascending position order.
+#pragma once
+
+#include "device.h"
+
+namespace gnnk {
+
+template <int NBT>
+struct Ids {
+    int32_t nb[NBT];
+    int32_t ed[NBT];
+};
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(4))) v4i* cint4_ptr;
+
+// ids of positions [q, q + NBT): scalar loads (q is uniform)
+template <int NBT>
+__device__ __forceinline__ void sload_ids(const CsrDev& C, int64_t q, Ids<NBT>& s) {
+    static_assert(NBT % 4 == 0, "batches hold a multiple of 4 positions");
+    cint4_ptr pn = (cint4_ptr)(C.idx + q);
+#pragma unroll
+    for (int k = 0; k < NBT / 4; ++k) {
+        const v4i v = pn[k];
+        s.nb[4 * k] = v.x; s.nb[4 * k + 1] = v.y; s.nb[4 * k + 2] = v.z; s.nb[4 * k + 3] = v.w;
+    }
+    if (C.eid) {
+        cint4_ptr pe = (cint4_ptr)(C.eid + q);
+#pragma unroll
+        for (int k = 0; k < NBT / 4; ++k) {
+            const v4i v = pe[k];
+            s.ed[4 * k] = v.x; s.ed[4 * k + 1] = v.y; s.ed[4 * k + 2] = v.z; s.ed[4 * k + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < NBT; ++k) s.ed[k] = (int32_t)(q + k);
+    }
+}
+
+// the value of slot u of lane group g among GC candidates held in scalars
+// (read through readfirstlane so the choice stays a register select and
+// never becomes an indexed access to a private array)
+template <int GC>
+__device__ __forceinline__ int32_t pick(const int32_t* v, int u, int g) {
+    if constexpr (GC == 1) {
+        return __builtin_amdgcn_readfirstlane(v[u]);
+    } else if constexpr (GC == 2) {
+        const int32_t x0 = __builtin_amdgcn_readfirstlane(v[2 * u]);
+        const int32_t x1 = __builtin_amdgcn_readfirstlane(v[2 * u + 1]);
+        return (g & 1) ? x1 : x0;
+    } else {
+        static_assert(GC == 4, "fast specs use 1, 2 or 4 lane groups");
+        const int32_t x0 = __builtin_amdgcn_readfirstlane(v[4 * u]);
+        const int32_t x1 = __builtin_amdgcn_readfirstlane(v[4 * u + 1]);
+        const int32_t x2 = __builtin_amdgcn_readfirstlane(v[4 * u + 2]);
+        const int32_t x3 = __builtin_amdgcn_readfirstlane(v[4 * u + 3]);
+        const int32_t lo = (g & 1) ? x1 : x0;
+        const int32_t hi = (g & 1) ? x3 : x2;
+        return (g & 2) ? hi : lo;
+    }
+}
+
+// Issue the loads of one full batch at position q (uniform) from its ids.
+template <typename T, int VEC, int OPK, int EXT, class S>
+__device__ __forceinline__ void issue_batch(const EngineArgs& A, const Ids<S::GC * UNR>& s, int64_t q, int g,
+                                            int32_t self, int col0, int h, const Pre<VEC>& pre, Raw<VEC>* r,
+                                            int32_t* nb, int32_t* ed, float& cbv) {
+    constexpr int GC = S::GC;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        nb[u] = pick<GC>(s.nb, u, g);
+        ed[u] = pick<GC>(s.ed, u, g);
+        fetch<T, VEC, OPK, EXT, S>(A, nb[u], ed[u], self, col0, h, pre, r[u]);
+    }
+    if constexpr (S::CB && OPK >= 1) {
+        // lane l reads element (l mod Hb) of edge q + l / Hb; lanes past the
+        // batch read the batch's first value
+        constexpr int NBT = GC * UNR;
+        const int lane = __lane_id();
+        const int hb = A.log2hb;
+        const int l = lane < (NBT << hb) ? lane : 0;
+        const T* p = reinterpret_cast<const T*>(A.b.data) + q * A.b.stride;
+        cbv = IO<T, 1>::load1(p + (int64_t)(l >> hb) * A.b.stride + (l & ((1 << hb) - 1)));
+    }
+}
+
+// Hand the edges of a full batch to consume (b of a CB spec arrives by
+// ds_bpermute from the coalesced load).
+template <int VEC, int OPK, class S, class F>
+__device__ __forceinline__ void take_batch(const EngineArgs& A, Raw<VEC>* r, const int32_t* nb, const int32_t* ed,
+                                           float cbv, int g, int h, F& consume) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        if constexpr (S::CB && OPK >= 1) {
+            const int src = ((g + S::GC * u) << A.log2hb) + (S::BK == OK_HEAD ? h : 0);
+            const float x = __shfl(cbv, src, WAVE);
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) r[u].b[i] = x;
+        }
+        consume(r[u], ed[u], nb[u], true);
+    }
+}
+
+// Per-lane ids of one batch: positions p0 + u * stride, clamped to b past e.
+// Positions fit in 32 bits (edge ids are int32).
+__device__ __forceinline__ void batch_ids(const CsrDev& C, int32_t b, int32_t e, int32_t p0, int32_t stride,
+                                          bool* ok, int32_t* nb, int32_t* ed) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        const int32_t p = p0 + u * stride;
+        ok[u] = p < e;
+        const int32_t pc = ok[u] ? p : b;
+        nb[u] = C.idx[pc];
+        ed[u] = C.eid ? C.eid[pc] : pc;
+    }
+}
+
+// Per-lane batches over positions b + start, b + start + stride, ... < e,
+// the next batch's ids loaded while the current batch's gathers are in
+// flight.  No CB for these (the b operand is read per slot).
+template <typename T, int VEC, int OPK, int EXT, class S, class F>
+__device__ __forceinline__ void walk_strided(const EngineArgs& A, int32_t self, int64_t b64, int64_t e64,
+                                             int64_t start, int stride, int col0, int h, const Pre<VEC>& pre,
+                                             F& consume) {
+    using SN = Spec<S::AT, S::AK, S::BT, S::BK, S::GC, false>;
+    const int32_t b = (int32_t)b64, e = (int32_t)e64;
+    const int32_t step = stride * UNR;
+    int32_t p0 = b + (int32_t)start;
+    if (p0 >= e) return;
+    int32_t nb[UNR], ed[UNR];
+    bool ok[UNR];
+    batch_ids(A.csr, b, e, p0, stride, ok, nb, ed);
+    for (; p0 < e; p0 += step) {
+        Raw<VEC> r[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT, SN>(A, nb[u], ed[u], self, col0, h, pre, r[u]);
+        bool okc[UNR];
+        int32_t edc[UNR], nbc[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            okc[u] = ok[u];
+            edc[u] = ed[u];
+            nbc[u] = nb[u];
+        }
+        batch_ids(A.csr, b, e, p0 + step, stride, ok, nb, ed);  // next batch, overlapping the gathers
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) consume(r[u], edc[u], nbc[u], okc[u]);
+    }
+}
+
+// The wavefront walks [b, e) of one row (see the file comment).  b and e
+// must be wave-uniform.
+template <typename T, int VEC, int OPK, int EXT, class S, class F>
+__device__ __forceinline__ void walk_row(const EngineArgs& A, int32_t self, int64_t b, int64_t e, int g, int G,
+                                         int col0, int h, const Pre<VEC>& pre, F& consume) {
+    if constexpr (!S::FAST) {
+        walk_strided<T, VEC, OPK, EXT, S>(A, self, b, e, g, G, col0, h, pre, consume);
+    } else {
+        constexpr int NBT = S::GC * UNR;
+        const int64_t nfull = (e - b) / NBT;
+#if GNNK_PIPE2
+        if (nfull > 0) {
+            Ids<NBT> ia, ib;
+            Raw<VEC> ra[UNR], rb[UNR];
+            int32_t na[UNR], ea[UNR], nbb[UNR], eb[UNR];
+            float ca = 0.0f, cb = 0.0f;
+            sload_ids<NBT>(A.csr, b, ia);
+            if (nfull > 1) sload_ids<NBT>(A.csr, b + NBT, ib);
+            issue_batch<T, VEC, OPK, EXT, S>(A, ia, b, g, self, col0, h, pre, ra, na, ea, ca);
+            for (int64_t i = 0;; i += 2) {
+                const int64_t q = b + i * NBT;
+                if (i + 1 < nfull) {
+                    issue_batch<T, VEC, OPK, EXT, S>(A, ib, q + NBT, g, self, col0, h, pre, rb, nbb, eb, cb);
+                    if (i + 2 < nfull) sload_ids<NBT>(A.csr, q + 2 * NBT, ia);
+                }
+                take_batch<VEC, OPK, S>(A, ra, na, ea, ca, g, h, consume);
+                if (i + 1 >= nfull) break;
+                if (i + 2 < nfull) {
+                    issue_batch<T, VEC, OPK, EXT, S>(A, ia, q + 2 * NBT, g, self, col0, h, pre, ra, na, ea, ca);
+                    if (i + 3 < nfull) sload_ids<NBT>(A.csr, q + 3 * NBT, ib);
+                }
+                take_batch<VEC, OPK, S>(A, rb, nbb, eb, cb, g, h, consume);
+                if (i + 2 >= nfull) break;
+            }
+        }
+#else
+        // one batch in flight per wavefront (registers for eight wavefronts
+        // per SIMD); the next batch's ids load while this batch's gathers
+        // are in flight
+        if (nfull > 0) {
+            Ids<NBT> ia;
+            sload_ids<NBT>(A.csr, b, ia);
+            for (int64_t i = 0; i < nfull; ++i) {
+                const int64_t q = b + i * NBT;
+                Raw<VEC> ra[UNR];
+                int32_t na[UNR], ea[UNR];
+                float ca = 0.0f;
+                issue_batch<T, VEC, OPK, EXT, S>(A, ia, q, g, self, col0, h, pre, ra, na, ea, ca);
+                if (i + 1 < nfull) sload_ids<NBT>(A.csr, q + NBT, ia);
+                take_batch<VEC, OPK, S>(A, ra, na, ea, ca, g, h, consume);
+            }
+        }
+#endif
+        const int64_t t0 = b + nfull * NBT;
+        if (t0 < e) walk_strided<T, VEC, OPK, EXT, S>(A, self, b, e, t0 - b + g, S::GC, col0, h, pre, consume);
+    }
+}
+
+// One lane group walks its own row [b, e) (b == e for no row).
+template <typename T, int VEC, int OPK, int EXT, class S, class F>
+__device__ __forceinline__ void walk_lane(const EngineArgs& A, int32_t self, int64_t b, int64_t e, int col0, int h,
+                                          const Pre<VEC>& pre, F& consume) {
+    walk_strided<T, VEC, OPK, EXT, S>(A, self, b, e, 0, 1, col0, h, pre, consume);
+}
+
+}  // namespace gnnk
