@@ -75,7 +75,7 @@ typedef enum { GNNK_SUM = 0, GNNK_MEAN = 1, GNNK_MAX = 2, GNNK_MIN = 3 } gnnk_re
 typedef enum { GNNK_SRC = 0, GNNK_EDGE = 1, GNNK_DST = 2 } gnnk_target;
 
 /* A dense (rows, heads, feat) tensor, row-major, with a row stride in
- * elements (>= heads * feat).  Broadcasting (Appendix D's multi-head forms):
+ * elements (>= heads * feat, < 2^31).  Broadcasting (Appendix D's multi-head forms):
  * an operand may be (H, F), (H, 1) or (1, 1) against an (H, F) message. */
 typedef struct {
     void* data;

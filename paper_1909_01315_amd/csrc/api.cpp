@@ -18,7 +18,8 @@ enum Kind { K_FULL = 0, K_HEADS = 1, K_SCALAR = 2, K_BAD = 3 };
 
 bool tensor_ok(const gnnk_tensor* t) {
     return t && t->heads >= 1 && t->feat >= 1 && (t->dtype == GNNK_F32 || t->dtype == GNNK_BF16) &&
-           t->row_stride >= (int64_t)t->heads * t->feat && t->rows >= 0 && (t->data || t->rows == 0);
+           t->row_stride >= (int64_t)t->heads * t->feat && t->row_stride < ((int64_t)1 << 31) && t->rows >= 0 &&
+           (t->data || t->rows == 0);
 }
 
 // shape of a tensor against an (H, F) message
@@ -250,6 +251,8 @@ Pick pick_sddmm(const gnnk_graph* g, const EngineArgs& A, const Geo& geo, int dt
     Pick p;
     if (options().no_fast || !fast_geo(geo, dtype) || ext_of(A.flags) != EXT_NONE || opk == 0) return p;
     if (!A.a.full || !A.b.full) return p;
+    // reduced outputs need power-of-two runs of lanes (DPP sums)
+    if (A.out.reduce && (A.out.red & (A.out.red - 1)) != 0) return p;
     const int es = dtype == 1 ? 2 : 4;
     if (A.a.target == T_NBR && A.b.target == T_SELF && fits32(A.a, g->n_src, es) && fits32(A.b, g->n_dst, es) &&
         (opk == 1 || A.op != M_NEGDIV2)) {

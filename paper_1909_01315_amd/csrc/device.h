@@ -227,7 +227,7 @@ __device__ __forceinline__ void ld_opd(const OperandDev& o, int32_t nb, int32_t 
             for (int i = 0; i < VEC; ++i) v[i] = x;
         }
     } else {
-        const T* base = reinterpret_cast<const T*>(o.data) + (int64_t)row * o.stride;
+        const T* base = reinterpret_cast<const T*>(o.data) + (uint64_t)(uint32_t)row * (uint32_t)o.stride;
         const bool full = KIND == DYN ? (o.full != 0) : KIND == OK_FULL;
         if (full) {
             IO<T, VEC>::load(base + col0, v);

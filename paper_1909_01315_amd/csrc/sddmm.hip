@@ -10,10 +10,10 @@
 
 namespace gnnk {
 
-// Output of one edge: VEC columns, or the sum over the lanes of a head (dot)
-// or of the row, computed with DPP within 16-lane rows when the run length is
-// a power of two.
-template <typename T, int VEC, int OPK, int EXT>
+// Output of one edge: VEC columns (RM = 0), or the sum over runs of
+// out.red lanes (a head for dot, or the whole row): RM = 1 for power-of-two
+// runs (DPP within 16-lane rows), RM = -1 reads the mode at run time.
+template <typename T, int VEC, int OPK, int EXT, int RM>
 struct SddmmSink {
     const EngineArgs& A;
     int lig, col0, h;
@@ -22,12 +22,14 @@ struct SddmmSink {
         double m[VEC];
         combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
         const bool neg = (A.flags & F_NEGATE) != 0;
-        if (!A.out.reduce) {
+        T* row = reinterpret_cast<T*>(A.out.data) + (uint64_t)(uint32_t)ed * (uint32_t)A.out.stride;
+        const bool reduce = RM < 0 ? A.out.reduce != 0 : RM > 0;
+        if (!reduce) {
             if (ok & active) {
                 float v[VEC];
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) v[i] = (float)(neg ? -m[i] : m[i]);
-                IO<T, VEC>::store(reinterpret_cast<T*>(A.out.data) + (int64_t)ed * A.out.stride + col0, v);
+                IO<T, VEC>::store(row + col0, v);
             }
         } else {
             double s = 0.0;
@@ -35,11 +37,12 @@ struct SddmmSink {
             for (int i = 0; i < VEC; ++i) s += m[i];
             const int red = A.out.red;
             s = active ? s : 0.0;
-            s = (red & (red - 1)) == 0 ? run_sum(s, red) : seg_sum(s, lig, red);
-            if (ok & active & ((lig % red) == 0)) {
-                const int64_t o = A.out.per_head ? h : 0;
-                IO<T, VEC>::store1(reinterpret_cast<T*>(A.out.data) + (int64_t)ed * A.out.stride + o,
-                                   (float)(neg ? -s : s));
+            if constexpr (RM > 0) s = run_sum(s, red);
+            else s = (red & (red - 1)) == 0 ? run_sum(s, red) : seg_sum(s, lig, red);
+            const bool writer = RM > 0 ? ((lig & (red - 1)) == 0) : ((lig % red) == 0);
+            if (ok & active & writer) {
+                const int o = A.out.per_head ? h : 0;
+                IO<T, VEC>::store1(row + o, (float)(neg ? -s : s));
             }
         }
     }
@@ -47,7 +50,7 @@ struct SddmmSink {
 
 // the edges of one row: by the whole wavefront (WAVE_ROW, uniform bounds) or
 // by this lane group alone
-template <typename T, int VEC, int OPK, int EXT, class S, bool WAVE_ROW>
+template <typename T, int VEC, int OPK, int EXT, int RM, class S, bool WAVE_ROW>
 __device__ __forceinline__ void sddmm_row(const EngineArgs& A, const Lanes& ln, int G, int L, int64_t r, int64_t b,
                                           int64_t e) {
     const GeomDev& geo = A.geo;
@@ -59,13 +62,13 @@ __device__ __forceinline__ void sddmm_row(const EngineArgs& A, const Lanes& ln, 
         const int h = col0 / geo.F;
         Pre<VEC> pre;
         if (r >= 0) load_pre<T, VEC, OPK, S>(A, self, col0, h, pre);
-        SddmmSink<T, VEC, OPK, EXT> sink{A, ln.lig, col0, h, active};
+        SddmmSink<T, VEC, OPK, EXT, RM> sink{A, ln.lig, col0, h, active};
         if constexpr (WAVE_ROW) walk_row<T, VEC, OPK, EXT, S>(A, self, b, e, ln.g, G, col0, h, pre, sink);
         else walk_lane<T, VEC, OPK, EXT, S>(A, self, b, e, col0, h, pre, sink);
     }
 }
 
-template <typename T, int VEC, int OPK, int EXT, class S>
+template <typename T, int VEC, int OPK, int EXT, int RM, class S>
 __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
     const int w = wave_id();
     if (w >= A.sch.w_small_end) return;
@@ -83,7 +86,7 @@ __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        sddmm_row<T, VEC, OPK, EXT, S, true>(A, ln, G, L, uniform64(r), uniform64(b), uniform64(e));
+        sddmm_row<T, VEC, OPK, EXT, RM, S, true>(A, ln, G, L, uniform64(r), uniform64(b), uniform64(e));
     } else {
         int64_t r = -1, b = 0, e = 0;
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * G + ln.g;
@@ -92,53 +95,43 @@ __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        sddmm_row<T, VEC, OPK, EXT, S, false>(A, ln, G, L, r, b, e);
+        sddmm_row<T, VEC, OPK, EXT, RM, S, false>(A, ln, G, L, r, b, e);
     }
 }
 
 namespace {
 
+template <int C>
+using SpUV = Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>;
+template <int C>
+using SpVU = Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>;
+
+template <typename T, int V, int C>
+void launch_sddmm_fast(const EngineArgs& a, int opk, int spec, int rm, dim3 grid, dim3 block, hipStream_t s) {
+    if (spec == SP_VU) {
+        if (rm) hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 1, SpVU<C>>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 0, SpVU<C>>), grid, block, 0, s, a);
+    } else if (opk == 1) {
+        if (rm) hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 1, SpUV<C>>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 0, SpUV<C>>), grid, block, 0, s, a);
+    } else {
+        hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, 0, SpUV<C>>), grid, block, 0, s, a);
+    }
+}
+
 template <typename T, int V>
 void launch_sddmm_t(const EngineArgs& a, int opk, int ext, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
     if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
         if (spec == SP_UV || spec == SP_VU) {
-            switch (gc) {
-                case 1: {
-                    constexpr int C = 1;
-                    if (spec == SP_VU) {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    } else if (opk == 1) {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    } else {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    }
-                } break;
-                case 2: {
-                    constexpr int C = 2;
-                    if (spec == SP_VU) {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    } else if (opk == 1) {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    } else {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    }
-                } break;
-                default: {
-                    constexpr int C = 4;
-                    if (spec == SP_VU) {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    } else if (opk == 1) {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    } else {
-                        hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>>), grid, block, 0, s, a);
-                    }
-                } break;
-            }
+            const int rm = a.out.reduce ? 1 : 0;
+            if (gc == 1) launch_sddmm_fast<T, V, 1>(a, opk, spec, rm, grid, block, s);
+            else if (gc == 2) launch_sddmm_fast<T, V, 2>(a, opk, spec, rm, grid, block, s);
+            else launch_sddmm_fast<T, V, 4>(a, opk, spec, rm, grid, block, s);
             return;
         }
     }
     GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
-        hipLaunchKernelGGL((sddmm_kernel<T, V, K, X, SpecDyn>), grid, block, 0, s, a);
+        hipLaunchKernelGGL((sddmm_kernel<T, V, K, X, -1, SpecDyn>), grid, block, 0, s, a);
     }))
 }
 

@@ -100,7 +100,7 @@ __device__ __forceinline__ void issue_batch(const EngineArgs& A, const Ids<S::GC
         const int hb = A.log2hb;
         const int l = lane < (NBT << hb) ? lane : 0;
         const T* p = reinterpret_cast<const T*>(A.b.data) + q * A.b.stride;
-        cbv = IO<T, 1>::load1(p + (int64_t)(l >> hb) * A.b.stride + (l & ((1 << hb) - 1)));
+        cbv = IO<T, 1>::load1(p + (uint32_t)(l >> hb) * (uint32_t)A.b.stride + (l & ((1 << hb) - 1)));
     }
 }
 
