@@ -237,6 +237,14 @@ gnnk_status edge_leaky_relu_backward(const gnnk_tensor* x, const gnnk_tensor* dy
  *   "seg_edges"   edges per hub-row segment (>= 32; default 2048)
  *   "no_split"    1: never split a row across waves (hub rows run whole)
  *   "small_deg"   rows of at most this in-degree share a wave (-1 = auto)
+ *   "schedule"    0 auto, 1 the row engine (node-parallel over the degree-
+ *                 sorted rows), 2 the edge-parallel walk over the COO form
+ *                 (equal edges per lane group; split rows combined in a fixed
+ *                 order), 3 edge-parallel with fp64 atomics for split rows
+ *                 (summation order not fixed).  Edge-parallel covers g-SpMM
+ *                 sum/mean and g-SDDMM; max/min, edge softmax and outputs
+ *                 summed over broadcast positions use the row engine.
+ *   "edge_chunk"  positions per lane group of edge-parallel walks (0 auto)
  *   "no_fast"     1: run every call on the kernels that read operand layouts
  *                 at run time (no compile-time specialised walks)
  * Returns GNNK_EINVAL for an unknown key or value. */

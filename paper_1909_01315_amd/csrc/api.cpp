@@ -123,7 +123,9 @@ gnnk_status out_desc(const gnnk_tensor* t, Kind k, const Geo& g, OutDev& o) {
         o.red = g.F / g.vec;
         o.per_head = 1;
     } else {
-        o.red = g.NV;
+        // the whole row: lanes past NV hold zeros, so a run of L lanes (a
+        // power of two) gives the same sum
+        o.red = g.L;
         o.per_head = 0;
     }
     return GNNK_OK;
@@ -137,6 +139,7 @@ CsrDev csr_of(const gnnk_graph* g, const Dir& d) {
     c.perm = d.perm;
     c.seg = d.seg;
     c.hub_off = d.hub_off;
+    c.row = d.row;
     c.ptr64 = g->ptr64;
     return c;
 }
@@ -266,6 +269,33 @@ Pick pick_sddmm(const gnnk_graph* g, const EngineArgs& A, const Geo& geo, int dt
     return p;
 }
 
+// Walk chosen for a pass: 0 the row engine, else the edge-parallel (COO)
+// walk, 2 deterministic or 3 with atomics (g-SpMM; g-SDDMM has no
+// reduction).  Automatic choice, from the degree histogram: the row engine
+// for g-SpMM (measured faster on both power-law graphs of the benchmark
+// set), and for g-SDDMM unless at least 10% of the edges sit in rows of
+// degree <= 64, where the per-row overhead of the row engine (one wavefront
+// per short row, partly idle slots) exceeds the cost of reading the
+// destination operand per edge.
+int pick_walk(const Dir& d, const Geo& geo, bool reduced_out, bool sddmm) {
+    const int64_t o = options().schedule;
+    if (o == 1 || reduced_out || d.n_rows == 0) return 0;
+    if (o >= 2) return (int)o;
+    (void)geo;
+    return (sddmm && d.low_deg_share >= 0.1) ? 2 : 0;
+}
+
+// positions per lane group of an edge-parallel walk: enough lane groups to
+// fill the chip several times, a bounded partial buffer
+void set_edge_chunks(EngineArgs& A, int64_t E, const Geo& geo) {
+    int64_t target = E / ((int64_t)65536 * geo.G);
+    int64_t sub = 64;
+    while (sub < target && sub < 2048) sub <<= 1;
+    if (options().edge_chunk > 0) sub = options().edge_chunk;
+    A.sub_edges = (int32_t)sub;
+    A.n_sub = (int32_t)((E + sub - 1) / sub);
+}
+
 // A row-reduction (g-SpMM) pass: sums, with hub partials and their combine.
 gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& geo, int dtype, int opk,
                          hipStream_t s) {
@@ -273,11 +303,35 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
     set_geo(A, geo);
     A.sch = schedule(d, geo, true);
     A.partial_stride = geo.D;
+    const Pick pk = pick_spmm(g, d, A, geo, dtype, opk, false);
+    const int walk = pick_walk(d, geo, A.out.reduce != 0, false);
+    if (walk) {
+        set_edge_chunks(A, g->n_edges, geo);
+        const size_t need = walk == 3 ? (size_t)d.n_rows * geo.D * 8 : (size_t)2 * A.n_sub * geo.D * 8;
+        if (need > 0) {
+            A.partial = graph_scratch(g, need);
+            if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
+        }
+        gnnk_status st = launch_status(launch_spmm_edge(A, g->n_edges, d.n_rows, dtype, geo.vec, opk, pk.spec, pk.gc,
+                                                        walk == 3 ? 1 : 0, s),
+                                       "edge-parallel g-SpMM launch");
+        if (st != GNNK_OK) return st;
+        // empty rows: the fill role of the row engine alone
+        EngineArgs F = A;
+        SchedDev& sc = F.sch;
+        sc.n_seg = 0;
+        sc.n_hub = 0;
+        sc.n_big = sc.n_nz;
+        sc.w_big_end = 0;
+        sc.w_small_end = 0;
+        sc.w_total = (int32_t)((d.n_rows - d.n_nz + (int64_t)geo.G * sc.fill_rows_per_group - 1) /
+                               ((int64_t)geo.G * sc.fill_rows_per_group));
+        return launch_status(launch_spmm(F, dtype, geo.vec, false, opk, SP_DYN, 0, s), "empty-row fill launch");
+    }
     if (A.sch.n_seg > 0) {
         A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 8);
         if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
     }
-    const Pick pk = pick_spmm(g, d, A, geo, dtype, opk, false);
     gnnk_status st = launch_status(launch_spmm(A, dtype, geo.vec, false, opk, pk.spec, pk.gc, s), "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
         st = launch_status(launch_spmm_combine(A, dtype, geo.vec, false, s), "g-SpMM combine launch");
@@ -289,6 +343,11 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
     set_geo(A, geo);
     A.sch = schedule(g->in, geo, false);
     const Pick pk = pick_sddmm(g, A, geo, dtype, opk);
+    if (pick_walk(g->in, geo, false, true)) {
+        set_edge_chunks(A, g->n_edges, geo);
+        return launch_status(launch_sddmm_edge(A, g->n_edges, dtype, geo.vec, opk, pk.spec, pk.gc, s),
+                             "edge-parallel g-SDDMM launch");
+    }
     return launch_status(launch_sddmm(A, dtype, geo.vec, opk, pk.spec, pk.gc, s), "g-SDDMM launch");
 }
 

@@ -197,12 +197,15 @@ __device__ __forceinline__ double seg_sum(double v, int lane_in_group, int red) 
 enum : int { DYN = -1 };
 enum : int { OK_FULL = 0, OK_HEAD = 1, OK_ROW = 2 };
 
-template <int AT_, int AK_, int BT_, int BK_, int GC_, bool CB_>
+template <int AT_, int AK_, int BT_, int BK_, int GC_, bool CB_, bool PRE_ = true>
 struct Spec {
     static constexpr int AT = AT_, AK = AK_, BT = BT_, BK = BK_;
     static constexpr int GC = GC_;    // lane groups per wavefront, 0 = runtime (no scalar id batches)
     static constexpr bool CB = CB_;   // b is read with one coalesced load per batch (identity edge ids)
     static constexpr bool FAST = GC_ > 0;
+    // an operand on the row itself is loaded once per row (false: per edge,
+    // as in edge-parallel walks where consecutive edges change rows)
+    static constexpr bool PRE = PRE_ && FAST;
 };
 using SpecDyn = Spec<DYN, DYN, DYN, DYN, 0, false>;
 
@@ -271,14 +274,14 @@ template <typename T, int VEC, int OPK, int EXT, class S>
 __device__ __forceinline__ void fetch(const EngineArgs& A, int32_t nb, int32_t ed, int32_t self, int col0, int h,
                                       const Pre<VEC>& pre, Raw<VEC>& r) {
     constexpr bool F = S::FAST;
-    if constexpr (F && S::AT == T_SELF) {
+    if constexpr (S::PRE && S::AT == T_SELF) {
 #pragma unroll
         for (int i = 0; i < VEC; ++i) r.a[i] = pre.a[i];
     } else {
         ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a);
     }
     if constexpr (OPK >= 1) {
-        if constexpr (F && S::BT == T_SELF) {
+        if constexpr (S::PRE && S::BT == T_SELF) {
 #pragma unroll
             for (int i = 0; i < VEC; ++i) r.b[i] = pre.b[i];
         } else if constexpr (!S::CB) {
@@ -303,8 +306,8 @@ __device__ __forceinline__ void fetch(const EngineArgs& A, int32_t nb, int32_t e
 // the operands of a fast spec that target the row itself
 template <typename T, int VEC, int OPK, class S>
 __device__ __forceinline__ void load_pre(const EngineArgs& A, int32_t self, int col0, int h, Pre<VEC>& pre) {
-    if constexpr (S::FAST && S::AT == T_SELF) ld_opd<T, VEC, T_SELF, S::AK, true>(A.a, 0, 0, self, col0, h, pre.a);
-    if constexpr (S::FAST && OPK >= 1 && S::BT == T_SELF)
+    if constexpr (S::PRE && S::AT == T_SELF) ld_opd<T, VEC, T_SELF, S::AK, true>(A.a, 0, 0, self, col0, h, pre.a);
+    if constexpr (S::PRE && OPK >= 1 && S::BT == T_SELF)
         ld_opd<T, VEC, T_SELF, S::BK, true>(A.b, 0, 0, self, col0, h, pre.b);
 }
 

@@ -77,7 +77,7 @@ constexpr size_t ALIGN = 256;
 struct Layout {
     size_t in_ptr = 0, in_idx = 0, in_eid = 0, out_ptr = 0, out_idx = 0, out_eid = 0;
     size_t in_deg = 0, out_deg = 0, in_perm = 0, out_perm = 0;
-    size_t in_seg = 0, out_seg = 0, in_hub = 0, out_hub = 0, flag = 0, total = 0;
+    size_t in_seg = 0, out_seg = 0, in_hub = 0, out_hub = 0, in_row = 0, out_row = 0, flag = 0, total = 0;
 };
 
 struct Bump {
@@ -109,6 +109,8 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, bool own_
     L.out_seg = b.take((size_t)seg_out * 16);
     L.in_hub = b.take((size_t)(hub_in + 1) * 4);
     L.out_hub = b.take((size_t)(hub_out + 1) * 4);
+    L.in_row = b.take((size_t)E * 4);
+    L.out_row = b.take((size_t)E * 4);
     L.flag = b.take(ALIGN);
     L.total = b.off;
     return L;
@@ -150,6 +152,11 @@ void schedule_dir(const std::vector<int64_t>& ptr, int64_t n_rows, int64_t S, Ho
     d.sorted_deg.resize((size_t)n_rows);
     for (int64_t k = 0; k < n_rows; ++k) d.sorted_deg[(size_t)k] = h.deg[(size_t)h.perm[(size_t)k]];
     h.max_deg = n_rows ? d.sorted_deg[0] : 0;
+    {
+        int64_t low = 0, all = ptr[n_rows] - ptr[0];
+        for (int64_t k = n_rows - 1; k >= 0 && d.sorted_deg[(size_t)k] <= 64; --k) low += d.sorted_deg[(size_t)k];
+        d.low_deg_share = all > 0 ? (double)low / (double)all : 0.0;
+    }
     h.n_nz = d.count_above(0);
     h.n_hub = d.count_above(S);
     h.hub_off.assign((size_t)h.n_hub + 1, 0);
@@ -252,7 +259,11 @@ gnnk_status finish_build(gnnk_graph* g, const std::vector<int32_t>& src_of_e, co
     g->out.seg = reinterpret_cast<int4*>(W + L.out_seg);
     g->in.hub_off = reinterpret_cast<int32_t*>(W + L.in_hub);
     g->out.hub_off = reinterpret_cast<int32_t*>(W + L.out_hub);
+    g->in.row = reinterpret_cast<int32_t*>(W + L.in_row);
+    g->out.row = reinterpret_cast<int32_t*>(W + L.out_row);
     g->flag = reinterpret_cast<int32_t*>(W + L.flag);
+    chk(launch_fill_rows(g->in.ptr, g->ptr64, g->n_dst, E, g->in.row, s));
+    chk(launch_fill_rows(g->out.ptr, g->ptr64, g->n_src, E, g->out.row, s));
     chk(upload(g->in.deg, hin.deg.data(), hin.deg.size(), s));
     chk(upload(g->out.deg, hout.deg.data(), hout.deg.size(), s));
     chk(upload(g->in.perm, hin.perm.data(), hin.perm.size(), s));
@@ -486,6 +497,13 @@ gnnk_status gnnk_set_option(const char* key, int64_t value) {
     } else if (k == "small_deg") {
         if (value < -1 || value > 4096) return fail(GNNK_EINVAL, "small_deg must be in [-1, 4096]");
         options().small_deg = value;
+    } else if (k == "schedule") {
+        if (value < 0 || value > 3) return fail(GNNK_EINVAL, "schedule is 0 (auto), 1 (row), 2 (edge) or 3 (edge, atomic)");
+        options().schedule = value;
+    } else if (k == "edge_chunk") {
+        if (value != 0 && (value < 4 || value > (1 << 20) || value % 4))
+            return fail(GNNK_EINVAL, "edge_chunk is 0 (auto) or a multiple of 4 in [4, 2^20]");
+        options().edge_chunk = value;
     } else if (k == "no_fast") {
         if (value != 0 && value != 1) return fail(GNNK_EINVAL, "no_fast is 0 or 1");
         options().no_fast = value;

@@ -24,7 +24,9 @@ struct Dir {
     int32_t* perm = nullptr;       // device rows by descending degree
     int4* seg = nullptr;           // device segments of hub rows
     int32_t* hub_off = nullptr;    // device first segment per hub row (n_hub + 1)
+    int32_t* row = nullptr;        // device row of each position (COO form)
     int64_t n_seg = 0, n_hub = 0, n_nz = 0, max_deg = 0;
+    double low_deg_share = 0.0;       // share of the edges in rows of degree <= 64
     std::vector<int32_t> sorted_deg;  // host, descending (bin boundaries by binary search)
     int64_t count_above(int64_t t) const;  // rows with degree > t
 };
@@ -52,6 +54,8 @@ struct Options {
     int64_t no_split = 0;
     int64_t small_deg = -1;
     int64_t no_fast = 0;  // 1: every call uses the runtime-layout kernels
+    int64_t schedule = 0; // 0 auto, 1 row engine, 2 edge-parallel, 3 edge-parallel with atomics
+    int64_t edge_chunk = 0; // positions per lane group of edge-parallel walks, 0 = auto
 };
 Options& options();
 

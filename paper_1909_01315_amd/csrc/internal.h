@@ -64,6 +64,7 @@ struct CsrDev {
     const int32_t* perm;    // rows by descending degree
     const int4* seg;        // {row, begin, end, hub index} per segment of a hub row
     const int32_t* hub_off; // first segment of each hub row (hub rows = perm[0, n_hub)), n_hub + 1 entries
+    const int32_t* row;     // row of each position (the COO form of the same CSR)
     int32_t ptr64;
     int32_t pad;
 };
@@ -122,6 +123,8 @@ struct EngineArgs {
     int32_t flags;
     int64_t mask_ld;         // row stride of mask_arg
     int32_t log2hb;          // coalesced b: log2 of the values per edge (heads, or 1 per row)
+    int32_t sub_edges;       // edge-parallel walks: positions per lane group (a sub-chunk)
+    int32_t n_sub;           // edge-parallel walks: number of sub-chunks
     int32_t pad2;
 };
 
@@ -146,6 +149,14 @@ bool fast_vec(int dtype, int vec);
 hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, int spec, int gc,
                        hipStream_t s);
 hipError_t launch_spmm_combine(const EngineArgs& a, int dtype, int vec, bool maxmin, hipStream_t s);
+// edge-parallel (COO) walks, edge.hip: mode 0 = partials of split rows combined
+// in order afterwards, mode 1 = fp64 atomics into scratch (a.partial, rows x D)
+hipError_t launch_spmm_edge(const EngineArgs& a, int64_t n_pos, int64_t n_rows, int dtype, int vec, int opk, int spec,
+                            int gc, int mode, hipStream_t s);
+hipError_t launch_sddmm_edge(const EngineArgs& a, int64_t n_pos, int dtype, int vec, int opk, int spec, int gc,
+                             hipStream_t s);
+hipError_t launch_fill_rows(const void* ptr, int ptr64, int64_t n_rows, int64_t n_edges, int32_t* row,
+                            hipStream_t s);
 hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, int spec, int gc, hipStream_t s);
 hipError_t launch_softmax(const EngineArgs& a, int dtype, int vec, bool backward, hipStream_t s);
 hipError_t launch_leaky(const void* x, const void* dy, void* y, int64_t rows, int32_t cols, int64_t sx,

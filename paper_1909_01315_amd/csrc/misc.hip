@@ -46,6 +46,21 @@ __global__ void validate_ptr_kernel(const P* ptr, int64_t n_rows, int64_t n_edge
     }
 }
 
+// row of every position of a CSR: the last row whose offset is <= p
+template <typename P>
+__global__ void fill_rows_kernel(const P* ptr, int64_t n_rows, int64_t n_edges, int32_t* row) {
+    for (int64_t p = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; p < n_edges;
+         p += (int64_t)gridDim.x * blockDim.x) {
+        int64_t lo = 0, hi = n_rows;  // ptr[lo] <= p < ptr[hi]
+        while (hi - lo > 1) {
+            const int64_t mid = (lo + hi) / 2;
+            if ((int64_t)ptr[mid] <= p) lo = mid;
+            else hi = mid;
+        }
+        row[p] = (int32_t)lo;
+    }
+}
+
 __global__ void iota_kernel(int32_t* out, int64_t n) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         out[i] = (int32_t)i;
@@ -98,6 +113,18 @@ hipError_t launch_validate_ptr(const void* ptr, int ptr64, int64_t n_rows, int64
     else
         hipLaunchKernelGGL((validate_ptr_kernel<int32_t>), grid, block, 0, s, (const int32_t*)ptr, n_rows, n_edges,
                            flag);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_rows(const void* ptr, int ptr64, int64_t n_rows, int64_t n_edges, int32_t* row,
+                            hipStream_t s) {
+    if (n_edges <= 0) return hipSuccess;
+    if (ptr64)
+        hipLaunchKernelGGL(fill_rows_kernel<int64_t>, dim3(grid_1d(n_edges)), dim3(256), 0, s,
+                           reinterpret_cast<const int64_t*>(ptr), n_rows, n_edges, row);
+    else
+        hipLaunchKernelGGL(fill_rows_kernel<int32_t>, dim3(grid_1d(n_edges)), dim3(256), 0, s,
+                           reinterpret_cast<const int32_t*>(ptr), n_rows, n_edges, row);
     return hipGetLastError();
 }
 
