@@ -28,6 +28,34 @@ __global__ void leaky_kernel(const T* x, const T* dy, T* y, int64_t rows, int32_
     }
 }
 
+// the same on a contiguous tensor: 16-byte vectors, grid-stride
+template <typename T, int VEC, bool BWD>
+__global__ __launch_bounds__(256) void leaky_flat_kernel(const T* x, const T* dy, T* y, int64_t n, float slope) {
+    const int64_t nv = n / VEC;
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv; i += (int64_t)gridDim.x * blockDim.x) {
+        float xv[VEC], out[VEC];
+        IO<T, VEC>::load(x + i * VEC, xv);
+        if (BWD) {
+            float d[VEC];
+            IO<T, VEC>::load(dy + i * VEC, d);
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) out[k] = xv[k] > 0.0f ? d[k] : slope * d[k];
+        } else {
+#pragma unroll
+            for (int k = 0; k < VEC; ++k) out[k] = xv[k] > 0.0f ? xv[k] : slope * xv[k];
+        }
+        IO<T, VEC>::store(y + i * VEC, out);
+    }
+    // the tail (fewer than VEC elements), by the first threads
+    const int64_t t = nv * VEC + blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    if (t < n) {
+        const float xv = IO<T, 1>::load1(x + t);
+        const float out = BWD ? (xv > 0.0f ? IO<T, 1>::load1(dy + t) : slope * IO<T, 1>::load1(dy + t))
+                              : (xv > 0.0f ? xv : slope * xv);
+        IO<T, 1>::store1(y + t, out);
+    }
+}
+
 __global__ void validate_kernel(const int32_t* idx, int64_t n, int64_t bound, int32_t* flag) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
         int32_t v = idx[i];
@@ -79,6 +107,27 @@ hipError_t launch_leaky(const void* x, const void* dy, void* y, int64_t rows, in
                         int64_t sdy, int64_t sy, float slope, int dtype, bool backward, hipStream_t s) {
     int64_t n = rows * (int64_t)cols;
     if (n <= 0) return hipSuccess;
+    const bool flat = (rows == 1 || (sx == cols && sy == cols && (!backward || sdy == cols)));
+    const uintptr_t al = (uintptr_t)x | (uintptr_t)y | (backward ? (uintptr_t)dy : 0);
+    if (flat && al % 16 == 0) {
+        dim3 grid(grid_1d(n / (dtype == 0 ? 4 : 8) + 1)), block(256);
+        if (dtype == 0) {
+            if (backward)
+                hipLaunchKernelGGL((leaky_flat_kernel<float, 4, true>), grid, block, 0, s, (const float*)x,
+                                   (const float*)dy, (float*)y, n, slope);
+            else
+                hipLaunchKernelGGL((leaky_flat_kernel<float, 4, false>), grid, block, 0, s, (const float*)x,
+                                   (const float*)dy, (float*)y, n, slope);
+        } else {
+            if (backward)
+                hipLaunchKernelGGL((leaky_flat_kernel<bf16_t, 8, true>), grid, block, 0, s, (const bf16_t*)x,
+                                   (const bf16_t*)dy, (bf16_t*)y, n, slope);
+            else
+                hipLaunchKernelGGL((leaky_flat_kernel<bf16_t, 8, false>), grid, block, 0, s, (const bf16_t*)x,
+                                   (const bf16_t*)dy, (bf16_t*)y, n, slope);
+        }
+        return hipGetLastError();
+    }
     dim3 grid(grid_1d(n)), block(256);
     if (dtype == 0) {
         if (backward)

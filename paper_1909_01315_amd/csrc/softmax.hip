@@ -1,6 +1,7 @@
 // Edge softmax over the in-edges of each destination, per column (the
 // attention normalisation applied to the per-edge scores of Appendix D), and
-// its backward.  Forward: max, then the sum of exp(s - max) in fp64, then
+// its backward.  Forward: one pass keeps the running max m and the fp64 sum
+// of exp(s - m), rescaled whenever m grows; a second pass writes
 // a = exp(s - max) / sum.  Backward: S = sum of a * g in fp64, then
 // ds = a * (g - S).  Rows use the degree-sorted schedule; hub rows leave
 // per-segment (max, sum) or S partials and a second launch combines them in
@@ -14,16 +15,31 @@ __device__ __forceinline__ void ld_edge(const OperandDev& o, int64_t ed, int col
     IO<T, VEC>::load(reinterpret_cast<const T*>(o.data) + ed * o.stride + col0, v);
 }
 
+// running (max, sum of exp(s - max)) over the edges of a lane group
 template <typename T, int VEC>
-__device__ __forceinline__ void softmax_pass_max(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
-                                                 int col0, float* mx) {
+__device__ __forceinline__ void softmax_pass_online(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
+                                                    int col0, float* mx, double* sum) {
     for (int64_t p = b + start; p < e; p += stride) {
         const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
         float s[VEC];
         ld_edge<T, VEC>(A.a, ed, col0, s);
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], s[i]);
+        for (int i = 0; i < VEC; ++i) {
+            const float mn = fmaxf(mx[i], s[i]);
+            const double f = (double)expf(fminf(mx[i], s[i]) - mn);  // exp of a non-positive number
+            sum[i] = s[i] > mx[i] ? sum[i] * f + 1.0 : sum[i] + f;
+            mx[i] = mn;
+        }
     }
+}
+
+// merge another (max, sum) pair into this one
+__device__ __forceinline__ void softmax_merge(float& m, double& s, float om, double os) {
+    const float mn = fmaxf(m, om);
+    const double f1 = m == -INFINITY ? 0.0 : (double)expf(m - mn);
+    const double f2 = om == -INFINITY ? 0.0 : (double)expf(om - mn);
+    s = s * f1 + os * f2;
+    m = mn;
 }
 
 template <typename T, int VEC>
@@ -104,17 +120,19 @@ __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
 #pragma unroll
         for (int i = 0; i < VEC; ++i) { mx[i] = -INFINITY; sum[i] = 0.0; }
         if (!BWD) {
-            softmax_pass_max<T, VEC>(A, b, e, start, stride, col0, mx);
+            softmax_pass_online<T, VEC>(A, b, e, start, stride, col0, mx, sum);
             if (coop)
                 for (int s = geo.L; s < WAVE; s <<= 1)
 #pragma unroll
-                    for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], __shfl_xor(mx[i], s, WAVE));
-        }
-        softmax_pass_sum<T, VEC>(A, b, e, start, stride, col0, mx, sum, BWD);
-        if (coop)
-            for (int s = geo.L; s < WAVE; s <<= 1)
+                    for (int i = 0; i < VEC; ++i)
+                        softmax_merge(mx[i], sum[i], __shfl_xor(mx[i], s, WAVE), shfl_xor_d(sum[i], s));
+        } else {
+            softmax_pass_sum<T, VEC>(A, b, e, start, stride, col0, mx, sum, BWD);
+            if (coop)
+                for (int s = geo.L; s < WAVE; s <<= 1)
 #pragma unroll
-                for (int i = 0; i < VEC; ++i) sum[i] += shfl_xor_d(sum[i], s);
+                    for (int i = 0; i < VEC; ++i) sum[i] += shfl_xor_d(sum[i], s);
+        }
         if (slot >= 0) {
             if (g == 0 && active) {
                 double* P = reinterpret_cast<double*>(A.partial) + (int64_t)slot * 2 * D;
