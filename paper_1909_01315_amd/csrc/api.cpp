@@ -532,6 +532,22 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
         A.deg = g->in.deg;
         A.mask_arg = arg_rhs;
         A.mask_ld = geo.D;
+        if (cmp && g->n_edges > 0) {
+            // the argmax scatter as a masked g-SpMM on the reverse graph: the
+            // winning columns of each edge are marked once in a bit mask laid
+            // out in reverse-CSR order, so the walk reads 4 bytes per 32
+            // columns per edge instead of the arg array of its destination
+            const int32_t words = (int32_t)((geo.D + 31) / 32);
+            uint32_t* bits = reinterpret_cast<uint32_t*>(graph_scratch(g, (size_t)g->n_edges * words * 4, 1));
+            if (!bits) return fail(GNNK_ENOMEM, "scratch allocation failed");
+            st = launch_status(launch_winner_bits(arg_rhs, g->n_dst, (int32_t)geo.D, g->out.pos, bits, g->n_edges,
+                                                  words, stream),
+                               "winner mask launch");
+            if (st != GNNK_OK) return st;
+            A.flags = (scale_flags & ~F_MASK_A) | F_BITS_A;
+            A.mask_arg = reinterpret_cast<const int32_t*>(bits);
+            A.mask_ld = words;
+        }
         st = run_spmm_sum(g, g->out, A, geo, dt, opk, stream);
         if (st != GNNK_OK) return st;
     }

@@ -258,7 +258,19 @@ struct Raw {
     float c[VEC];
     int32_t k[VEC];
     int32_t dg;
+    uint32_t kb;  // EXT_BITS: the winner bits of this lane's VEC columns
 };
+
+// EXT_BITS: the winner bits of an edge (its CSR position) are read before
+// the edge's operands, so a lane with no winning column skips its load of a.
+template <int VEC, int EXT>
+__device__ __forceinline__ void fetch_bits(const EngineArgs& A, int32_t pos, int col0, Raw<VEC>& r) {
+    if constexpr (EXT == EXT_BITS) {
+        const uint32_t* M = reinterpret_cast<const uint32_t*>(A.mask_arg);
+        const uint32_t w = M[(uint64_t)(uint32_t)pos * (uint32_t)A.mask_ld + (uint32_t)(col0 >> 5)];
+        r.kb = (w >> (col0 & 31)) & ((VEC == 32 ? 0u : (1u << VEC)) - 1u);
+    }
+}
 
 // Values of an operand that targets the row itself, loaded once per row.
 template <int VEC>
@@ -277,6 +289,10 @@ __device__ __forceinline__ void fetch(const EngineArgs& A, int32_t nb, int32_t e
     if constexpr (S::PRE && S::AT == T_SELF) {
 #pragma unroll
         for (int i = 0; i < VEC; ++i) r.a[i] = pre.a[i];
+    } else if constexpr (EXT == EXT_BITS) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) r.a[i] = 0.0f;
+        if (r.kb) ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a);
     } else {
         ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a);
     }
@@ -330,6 +346,10 @@ __device__ __forceinline__ void combine_f64(const EngineArgs& A, const Raw<VEC>&
     if constexpr (EXT == EXT_MASK) {
 #pragma unroll
         for (int i = 0; i < VEC; ++i) ad[i] = (r.k[i] == ed) ? ad[i] : 0.0;
+    }
+    if constexpr (EXT == EXT_BITS) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) ad[i] = ((r.kb >> i) & 1u) ? ad[i] : 0.0;
     }
     if constexpr (OPK == 0) {
 #pragma unroll
@@ -518,10 +538,19 @@ __device__ __forceinline__ int wave_id() {
         default: { constexpr int K = 2; __VA_ARGS__; } break; \
     }
 
+// without EXT_BITS (g-SDDMM passes never read winner masks)
+#define GNNK_EXT3_DISPATCH(EXT_, ...)                                 \
+    switch (EXT_) {                                                   \
+        case EXT_SCALE: { constexpr int X = EXT_SCALE; __VA_ARGS__; } break; \
+        case EXT_MASK: { constexpr int X = EXT_MASK; __VA_ARGS__; } break;   \
+        default: { constexpr int X = EXT_NONE; __VA_ARGS__; } break;         \
+    }
+
 #define GNNK_EXT_DISPATCH(EXT_, ...)                                  \
     switch (EXT_) {                                                   \
         case EXT_SCALE: { constexpr int X = EXT_SCALE; __VA_ARGS__; } break; \
         case EXT_MASK: { constexpr int X = EXT_MASK; __VA_ARGS__; } break;   \
+        case EXT_BITS: { constexpr int X = EXT_BITS; __VA_ARGS__; } break;   \
         default: { constexpr int X = EXT_NONE; __VA_ARGS__; } break;         \
     }
 

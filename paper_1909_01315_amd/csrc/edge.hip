@@ -34,12 +34,13 @@ __device__ __forceinline__ void sub_range(const EngineArgs& A, int64_t k, int64_
 // Per-lane ids and rows of UNR consecutive positions p0 .. p0 + UNR - 1,
 // clamped to sb past se.
 __device__ __forceinline__ void coo_ids(const CsrDev& C, int32_t sb, int32_t se, int32_t p0, bool* ok, int32_t* nb,
-                                        int32_t* ed, int32_t* rw) {
+                                        int32_t* ed, int32_t* rw, int32_t* ps) {
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
         const int32_t p = p0 + u;
         ok[u] = p < se;
         const int32_t pc = ok[u] ? p : sb;
+        ps[u] = pc;
         nb[u] = C.idx[pc];
         ed[u] = C.eid ? C.eid[pc] : pc;
         rw[u] = C.row[pc];
@@ -108,11 +109,13 @@ __global__ __launch_bounds__(256) void spmm_edge_kernel(EngineArgs A, int64_t n_
             for (int i = 0; i < VEC; ++i) acc[i] = 0.0;
         };
         Pre<VEC> pre;
-        int32_t nb[UNR], ed[UNR], rw[UNR];
+        int32_t nb[UNR], ed[UNR], rw[UNR], ps[UNR];
         bool ok[UNR];
         for (int32_t p0 = sb; p0 < se; p0 += UNR) {
-            coo_ids(A.csr, sb, se, p0, ok, nb, ed, rw);
+            coo_ids(A.csr, sb, se, p0, ok, nb, ed, rw, ps);
             Raw<VEC> r[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) fetch_bits<VEC, EXT>(A, ps[u], col0, r[u]);
 #pragma unroll
             for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT, SN>(A, nb[u], ed[u], rw[u], col0, h, pre, r[u]);
 #pragma unroll
@@ -225,11 +228,13 @@ __global__ __launch_bounds__(256) void sddmm_edge_kernel(EngineArgs A, int64_t n
         const int col0 = active ? j * VEC : 0;
         const int h = col0 / geo.F;
         Pre<VEC> pre;
-        int32_t nb[UNR], ed[UNR], rw[UNR];
+        int32_t nb[UNR], ed[UNR], rw[UNR], ps[UNR];
         bool ok[UNR];
         for (int32_t p0 = sb; p0 < se; p0 += UNR) {
-            coo_ids(A.csr, sb, se, p0, ok, nb, ed, rw);
+            coo_ids(A.csr, sb, se, p0, ok, nb, ed, rw, ps);
             Raw<VEC> r[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) fetch_bits<VEC, EXT>(A, ps[u], col0, r[u]);
 #pragma unroll
             for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT, SN>(A, nb[u], ed[u], rw[u], col0, h, pre, r[u]);
 #pragma unroll
@@ -334,7 +339,7 @@ void sddmm_edge_t(const EngineArgs& a, int64_t n_pos, int opk, int ext, int spec
             return;
         }
     }
-    GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
+    GNNK_OPK_DISPATCH(opk, GNNK_EXT3_DISPATCH(ext, {
         hipLaunchKernelGGL((sddmm_edge_kernel<T, V, K, X, -1, SpecDyn>), grid, block, 0, s, a, n_pos);
     }))
 }

@@ -49,22 +49,24 @@ int64_t Dir::count_above(int64_t t) const {
     return (int64_t)(it - sorted_deg.begin());
 }
 
-void* graph_scratch(gnnk_graph* g, size_t bytes) {
+void* graph_scratch(gnnk_graph* g, size_t bytes, int slot) {
     std::lock_guard<std::mutex> lk(g->scratch_mu);
-    if (bytes <= g->scratch_bytes) return g->scratch;
-    if (g->scratch) {
+    void*& buf = slot ? g->scratch2 : g->scratch;
+    size_t& have = slot ? g->scratch2_bytes : g->scratch_bytes;
+    if (bytes <= have) return buf;
+    if (buf) {
         (void)hipDeviceSynchronize();  // in-flight kernels may still read the old buffer
-        (void)hipFree(g->scratch);
-        g->scratch = nullptr;
-        g->scratch_bytes = 0;
+        (void)hipFree(buf);
+        buf = nullptr;
+        have = 0;
     }
     size_t want = bytes + bytes / 4;
-    if (hipMalloc(&g->scratch, want) != hipSuccess) {
-        g->scratch = nullptr;
+    if (hipMalloc(&buf, want) != hipSuccess) {
+        buf = nullptr;
         return nullptr;
     }
-    g->scratch_bytes = want;
-    return g->scratch;
+    have = want;
+    return buf;
 }
 
 // ---------------------------------------------------------------------------
@@ -77,7 +79,8 @@ constexpr size_t ALIGN = 256;
 struct Layout {
     size_t in_ptr = 0, in_idx = 0, in_eid = 0, out_ptr = 0, out_idx = 0, out_eid = 0;
     size_t in_deg = 0, out_deg = 0, in_perm = 0, out_perm = 0;
-    size_t in_seg = 0, out_seg = 0, in_hub = 0, out_hub = 0, in_row = 0, out_row = 0, flag = 0, total = 0;
+    size_t in_seg = 0, out_seg = 0, in_hub = 0, out_hub = 0, in_row = 0, out_row = 0, out_pos = 0, flag = 0,
+           total = 0;
 };
 
 struct Bump {
@@ -111,6 +114,7 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, bool own_
     L.out_hub = b.take((size_t)(hub_out + 1) * 4);
     L.in_row = b.take((size_t)E * 4);
     L.out_row = b.take((size_t)E * 4);
+    L.out_pos = b.take((size_t)E * 4);
     L.flag = b.take(ALIGN);
     L.total = b.off;
     return L;
@@ -261,9 +265,11 @@ gnnk_status finish_build(gnnk_graph* g, const std::vector<int32_t>& src_of_e, co
     g->out.hub_off = reinterpret_cast<int32_t*>(W + L.out_hub);
     g->in.row = reinterpret_cast<int32_t*>(W + L.in_row);
     g->out.row = reinterpret_cast<int32_t*>(W + L.out_row);
+    g->out.pos = reinterpret_cast<int32_t*>(W + L.out_pos);
     g->flag = reinterpret_cast<int32_t*>(W + L.flag);
     chk(launch_fill_rows(g->in.ptr, g->ptr64, g->n_dst, E, g->in.row, s));
     chk(launch_fill_rows(g->out.ptr, g->ptr64, g->n_src, E, g->out.row, s));
+    chk(launch_inverse(g->out.eid, E, g->out.pos, s));
     chk(upload(g->in.deg, hin.deg.data(), hin.deg.size(), s));
     chk(upload(g->out.deg, hout.deg.data(), hout.deg.size(), s));
     chk(upload(g->in.perm, hin.perm.data(), hin.perm.size(), s));
@@ -476,6 +482,10 @@ gnnk_status graph_validate(gnnk_graph_t g, hipStream_t stream) {
 gnnk_status graph_destroy(gnnk_graph_t g) {
     clear_error();
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (g->scratch2) {
+        (void)hipDeviceSynchronize();
+        (void)hipFree(g->scratch2);
+    }
     if (g->scratch) {
         (void)hipDeviceSynchronize();
         (void)hipFree(g->scratch);

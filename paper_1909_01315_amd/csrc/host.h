@@ -25,6 +25,7 @@ struct Dir {
     int4* seg = nullptr;           // device segments of hub rows
     int32_t* hub_off = nullptr;    // device first segment per hub row (n_hub + 1)
     int32_t* row = nullptr;        // device row of each position (COO form)
+    int32_t* pos = nullptr;        // device position of each edge id in this CSR
     int64_t n_seg = 0, n_hub = 0, n_nz = 0, max_deg = 0;
     double low_deg_share = 0.0;       // share of the edges in rows of degree <= 64
     std::vector<int32_t> sorted_deg;  // host, descending (bin boundaries by binary search)
@@ -44,6 +45,9 @@ struct gnnk_graph {
     // scratch for hub-row partials, owned by the handle and grown on demand
     void* scratch = nullptr;
     size_t scratch_bytes = 0;
+    // second scratch (winner masks of max/min backward)
+    void* scratch2 = nullptr;
+    size_t scratch2_bytes = 0;
     std::mutex scratch_mu;
 };
 
@@ -63,7 +67,8 @@ gnnk_status fail(gnnk_status st, const char* fmt, ...);
 gnnk_status hip_fail(hipError_t e, const char* what);
 void clear_error();
 
-// scratch of at least `bytes` bytes owned by g (nullptr on failure)
-void* graph_scratch(gnnk_graph* g, size_t bytes);
+// scratch of at least `bytes` bytes owned by g (nullptr on failure); slot 0
+// holds partials, slot 1 winner masks
+void* graph_scratch(gnnk_graph* g, size_t bytes, int slot = 0);
 
 }  // namespace gnnk

@@ -98,12 +98,19 @@ enum : int32_t {
     F_OWN_MEAN = 4,     // the reduced value is divided by the row's own degree
     F_NEGATE = 8,       // the output is negated
     F_IS_MIN = 16,      // max/min reductions: minimum
+    F_BITS_A = 32,      // a is zeroed unless its column's bit is set in the winner mask of the position
 };
 
 // EXT: extra treatment of operand a in backward passes
-enum : int { EXT_NONE = 0, EXT_SCALE = 1 /* a / deg(row of a) */, EXT_MASK = 2 /* a where arg == edge */ };
+enum : int {
+    EXT_NONE = 0,
+    EXT_SCALE = 1,  // a / deg(row of a)
+    EXT_MASK = 2,   // a where arg[row of a][col] == edge id
+    EXT_BITS = 3,   // a where bit col of the winner mask at this CSR position is set
+};
 
 inline int ext_of(int32_t flags) {
+    if (flags & F_BITS_A) return EXT_BITS;
     return (flags & F_MASK_A) ? EXT_MASK : ((flags & F_SCALE_A_DEG) ? EXT_SCALE : EXT_NONE);
 }
 
@@ -115,7 +122,8 @@ struct EngineArgs {
     OutDev out;
     int32_t* arg_nbr;        // max/min: neighbour id of the winner (nullable)
     int32_t* arg_edge;       // max/min: edge id of the winner (nullable)
-    const int32_t* mask_arg; // F_MASK_A: edge-id array (rows of a's target, D columns)
+    const int32_t* mask_arg; // F_MASK_A: edge-id array (rows of a's target, D columns);
+                             // F_BITS_A: winner bits, mask_ld 32-bit words per CSR position
     const int32_t* deg;      // F_SCALE_A_DEG: degree per row of a's target
     void* partial;           // hub-row partials (fp64 sums, or fp32 value + int32 edge + int32 nbr)
     int64_t partial_stride;  // elements per segment row (D)
@@ -165,6 +173,12 @@ hipError_t launch_validate(const int32_t* idx, int64_t n, int64_t bound, int32_t
 hipError_t launch_validate_ptr(const void* ptr, int ptr64, int64_t n_rows, int64_t n_edges, int32_t* flag,
                                hipStream_t s);
 hipError_t launch_iota(int32_t* out, int64_t n, hipStream_t s);
+// pos[perm[q]] = q for q < n
+hipError_t launch_inverse(const int32_t* perm, int64_t n, int32_t* pos, hipStream_t s);
+// Winner masks of max/min: bits[pos_of_edge[e] * words + c / 32] has bit c % 32
+// set iff arg_e[v * D + c] == e for some row v (zeroed first).
+hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, const int32_t* pos_of_edge,
+                              uint32_t* bits, int64_t n_edges, int32_t words, hipStream_t s);
 hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int64_t n, hipStream_t s);
 
 }  // namespace gnnk

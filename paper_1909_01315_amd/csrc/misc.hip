@@ -89,6 +89,28 @@ __global__ void fill_rows_kernel(const P* ptr, int64_t n_rows, int64_t n_edges, 
     }
 }
 
+__global__ void inverse_kernel(const int32_t* perm, int64_t n, int32_t* pos) {
+    for (int64_t q = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; q < n; q += (int64_t)gridDim.x * blockDim.x)
+        pos[perm[q]] = (int32_t)q;
+}
+
+__global__ void zero_words_kernel(uint32_t* w, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        w[i] = 0u;
+}
+
+// one thread per (row, column) of the arg array; OR is order-free, so the
+// mask does not depend on the order of the atomics
+__global__ void winner_bits_kernel(const int32_t* arg_e, int64_t n, int32_t D, const int32_t* pos_of_edge,
+                                   uint32_t* bits, int32_t words, int64_t n_edges) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t e = arg_e[i];
+        if (e < 0 || e >= n_edges) continue;  // empty rows (-1); ids outside the graph are ignored
+        const int32_t c = (int32_t)(i % D);
+        atomicOr(bits + (int64_t)pos_of_edge[e] * words + (c >> 5), 1u << (c & 31));
+    }
+}
+
 __global__ void iota_kernel(int32_t* out, int64_t n) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         out[i] = (int32_t)i;
@@ -174,6 +196,22 @@ hipError_t launch_fill_rows(const void* ptr, int ptr64, int64_t n_rows, int64_t 
     else
         hipLaunchKernelGGL(fill_rows_kernel<int32_t>, dim3(grid_1d(n_edges)), dim3(256), 0, s,
                            reinterpret_cast<const int32_t*>(ptr), n_rows, n_edges, row);
+    return hipGetLastError();
+}
+
+hipError_t launch_inverse(const int32_t* perm, int64_t n, int32_t* pos, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(inverse_kernel, dim3(grid_1d(n)), dim3(256), 0, s, perm, n, pos);
+    return hipGetLastError();
+}
+
+hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, const int32_t* pos_of_edge,
+                              uint32_t* bits, int64_t n_edges, int32_t words, hipStream_t s) {
+    const int64_t nw = n_edges * words, n = n_rows * D;
+    if (nw > 0) hipLaunchKernelGGL(zero_words_kernel, dim3(grid_1d(nw)), dim3(256), 0, s, bits, nw);
+    if (n > 0)
+        hipLaunchKernelGGL(winner_bits_kernel, dim3(grid_1d(n)), dim3(256), 0, s, arg_e, n, D, pos_of_edge, bits,
+                           words, n_edges);
     return hipGetLastError();
 }
 

@@ -130,7 +130,7 @@ void launch_sddmm_t(const EngineArgs& a, int opk, int ext, int spec, int gc, dim
             return;
         }
     }
-    GNNK_OPK_DISPATCH(opk, GNNK_EXT_DISPATCH(ext, {
+    GNNK_OPK_DISPATCH(opk, GNNK_EXT3_DISPATCH(ext, {
         hipLaunchKernelGGL((sddmm_kernel<T, V, K, X, -1, SpecDyn>), grid, block, 0, s, a);
     }))
 }

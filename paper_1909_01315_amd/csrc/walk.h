@@ -87,6 +87,8 @@ __device__ __forceinline__ void issue_batch(const EngineArgs& A, const Ids<S::GC
                                             int32_t* nb, int32_t* ed, float& cbv) {
     constexpr int GC = S::GC;
 #pragma unroll
+    for (int u = 0; u < UNR; ++u) fetch_bits<VEC, EXT>(A, (int32_t)q + g + GC * u, col0, r[u]);
+#pragma unroll
     for (int u = 0; u < UNR; ++u) {
         nb[u] = pick<GC>(s.nb, u, g);
         ed[u] = pick<GC>(s.ed, u, g);
@@ -124,12 +126,13 @@ __device__ __forceinline__ void take_batch(const EngineArgs& A, Raw<VEC>* r, con
 // Per-lane ids of one batch: positions p0 + u * stride, clamped to b past e.
 // Positions fit in 32 bits (edge ids are int32).
 __device__ __forceinline__ void batch_ids(const CsrDev& C, int32_t b, int32_t e, int32_t p0, int32_t stride,
-                                          bool* ok, int32_t* nb, int32_t* ed) {
+                                          bool* ok, int32_t* nb, int32_t* ed, int32_t* ps) {
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
         const int32_t p = p0 + u * stride;
         ok[u] = p < e;
         const int32_t pc = ok[u] ? p : b;
+        ps[u] = pc;
         nb[u] = C.idx[pc];
         ed[u] = C.eid ? C.eid[pc] : pc;
     }
@@ -147,11 +150,13 @@ __device__ __forceinline__ void walk_strided(const EngineArgs& A, int32_t self, 
     const int32_t step = stride * UNR;
     int32_t p0 = b + (int32_t)start;
     if (p0 >= e) return;
-    int32_t nb[UNR], ed[UNR];
+    int32_t nb[UNR], ed[UNR], ps[UNR];
     bool ok[UNR];
-    batch_ids(A.csr, b, e, p0, stride, ok, nb, ed);
+    batch_ids(A.csr, b, e, p0, stride, ok, nb, ed, ps);
     for (; p0 < e; p0 += step) {
         Raw<VEC> r[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) fetch_bits<VEC, EXT>(A, ps[u], col0, r[u]);
 #pragma unroll
         for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT, SN>(A, nb[u], ed[u], self, col0, h, pre, r[u]);
         bool okc[UNR];
@@ -162,7 +167,7 @@ __device__ __forceinline__ void walk_strided(const EngineArgs& A, int32_t self, 
             edc[u] = ed[u];
             nbc[u] = nb[u];
         }
-        batch_ids(A.csr, b, e, p0 + step, stride, ok, nb, ed);  // next batch, overlapping the gathers
+        batch_ids(A.csr, b, e, p0 + step, stride, ok, nb, ed, ps);  // next batch, overlapping the gathers
 #pragma unroll
         for (int u = 0; u < UNR; ++u) consume(r[u], edc[u], nbc[u], okc[u]);
     }
