@@ -229,6 +229,20 @@ gnnk_status edge_leaky_relu(const gnnk_tensor* x, gnnk_tensor* y, float slope, h
 gnnk_status edge_leaky_relu_backward(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* dx, float slope,
                                      hipStream_t stream);
 
+/* Fused graph attention: the multi-head attention layer of Appendix D (a
+ * g-SDDMM u_add_v producing per-head edge scores, leaky ReLU, softmax over
+ * the in-edges of each destination, then a g-SpMM u_mul_e/sum) in one pass
+ * over each destination's in-edges, without writing the scores:
+ *   s[e, h]   = leaky(el[u, h] + er[v, h])      (fp32, as edge_leaky_relu)
+ *   out[v, h] = sum over in-edges of softmax_v(s)[e, h] * feat[u, h, :]
+ * feat: (num_src, H, F); el: (num_src, H, 1); er: (num_dst, H, 1); out:
+ * (num_dst, H, F).  attn (nullable, (num_edges, H, 1)) receives the softmax,
+ * which the backward pass (gspmm_backward, edge_softmax_backward, ...) needs.
+ * The running maximum is tracked per destination and head and the fp64 sums
+ * are rescaled when it grows; destinations without in-edges get 0.
+ * Errors: GNNK_EINVAL on shapes or dtypes. */
+gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el, const gnnk_tensor* er,
+                          float slope, gnnk_tensor* out, gnnk_tensor* attn, hipStream_t stream);
 /* ------------------------------------------------------------------------ */
 /* Tuning knobs, for schedule comparisons (forcing node- or edge-balanced
  * schedules; the paper's Table 1 states both are valid for commutative and

@@ -716,6 +716,53 @@ gnnk_status edge_softmax_backward(gnnk_graph_t g, const gnnk_tensor* out, const 
     return softmax_common(g, out, grad_out, grad_score, true, stream);
 }
 
+gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el, const gnnk_tensor* er,
+                          float slope, gnnk_tensor* out, gnnk_tensor* attn, hipStream_t stream) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (!tensor_ok(feat) || !tensor_ok(el) || !tensor_ok(er) || !tensor_ok(out) || (attn && !tensor_ok(attn)))
+        return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({feat, el, er, out, attn})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
+    const int H = feat->heads, F = feat->feat;
+    if (feat->rows != g->n_src || el->rows != g->n_src || er->rows != g->n_dst || out->rows != g->n_dst)
+        return fail(GNNK_EINVAL, "row counts must be num_src (feat, el) and num_dst (er, out)");
+    if (el->heads != H || el->feat != 1 || er->heads != H || er->feat != 1 || out->heads != H || out->feat != F)
+        return fail(GNNK_EINVAL, "shapes must be feat (H, F), el and er (H, 1), out (H, F)");
+    if (attn && (attn->rows != g->n_edges || attn->heads != H || attn->feat != 1))
+        return fail(GNNK_EINVAL, "attn must be (num_edges, H, 1)");
+    // el and er broadcast over features: keep heads separate (F per head)
+    std::vector<Member> ms{{feat, K_FULL}, {el, K_FULL}, {out, K_FULL}};
+    Geo geo;
+    gnnk_status st = choose_geo(H, F, ms, {}, geo);
+    if (st != GNNK_OK) return st;
+    if (g->n_dst == 0) return GNNK_OK;
+    EngineArgs A{};
+    A.a = operand(feat, K_FULL, T_NBR);
+    A.b = operand(el, ms[1].kind, T_NBR);
+    A.op = M_MUL;
+    A.out.data = out->data;
+    A.out.stride = out->row_stride;
+    A.out.red = 1;
+    A.csr = csr_of(g, g->in);
+    set_geo(A, geo);
+    A.sch = schedule(g->in, geo, true);
+    const int dt = dtype_code(out);
+    const size_t part = (size_t)A.sch.n_seg * 3 * geo.D * 8, ml = attn ? (size_t)A.sch.n_hub * 2 * geo.D * 8 : 0;
+    void* row_ml = nullptr;
+    if (part + ml > 0) {
+        char* p = reinterpret_cast<char*>(graph_scratch(g, part + ml));
+        if (!p) return fail(GNNK_ENOMEM, "scratch allocation failed");
+        A.partial = p;
+        row_ml = ml ? p + part : nullptr;
+    }
+    const int es = dt == 1 ? 2 : 4;
+    const bool fast = !options().no_fast && fast_geo(geo, dt) && fits32(A.a, g->n_src, es) &&
+                      fits32(A.b, g->n_src, es);
+    return launch_status(launch_gat(A, er->data, er->row_stride, attn ? attn->data : nullptr,
+                                    attn ? attn->row_stride : 0, slope, row_ml, dt, geo.vec, fast ? geo.G : 0, stream),
+                         "fused attention launch");
+}
+
 static gnnk_status leaky_common(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* y, float slope,
                                 bool backward, hipStream_t stream) {
     if (!tensor_ok(x) || (backward && !tensor_ok(dy)) || !tensor_ok(y)) return fail(GNNK_EINVAL, "malformed tensor");

@@ -163,6 +163,10 @@ hipError_t launch_spmm_edge(const EngineArgs& a, int64_t n_pos, int64_t n_rows, 
                             int gc, int mode, hipStream_t s);
 hipError_t launch_sddmm_edge(const EngineArgs& a, int64_t n_pos, int dtype, int vec, int opk, int spec, int gc,
                              hipStream_t s);
+// fused attention, gat.hip (a: feat at the neighbour, b: el at the neighbour;
+// row_ml: n_hub x 2 x D doubles when attn is written)
+hipError_t launch_gat(const EngineArgs& a, const void* er, int64_t er_stride, void* attn, int64_t attn_stride,
+                      float slope, void* row_ml, int dtype, int vec, int gc, hipStream_t s);
 hipError_t launch_fill_rows(const void* ptr, int ptr64, int64_t n_rows, int64_t n_edges, int32_t* row,
                             hipStream_t s);
 hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, int spec, int gc, hipStream_t s);

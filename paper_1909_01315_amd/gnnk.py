@@ -80,6 +80,8 @@ SYMBOLS = {
     "edge_leaky_relu": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p],
     "edge_leaky_relu_backward": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
                                  ctypes.c_void_p],
+    "gat_aggregate": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
+                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
     "gnnk_set_option": [ctypes.c_char_p, ctypes.c_int64],
     "gnnk_last_error": [],
 }
@@ -361,6 +363,21 @@ def edge_softmax_backward(g: Graph, out, grad_out, grad_score=None, stream=None)
     d1, d2, d3 = _desc(out), _desc(grad_out), _desc(grad_score)
     _check(load().edge_softmax_backward(g.handle, _ref(d1), _ref(d2), _ref(d3), _stream(stream)))
     return grad_score
+
+
+def gat_aggregate(g: Graph, feat, el, er, slope: float = 0.2, out=None, attn=None, want_attn: bool = False,
+                  stream=None):
+    """Fused attention: out[v, h] = sum over in-edges of softmax_v(leaky(el[u, h] + er[v, h])) * feat[u, h, :].
+    Returns out, or (out, attn) with want_attn (or attn given)."""
+    feat, el, er = _as3(feat), _as3(el), _as3(er)
+    if out is None:
+        out = torch.empty((g.num_dst, feat.shape[1], feat.shape[2]), dtype=feat.dtype, device=feat.device)
+    if want_attn and attn is None:
+        attn = torch.empty((g.num_edges, feat.shape[1], 1), dtype=feat.dtype, device=feat.device)
+    d = [_desc(x) for x in (feat, el, er, out, attn)]
+    _check(load().gat_aggregate(g.handle, _ref(d[0]), _ref(d[1]), _ref(d[2]), ctypes.c_float(slope), _ref(d[3]),
+                                _ref(d[4]), _stream(stream)))
+    return (out, attn) if attn is not None else out
 
 
 def edge_leaky_relu(x, slope: float = 0.2, y=None, stream=None):

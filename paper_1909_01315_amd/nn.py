@@ -114,6 +114,30 @@ class _LeakyReLU(torch.autograd.Function):
         return gnnk.edge_leaky_relu_backward(x, _c(dy).view(x.shape), ctx.slope).view(x.shape), None
 
 
+class _FusedGAT(torch.autograd.Function):
+    """gat_aggregate forward (one pass per destination, attention kept for
+    backward); backward as the chain of the unfused gradients, recomputing
+    the pre-activation scores for the leaky ReLU."""
+
+    @staticmethod
+    def forward(ctx, g, feat, el, er, slope):
+        out, a = gnnk.gat_aggregate(g, feat, el, er, slope, want_attn=True)
+        ctx.g, ctx.slope = g, slope
+        ctx.save_for_backward(feat, el, er, a)
+        return out
+
+    @staticmethod
+    def backward(ctx, dout):
+        feat, el, er, a = ctx.saved_tensors
+        g = ctx.g
+        dfeat, da = gnnk.gspmm_backward(g, "mul", "sum", feat, a, _c(dout))
+        ds = gnnk.edge_softmax_backward(g, a, da)
+        s = gnnk.gsddmm(g, "add", el, "u", er, "v")
+        ds = gnnk.edge_leaky_relu_backward(s, ds, ctx.slope)
+        d_el, d_er = gnnk.gsddmm_backward(g, "add", el, "u", er, "v", ds)
+        return None, dfeat.view(feat.shape), d_el.view(el.shape), d_er.view(er.shape), None
+
+
 # ---------------------------------------------------------------------------
 # functional API (same names and argument order as the C ABI)
 
@@ -136,6 +160,11 @@ def edge_softmax(g, score):
 def leaky_relu(x, slope: float = 0.2):
     """Differentiable leaky ReLU computed by the library's edge kernel."""
     return _LeakyReLU.apply(_c(x), float(slope))
+
+
+def gat_aggregate(g, feat, el, er, slope: float = 0.2):
+    """Differentiable fused attention aggregation (gat_aggregate)."""
+    return _FusedGAT.apply(g, _c(feat), _c(el), _c(er), float(slope))
 
 
 def degrees(g):
@@ -188,9 +217,11 @@ class GATConv(torch.nn.Module):
     leaky ReLU, softmax over in-edges, and the attention-weighted sum of the
     projected source features (u_mul_e/sum) -- the chain of Appendix D."""
 
-    def __init__(self, in_feats: int, out_feats: int, num_heads: int, negative_slope: float = 0.2):
+    def __init__(self, in_feats: int, out_feats: int, num_heads: int, negative_slope: float = 0.2,
+                 fused: bool = False):
         super().__init__()
         self.H, self.F = num_heads, out_feats
+        self.fused = fused  # one-pass gat_aggregate in forward
         self.fc = torch.nn.Linear(in_feats, out_feats * num_heads, bias=False)
         self.attn_l = torch.nn.Parameter(torch.empty(1, num_heads, out_feats))
         self.attn_r = torch.nn.Parameter(torch.empty(1, num_heads, out_feats))
@@ -204,6 +235,8 @@ class GATConv(torch.nn.Module):
         feat = self.fc(x).view(-1, self.H, self.F)
         el = (feat * self.attn_l).sum(-1, keepdim=True)  # (N, H, 1)
         er = (feat[: g.num_dst] * self.attn_r).sum(-1, keepdim=True)
+        if self.fused and not return_attention:
+            return gat_aggregate(g, feat, el, er, self.slope)
         s = leaky_relu(gsddmm(g, "add", el, "u", er, "v"), self.slope)  # (E, H, 1)
         a = edge_softmax(g, s)
         out = gspmm(g, "mul", "sum", feat, a)  # (N_dst, H, F)

@@ -156,6 +156,24 @@ def test_c3_gat_scores_softmax(c3):
     assert_close(host(dr)[c3.rows], gr, name="c3 d_er")
 
 
+def test_c3_fused_gat(c3):
+    N, E = c3.sg.n_dst, c3.sg.n_edges
+    fs = synth.feat_seed(3)
+    X = synth.normal(fs, "X", (N, 8, 16))
+    el = synth.normal(fs, "el", (N, 8, 1))
+    er = synth.normal(fs, "er", (N, 8, 1))
+    out, attn = gnnk.gat_aggregate(c3.g, dev(X), dev(el), dev(er), 0.2, want_attn=True)
+    log("c3 fused attention: oracle chain on sampled rows (hub rows included)")
+    score = orc.leaky_relu(orc.gsddmm(c3.o, "add", el, "u", er, "v"), 0.2)
+    a_rows, eids = orc.edge_softmax(c3.o, score, rows=c3.rows)
+    del score
+    assert_close(host(attn)[eids], a_rows, name="c3 fused attention")
+    a_full = np.zeros((E, 8, 1), np.float32)
+    a_full[eids] = a_rows
+    ref = orc.gspmm(c3.o, "mul", "sum", X, a_full, rows=c3.rows)
+    assert_close(host(out)[c3.rows], ref, name="c3 fused attention output")
+
+
 def test_c3_sage_mean_and_max(c3):
     N = c3.sg.n_dst
     X = synth.normal(synth.feat_seed(3), "X", (N, 1, 128))
