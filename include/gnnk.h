@@ -251,7 +251,7 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
  *   "seg_edges"   edges per hub-row segment (>= 32; default 2048)
  *   "no_split"    1: never split a row across waves (hub rows run whole)
  *   "small_deg"   rows of at most this in-degree share a wave (-1 = auto)
- *   "schedule"    0 auto, 1 the row engine (node-parallel over the degree-
+ *   "schedule"    0 auto (the row engine), 1 the row engine (node-parallel over the degree-
  *                 sorted rows), 2 the edge-parallel walk over the COO form
  *                 (equal edges per lane group; split rows combined in a fixed
  *                 order), 3 edge-parallel with fp64 atomics for split rows

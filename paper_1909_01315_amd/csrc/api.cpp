@@ -119,7 +119,7 @@ gnnk_status out_desc(const gnnk_tensor* t, Kind k, const Geo& g, OutDev& o) {
     }
     o.reduce = 1;
     if (g.nchunk > 1) return fail(GNNK_EUNSUPPORTED, "reduced outputs need D / vec <= 64");
-    if (k == K_HEADS) {
+    if (k == K_HEADS && g.F != g.D) {
         o.red = g.F / g.vec;
         o.per_head = 1;
     } else {
@@ -215,13 +215,14 @@ struct Pick {
 };
 
 bool fast_geo(const Geo& geo, int dtype) {
-    return (geo.G == 1 || geo.G == 2 || geo.G == 4) && fast_vec(dtype, geo.vec);
+    return geo.G >= 1 && geo.G <= 32 && fast_vec(dtype, geo.vec);
 }
 
 // the compile-time layout of a g-SpMM call, when one matches
 Pick pick_spmm(const gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& geo, int dtype, int opk, bool maxmin) {
     Pick p;
-    if (options().no_fast || !fast_geo(geo, dtype)) return p;
+    // outputs summed over broadcast positions keep the runtime-layout kernels
+    if (options().no_fast || !fast_geo(geo, dtype) || A.out.reduce) return p;
     const int es = dtype == 1 ? 2 : 4;
     const int64_t nrows = table_rows(g, d, T_NBR);
     if (A.a.target != T_NBR || !A.a.full || !fits32(A.a, nrows, es)) return p;
@@ -271,18 +272,16 @@ Pick pick_sddmm(const gnnk_graph* g, const EngineArgs& A, const Geo& geo, int dt
 
 // Walk chosen for a pass: 0 the row engine, else the edge-parallel (COO)
 // walk, 2 deterministic or 3 with atomics (g-SpMM; g-SDDMM has no
-// reduction).  Automatic choice, from the degree histogram: the row engine
-// for g-SpMM (measured faster on both power-law graphs of the benchmark
-// set), and for g-SDDMM unless at least 10% of the edges sit in rows of
-// degree <= 64, where the per-row overhead of the row engine (one wavefront
-// per short row, partly idle slots) exceeds the cost of reading the
-// destination operand per edge.
-int pick_walk(const Dir& d, const Geo& geo, bool reduced_out, bool sddmm) {
+// reduction).  The automatic choice is the row engine: with compile-time
+// layouts for 1-32 lane groups it is faster than the edge walk for g-SpMM
+// and g-SDDMM at every feature width from 1 to 128 on a constant-degree
+// graph and on both power-law graphs of the benchmark set (the sensitivity
+// sweep, python -m paper_1909_01315_amd.sweep); the edge walk stays
+// available as an explicit schedule.
+int pick_walk(const Dir& d, bool reduced_out) {
     const int64_t o = options().schedule;
     if (o == 1 || reduced_out || d.n_rows == 0) return 0;
-    if (o >= 2) return (int)o;
-    (void)geo;
-    return (sddmm && d.low_deg_share >= 0.1) ? 2 : 0;
+    return o >= 2 ? (int)o : 0;
 }
 
 // positions per lane group of an edge-parallel walk: enough lane groups to
@@ -304,7 +303,7 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
     A.sch = schedule(d, geo, true);
     A.partial_stride = geo.D;
     const Pick pk = pick_spmm(g, d, A, geo, dtype, opk, false);
-    const int walk = pick_walk(d, geo, A.out.reduce != 0, false);
+    const int walk = pick_walk(d, A.out.reduce != 0);
     if (walk) {
         set_edge_chunks(A, g->n_edges, geo);
         const size_t need = walk == 3 ? (size_t)d.n_rows * geo.D * 8 : (size_t)2 * A.n_sub * geo.D * 8;
@@ -343,7 +342,7 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
     set_geo(A, geo);
     A.sch = schedule(g->in, geo, false);
     const Pick pk = pick_sddmm(g, A, geo, dtype, opk);
-    if (pick_walk(g->in, geo, false, true)) {
+    if (pick_walk(g->in, false)) {
         set_edge_chunks(A, g->n_edges, geo);
         return launch_status(launch_sddmm_edge(A, g->n_edges, dtype, geo.vec, opk, pk.spec, pk.gc, s),
                              "edge-parallel g-SDDMM launch");

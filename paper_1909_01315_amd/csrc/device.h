@@ -531,6 +531,17 @@ __device__ __forceinline__ int wave_id() {
         default: { constexpr int V = 1; __VA_ARGS__; } break; \
     }
 
+// lane groups of a fast spec
+#define GNNK_GC_DISPATCH(GC_, ...)                                \
+    switch (GC_) {                                                \
+        case 1: { constexpr int C = 1; __VA_ARGS__; } break;      \
+        case 2: { constexpr int C = 2; __VA_ARGS__; } break;      \
+        case 4: { constexpr int C = 4; __VA_ARGS__; } break;      \
+        case 8: { constexpr int C = 8; __VA_ARGS__; } break;      \
+        case 16: { constexpr int C = 16; __VA_ARGS__; } break;    \
+        default: { constexpr int C = 32; __VA_ARGS__; } break;    \
+    }
+
 #define GNNK_OPK_DISPATCH(OPK_, ...)                          \
     switch (OPK_) {                                           \
         case 0: { constexpr int K = 0; __VA_ARGS__; } break;  \

@@ -304,9 +304,7 @@ void spmm_edge_t(const EngineArgs& a, int64_t n_pos, int opk, int ext, int spec,
                                        a, n_pos);
                 }
             };
-            if (gc == 1) go(std::integral_constant<int, 1>{});
-            else if (gc == 2) go(std::integral_constant<int, 2>{});
-            else go(std::integral_constant<int, 4>{});
+            GNNK_GC_DISPATCH(gc, go(std::integral_constant<int, C>{}))
             return;
         }
     }
@@ -333,9 +331,7 @@ void sddmm_edge_t(const EngineArgs& a, int64_t n_pos, int opk, int ext, int spec
                     hipLaunchKernelGGL((sddmm_edge_kernel<T, V, 2, EXT_NONE, 0, SpUV<C>>), grid, block, 0, s, a, n_pos);
                 }
             };
-            if (gc == 1) go(std::integral_constant<int, 1>{});
-            else if (gc == 2) go(std::integral_constant<int, 2>{});
-            else go(std::integral_constant<int, 4>{});
+            GNNK_GC_DISPATCH(gc, go(std::integral_constant<int, C>{}))
             return;
         }
     }

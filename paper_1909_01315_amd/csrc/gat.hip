@@ -288,17 +288,11 @@ template <typename T, int V, bool ATTN>
 void gat_launch_t(const EngineArgs& a, const GatArgs& g, int gc, hipStream_t s) {
     const dim3 grid(blocks_for_waves(a.sch.w_total)), block(WAVE * WPB);
     if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
-        if (gc == 1) {
-            hipLaunchKernelGGL((gat_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, 1, false>, ATTN>), grid,
-                               block, 0, s, a, g);
-            return;
-        } else if (gc == 2) {
-            hipLaunchKernelGGL((gat_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, 2, false>, ATTN>), grid,
-                               block, 0, s, a, g);
-            return;
-        } else if (gc == 4) {
-            hipLaunchKernelGGL((gat_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, 4, false>, ATTN>), grid,
-                               block, 0, s, a, g);
+        if (gc > 0) {
+            GNNK_GC_DISPATCH(gc, {
+                hipLaunchKernelGGL((gat_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, C, false>, ATTN>), grid,
+                                   block, 0, s, a, g);
+            })
             return;
         }
     }

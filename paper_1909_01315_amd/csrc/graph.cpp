@@ -156,11 +156,6 @@ void schedule_dir(const std::vector<int64_t>& ptr, int64_t n_rows, int64_t S, Ho
     d.sorted_deg.resize((size_t)n_rows);
     for (int64_t k = 0; k < n_rows; ++k) d.sorted_deg[(size_t)k] = h.deg[(size_t)h.perm[(size_t)k]];
     h.max_deg = n_rows ? d.sorted_deg[0] : 0;
-    {
-        int64_t low = 0, all = ptr[n_rows] - ptr[0];
-        for (int64_t k = n_rows - 1; k >= 0 && d.sorted_deg[(size_t)k] <= 64; --k) low += d.sorted_deg[(size_t)k];
-        d.low_deg_share = all > 0 ? (double)low / (double)all : 0.0;
-    }
     h.n_nz = d.count_above(0);
     h.n_hub = d.count_above(S);
     h.hub_off.assign((size_t)h.n_hub + 1, 0);

@@ -27,7 +27,6 @@ struct Dir {
     int32_t* row = nullptr;        // device row of each position (COO form)
     int32_t* pos = nullptr;        // device position of each edge id in this CSR
     int64_t n_seg = 0, n_hub = 0, n_nz = 0, max_deg = 0;
-    double low_deg_share = 0.0;       // share of the edges in rows of degree <= 64
     std::vector<int32_t> sorted_deg;  // host, descending (bin boundaries by binary search)
     int64_t count_above(int64_t t) const;  // rows with degree > t
 };

@@ -124,9 +124,7 @@ void launch_sddmm_t(const EngineArgs& a, int opk, int ext, int spec, int gc, dim
     if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
         if (spec == SP_UV || spec == SP_VU) {
             const int rm = a.out.reduce ? 1 : 0;
-            if (gc == 1) launch_sddmm_fast<T, V, 1>(a, opk, spec, rm, grid, block, s);
-            else if (gc == 2) launch_sddmm_fast<T, V, 2>(a, opk, spec, rm, grid, block, s);
-            else launch_sddmm_fast<T, V, 4>(a, opk, spec, rm, grid, block, s);
+            GNNK_GC_DISPATCH(gc, launch_sddmm_fast<T, V, C>(a, opk, spec, rm, grid, block, s))
             return;
         }
     }

@@ -364,13 +364,6 @@ using SpUER = Spec<T_NBR, OK_FULL, T_EDGE, OK_ROW, GC, CB>;
 template <int GC>
 using SpCU = Spec<T_NBR, OK_FULL, DYN, DYN, GC, false>;
 
-#define GNNK_GC_DISPATCH(GC_, ...)                               \
-    switch (GC_) {                                               \
-        case 1: { constexpr int C = 1; __VA_ARGS__; } break;     \
-        case 2: { constexpr int C = 2; __VA_ARGS__; } break;     \
-        default: { constexpr int C = 4; __VA_ARGS__; } break;    \
-    }
-
 template <typename T, int V>
 void launch_sum_t(const EngineArgs& a, int opk, int ext, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
     if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {

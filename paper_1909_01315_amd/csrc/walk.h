@@ -5,13 +5,14 @@
 // b + g, b + g + G, ...; a batch is UNR consecutive positions per group, so
 // G * UNR consecutive positions per wavefront.
 //
-// Under a fast spec (G known at compile time) full batches are software
-// pipelined: the neighbour and edge ids of a batch come from scalar loads
-// issued two batches ahead (waited on through the scalar counter, so they
-// never wait behind the vector gathers), the gathers of batch i + 1 are in
-// flight while batch i is combined, and a per-edge head or row value of b
-// (the attention weights) is read with one coalesced load per batch and
-// moved to its lanes with ds_bpermute.  The last, partial batch and every
+// Under a fast spec (G known at compile time) full batches have no per-slot
+// selects.  With G <= 4 the neighbour and edge ids of a batch come from
+// scalar loads issued one batch ahead (waited on through the scalar counter,
+// so they never wait behind the vector gathers); with G >= 8 (a scalar
+// batch would need 32-128 scalar registers) every lane loads its group's
+// ids, the next batch's after this batch's gathers.  A per-edge head or row
+// value of b (the attention weights) is read with one coalesced load per
+// batch and moved to its lanes with ds_bpermute.  The last, partial batch and every
 // batch of a runtime-G call read their ids per lane, clamp positions past
 // the row end to the row start (always in bounds) and drop those slots.
 //
@@ -69,7 +70,7 @@ __device__ __forceinline__ int32_t pick(const int32_t* v, int u, int g) {
         const int32_t x1 = __builtin_amdgcn_readfirstlane(v[2 * u + 1]);
         return (g & 1) ? x1 : x0;
     } else {
-        static_assert(GC == 4, "fast specs use 1, 2 or 4 lane groups");
+        static_assert(GC == 4, "scalar id batches serve 1, 2 or 4 lane groups");
         const int32_t x0 = __builtin_amdgcn_readfirstlane(v[4 * u]);
         const int32_t x1 = __builtin_amdgcn_readfirstlane(v[4 * u + 1]);
         const int32_t x2 = __builtin_amdgcn_readfirstlane(v[4 * u + 2]);
@@ -80,20 +81,17 @@ __device__ __forceinline__ int32_t pick(const int32_t* v, int u, int g) {
     }
 }
 
-// Issue the loads of one full batch at position q (uniform) from its ids.
+// Issue the loads of one full batch at position q (uniform), slot u of
+// lane group g being position q + g + GC * u with ids nb[u], ed[u].
 template <typename T, int VEC, int OPK, int EXT, class S>
-__device__ __forceinline__ void issue_batch(const EngineArgs& A, const Ids<S::GC * UNR>& s, int64_t q, int g,
-                                            int32_t self, int col0, int h, const Pre<VEC>& pre, Raw<VEC>* r,
-                                            int32_t* nb, int32_t* ed, float& cbv) {
+__device__ __forceinline__ void issue_slots(const EngineArgs& A, const int32_t* nb, const int32_t* ed, int64_t q,
+                                            int g, int32_t self, int col0, int h, const Pre<VEC>& pre, Raw<VEC>* r,
+                                            float& cbv) {
     constexpr int GC = S::GC;
 #pragma unroll
     for (int u = 0; u < UNR; ++u) fetch_bits<VEC, EXT>(A, (int32_t)q + g + GC * u, col0, r[u]);
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-        nb[u] = pick<GC>(s.nb, u, g);
-        ed[u] = pick<GC>(s.ed, u, g);
-        fetch<T, VEC, OPK, EXT, S>(A, nb[u], ed[u], self, col0, h, pre, r[u]);
-    }
+    for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT, S>(A, nb[u], ed[u], self, col0, h, pre, r[u]);
     if constexpr (S::CB && OPK >= 1) {
         // lane l reads element (l mod Hb) of edge q + l / Hb; lanes past the
         // batch read the batch's first value
@@ -103,6 +101,30 @@ __device__ __forceinline__ void issue_batch(const EngineArgs& A, const Ids<S::GC
         const int l = lane < (NBT << hb) ? lane : 0;
         const T* p = reinterpret_cast<const T*>(A.b.data) + q * A.b.stride;
         cbv = IO<T, 1>::load1(p + (uint32_t)(l >> hb) * (uint32_t)A.b.stride + (l & ((1 << hb) - 1)));
+    }
+}
+
+// the same with the ids taken from the scalar batch (GC <= 4)
+template <typename T, int VEC, int OPK, int EXT, class S>
+__device__ __forceinline__ void issue_batch(const EngineArgs& A, const Ids<S::GC * UNR>& s, int64_t q, int g,
+                                            int32_t self, int col0, int h, const Pre<VEC>& pre, Raw<VEC>* r,
+                                            int32_t* nb, int32_t* ed, float& cbv) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        nb[u] = pick<S::GC>(s.nb, u, g);
+        ed[u] = pick<S::GC>(s.ed, u, g);
+    }
+    issue_slots<T, VEC, OPK, EXT, S>(A, nb, ed, q, g, self, col0, h, pre, r, cbv);
+}
+
+// per-lane ids of a full batch (GC >= 8: a scalar batch would need too many
+// scalar registers); every lane of group g reads its group's ids
+__device__ __forceinline__ void vload_ids(const CsrDev& C, int64_t q, int g, int GC, int32_t* nb, int32_t* ed) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        const int32_t p = (int32_t)q + g + GC * u;
+        nb[u] = C.idx[p];
+        ed[u] = C.eid ? C.eid[p] : p;
     }
 }
 
@@ -183,49 +205,43 @@ __device__ __forceinline__ void walk_row(const EngineArgs& A, int32_t self, int6
     } else {
         constexpr int NBT = S::GC * UNR;
         const int64_t nfull = (e - b) / NBT;
-#if GNNK_PIPE2
-        if (nfull > 0) {
-            Ids<NBT> ia, ib;
-            Raw<VEC> ra[UNR], rb[UNR];
-            int32_t na[UNR], ea[UNR], nbb[UNR], eb[UNR];
-            float ca = 0.0f, cb = 0.0f;
-            sload_ids<NBT>(A.csr, b, ia);
-            if (nfull > 1) sload_ids<NBT>(A.csr, b + NBT, ib);
-            issue_batch<T, VEC, OPK, EXT, S>(A, ia, b, g, self, col0, h, pre, ra, na, ea, ca);
-            for (int64_t i = 0;; i += 2) {
-                const int64_t q = b + i * NBT;
-                if (i + 1 < nfull) {
-                    issue_batch<T, VEC, OPK, EXT, S>(A, ib, q + NBT, g, self, col0, h, pre, rb, nbb, eb, cb);
-                    if (i + 2 < nfull) sload_ids<NBT>(A.csr, q + 2 * NBT, ia);
+        if constexpr (S::GC <= 4) {
+            // one batch in flight per wavefront; the next batch's ids load
+            // (scalar) while this batch's gathers are in flight
+            if (nfull > 0) {
+                Ids<NBT> ia;
+                sload_ids<NBT>(A.csr, b, ia);
+                for (int64_t i = 0; i < nfull; ++i) {
+                    const int64_t q = b + i * NBT;
+                    Raw<VEC> ra[UNR];
+                    int32_t na[UNR], ea[UNR];
+                    float ca = 0.0f;
+                    issue_batch<T, VEC, OPK, EXT, S>(A, ia, q, g, self, col0, h, pre, ra, na, ea, ca);
+                    if (i + 1 < nfull) sload_ids<NBT>(A.csr, q + NBT, ia);
+                    take_batch<VEC, OPK, S>(A, ra, na, ea, ca, g, h, consume);
                 }
-                take_batch<VEC, OPK, S>(A, ra, na, ea, ca, g, h, consume);
-                if (i + 1 >= nfull) break;
-                if (i + 2 < nfull) {
-                    issue_batch<T, VEC, OPK, EXT, S>(A, ia, q + 2 * NBT, g, self, col0, h, pre, ra, na, ea, ca);
-                    if (i + 3 < nfull) sload_ids<NBT>(A.csr, q + 3 * NBT, ib);
-                }
-                take_batch<VEC, OPK, S>(A, rb, nbb, eb, cb, g, h, consume);
-                if (i + 2 >= nfull) break;
             }
-        }
-#else
-        // one batch in flight per wavefront (registers for eight wavefronts
-        // per SIMD); the next batch's ids load while this batch's gathers
-        // are in flight
-        if (nfull > 0) {
-            Ids<NBT> ia;
-            sload_ids<NBT>(A.csr, b, ia);
-            for (int64_t i = 0; i < nfull; ++i) {
-                const int64_t q = b + i * NBT;
-                Raw<VEC> ra[UNR];
+        } else {
+            // ids per lane, the next batch's loaded after this batch's gathers
+            if (nfull > 0) {
                 int32_t na[UNR], ea[UNR];
-                float ca = 0.0f;
-                issue_batch<T, VEC, OPK, EXT, S>(A, ia, q, g, self, col0, h, pre, ra, na, ea, ca);
-                if (i + 1 < nfull) sload_ids<NBT>(A.csr, q + NBT, ia);
-                take_batch<VEC, OPK, S>(A, ra, na, ea, ca, g, h, consume);
+                vload_ids(A.csr, b, g, S::GC, na, ea);
+                for (int64_t i = 0; i < nfull; ++i) {
+                    const int64_t q = b + i * NBT;
+                    Raw<VEC> ra[UNR];
+                    float ca = 0.0f;
+                    issue_slots<T, VEC, OPK, EXT, S>(A, na, ea, q, g, self, col0, h, pre, ra, ca);
+                    int32_t nc[UNR], ec[UNR];
+#pragma unroll
+                    for (int u = 0; u < UNR; ++u) {
+                        nc[u] = na[u];
+                        ec[u] = ea[u];
+                    }
+                    if (i + 1 < nfull) vload_ids(A.csr, q + NBT, g, S::GC, na, ea);
+                    take_batch<VEC, OPK, S>(A, ra, nc, ec, ca, g, h, consume);
+                }
             }
         }
-#endif
         const int64_t t0 = b + nfull * NBT;
         if (t0 < e) walk_strided<T, VEC, OPK, EXT, S>(A, self, b, e, t0 - b + g, S::GC, col0, h, pre, consume);
     }

@@ -180,6 +180,20 @@ def uniform_graph(seed: int, n_src: int, n_dst: int, n_edges: int, self_loops: b
     return Graph(name, n_src, n_dst, src, dst)
 
 
+def knn_graph(seed: int, n: int, k: int, name: str = "knn") -> Graph:
+    """Constant in-degree graph (a k-nearest-neighbour graph's shape): every
+    node receives k edges from uniform random sources (Appendix D's
+    sensitivity study contrasts such graphs with power-law ones)."""
+    lib = _load()
+    src = np.empty(n * k, dtype=np.int32)
+    dummy = np.empty(n * k, dtype=np.int32)
+    if n * k:
+        lib.synth_uniform_edges(seed, stream_id("knn"), n * k, n, n, _ptr(src), _ptr(dummy))
+    dst = np.repeat(np.arange(n, dtype=np.int32), k)
+    src, dst = sort_coo(src, dst, n, n)
+    return Graph(name, n, n, src, dst)
+
+
 def graph_c1() -> Graph:
     g = uniform_graph(SEED_BASE + 1, 1024, 1024, 16384, self_loops=True, name="c1")
     return g
