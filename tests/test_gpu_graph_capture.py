@@ -1,0 +1,102 @@
+"""The library under HIP graph capture: a GAT layer forward + backward and a
+SAGE-mean aggregation captured once into a torch.cuda.CUDAGraph (HIP graph on
+ROCm) and replayed several times, with eager work and synchronisations
+between replays; every replay must equal the eager result bit for bit (the
+kernels are deterministic, and no call inside issues hipMemsetAsync, whose
+graph nodes have misbehaved on replays).  Scratch buffers are sized by an
+eager warm-up call before capture."""
+import numpy as np
+import pytest
+import torch
+
+from paper_1909_01315_amd import gnnk, nn, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def test_gat_and_sage_replay_equals_eager():
+    sg = synth.graph_c2()
+    dev = "cuda"
+    g = gnnk.Graph.from_coo(torch.from_numpy(sg.src).to(dev), torch.from_numpy(sg.dst).to(dev), sg.n_src, sg.n_dst)
+    torch.manual_seed(11)
+    N = sg.n_src
+    X = torch.randn(N, 8, 16, device=dev)
+    el = torch.randn(N, 8, 1, device=dev)
+    er = torch.randn(N, 8, 1, device=dev)
+    dZ = torch.randn(N, 8, 16, device=dev)
+    H = torch.randn(N, 1, 64, device=dev)
+
+    def step():
+        s = gnnk.gsddmm(g, "add", el, "u", er, "v")
+        s2 = gnnk.edge_leaky_relu(s, 0.2)
+        a = gnnk.edge_softmax(g, s2)
+        z = gnnk.gspmm(g, "mul", "sum", X, a)
+        dx, da = gnnk.gspmm_backward(g, "mul", "sum", X, a, dZ)
+        ds = gnnk.edge_leaky_relu_backward(s, gnnk.edge_softmax_backward(g, a, da), 0.2)
+        d_el, d_er = gnnk.gsddmm_backward(g, "add", el, "u", er, "v", ds)
+        m = gnnk.gspmm(g, "copy_lhs", "mean", H)
+        fz = gnnk.gat_aggregate(g, X, el, er, 0.2)
+        return [z, dx, da, d_el, d_er, m, fz]
+
+    eager = [t.clone() for t in step()]  # also sizes the scratch buffers
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        outs = step()
+    for rep in range(4):
+        for t in outs:
+            t.fill_(float("nan"))
+        graph.replay()
+        torch.cuda.synchronize()
+        for k, (a, b) in enumerate(zip(outs, eager)):
+            assert torch.equal(a, b), f"replay {rep}: output {k} differs from eager"
+        _ = (X * 2).sum().item()  # eager work between replays
+    g.destroy()
+
+
+def test_small_graph_step_time_graph_vs_eager():
+    """On a small graph every call is launch-bound; the captured step must
+    not be slower than the eager one (printed for the record)."""
+    sg = synth.graph_c2()
+    dev = "cuda"
+    g = gnnk.Graph.from_coo(torch.from_numpy(sg.src).to(dev), torch.from_numpy(sg.dst).to(dev), sg.n_src, sg.n_dst)
+    X = torch.randn(sg.n_src, 1, 64, device=dev)
+    w = torch.from_numpy(sg.extra["gcn_w"]).to(dev).view(-1, 1, 1)
+    out = torch.empty(sg.n_dst, 1, 64, device=dev)
+
+    def step():
+        for _ in range(10):
+            gnnk.gspmm(g, "mul", "sum", X, w, out=out)
+
+    step()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+
+    def timed(fn, n=20):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        e1.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    t_eager, t_graph = timed(step), timed(graph.replay)
+    print(f"c2 10 x gspmm u_mul_e/sum D=64: eager {t_eager * 1e3:.1f} us, graph replay {t_graph * 1e3:.1f} us")
+    assert t_graph <= t_eager * 1.1
+    g.destroy()
