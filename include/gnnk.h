@@ -110,9 +110,12 @@ typedef struct {
  * out-degrees, rows sorted by degree for scheduling, and the segment tables
  * of rows longer than seg_edges.  Derived arrays live in a caller-allocated
  * device workspace of graph_workspace_bytes() bytes, which the caller keeps
- * alive (with any borrowed index arrays) until graph_destroy.  Building is
- * done by the host library: the index arrays are copied to the host once,
- * which synchronises `stream`. */
+ * alive (with any borrowed index arrays) until graph_destroy.  Building runs
+ * on the device, on `stream`: stable radix sorts of (row, edge id) pairs, so
+ * each row lists its edges in ascending edge id, row offsets by binary search
+ * in the sorted rows, and rows ordered by descending degree (ties by row id).
+ * The call synchronises `stream` twice (after checking the input, and to read
+ * back the sorted degrees) and may allocate the handle's scratch buffer. */
 
 /* Upper bound of the workspace for a graph of this size; ptr_t is the width
  * of the CSR row offsets the handle builds (GNNK_I64 needed when
@@ -123,7 +126,8 @@ gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_
 /* From an edge list in edge-id order: edge e goes src[e] -> dst[e] (device
  * int32 arrays of num_edges entries, only read during the call).  Edges of a
  * destination keep ascending edge id in the in-CSR, edges of a source keep
- * ascending edge id in the out-CSR.  Multi-edges and self-loops are legal. */
+ * ascending edge id in the out-CSR.  Multi-edges and self-loops are legal; an
+ * endpoint out of range returns GNNK_EINVAL. */
 gnnk_status graph_create_coo(int64_t num_src, int64_t num_dst, int64_t num_edges, const int32_t* src,
                              const int32_t* dst, gnnk_itype ptr_t, void* workspace, size_t ws_bytes,
                              hipStream_t stream, gnnk_graph_t* out);
@@ -132,7 +136,9 @@ gnnk_status graph_create_coo(int64_t num_src, int64_t num_dst, int64_t num_edges
  * int32 source ids) and eids (num_edges int32 edge ids, or NULL when the edge
  * id is the position).  These device arrays are borrowed, not copied: keep
  * them unchanged until graph_destroy.  Rows must be ascending in position
- * (indptr non-decreasing, indptr[0] == 0, indptr[num_dst] == num_edges). */
+ * (indptr non-decreasing, indptr[0] == 0, indptr[num_dst] == num_edges),
+ * indices below num_src, and eids a permutation of 0..num_edges-1; any
+ * violation returns GNNK_EINVAL and builds nothing. */
 gnnk_status graph_create_csr(int64_t num_src, int64_t num_dst, int64_t num_edges, const void* indptr,
                              gnnk_itype ptr_t, const int32_t* indices, const int32_t* eids, void* workspace,
                              size_t ws_bytes, hipStream_t stream, gnnk_graph_t* out);

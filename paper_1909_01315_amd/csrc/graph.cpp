@@ -2,9 +2,10 @@
 // the original edge ids (Appendix A, definition of the reverse graph), the
 // degree arrays, rows sorted by degree, and the segment tables of hub rows.
 //
-// The structures are built on the host from one copy of the index arrays
-// (stable counting sorts, so the edges of a node keep ascending edge id) and
-// uploaded into the caller's workspace.
+// Every structure is built on the device (build.hip: stable radix sorts, so
+// the edges of a node keep ascending edge id) into the caller's workspace.
+// The host reads back only a flag word and the sorted degrees, from which it
+// derives the role boundaries of the schedule and the hub segment offsets.
 #include <stdio.h>
 #include <string.h>
 
@@ -76,11 +77,18 @@ namespace {
 
 constexpr size_t ALIGN = 256;
 
+// flag bits of the validation and build kernels
+constexpr int32_t FLAG_INDEX = 1;     // an endpoint or index out of range
+constexpr int32_t FLAG_PTR = 2;       // row offsets not a valid CSR
+constexpr int32_t FLAG_PERM = 4;      // edge ids not a permutation
+constexpr int32_t FLAG_NOT_IDENT = 8; // edge ids differ from in-CSR positions
+
+// Fixed-size regions first, then the hub tables whose sizes are known only
+// once the degrees are sorted.
 struct Layout {
     size_t in_ptr = 0, in_idx = 0, in_eid = 0, out_ptr = 0, out_idx = 0, out_eid = 0;
-    size_t in_deg = 0, out_deg = 0, in_perm = 0, out_perm = 0;
-    size_t in_seg = 0, out_seg = 0, in_hub = 0, out_hub = 0, in_row = 0, out_row = 0, out_pos = 0, flag = 0,
-           total = 0;
+    size_t in_deg = 0, out_deg = 0, in_perm = 0, out_perm = 0, in_row = 0, out_row = 0, out_pos = 0, flag = 0;
+    size_t in_hub = 0, out_hub = 0, in_seg = 0, out_seg = 0, total = 0;
 };
 
 struct Bump {
@@ -92,15 +100,13 @@ struct Bump {
     }
 };
 
-Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, bool own_in, bool in_eid, int64_t seg_in,
-                   int64_t seg_out, int64_t hub_in, int64_t hub_out) {
+Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t hub_in, int64_t hub_out, int64_t seg_in,
+                   int64_t seg_out) {
     Layout L;
     Bump b;
-    if (own_in) {
-        L.in_ptr = b.take((size_t)(n_dst + 1) * ps);
-        L.in_idx = b.take((size_t)E * 4);
-    }
-    if (in_eid) L.in_eid = b.take((size_t)E * 4);
+    L.in_ptr = b.take((size_t)(n_dst + 1) * ps);
+    L.in_idx = b.take((size_t)E * 4);
+    L.in_eid = b.take((size_t)E * 4);
     L.out_ptr = b.take((size_t)(n_src + 1) * ps);
     L.out_idx = b.take((size_t)E * 4);
     L.out_eid = b.take((size_t)E * 4);
@@ -108,14 +114,14 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, bool own_
     L.out_deg = b.take((size_t)n_src * 4);
     L.in_perm = b.take((size_t)n_dst * 4);
     L.out_perm = b.take((size_t)n_src * 4);
-    L.in_seg = b.take((size_t)seg_in * 16);
-    L.out_seg = b.take((size_t)seg_out * 16);
-    L.in_hub = b.take((size_t)(hub_in + 1) * 4);
-    L.out_hub = b.take((size_t)(hub_out + 1) * 4);
     L.in_row = b.take((size_t)E * 4);
     L.out_row = b.take((size_t)E * 4);
     L.out_pos = b.take((size_t)E * 4);
     L.flag = b.take(ALIGN);
+    L.in_hub = b.take((size_t)(hub_in + 1) * 4);
+    L.out_hub = b.take((size_t)(hub_out + 1) * 4);
+    L.in_seg = b.take((size_t)seg_in * 16);
+    L.out_seg = b.take((size_t)seg_out * 16);
     L.total = b.off;
     return L;
 }
@@ -124,160 +130,233 @@ bool sizes_ok(int64_t n_src, int64_t n_dst, int64_t E) {
     return n_src >= 0 && n_dst >= 0 && E >= 0 && n_src < INT32_MAX && n_dst < INT32_MAX && E < INT32_MAX;
 }
 
-// edges of each row in ascending edge id (stable counting sort by key)
-void counting_csr(int64_t n_rows, int64_t E, const int32_t* key, const int32_t* other, std::vector<int64_t>& ptr,
-                  std::vector<int32_t>& idx, std::vector<int32_t>& eid) {
-    ptr.assign((size_t)n_rows + 1, 0);
-    for (int64_t e = 0; e < E; ++e) ptr[(size_t)key[e] + 1]++;
-    for (int64_t r = 0; r < n_rows; ++r) ptr[r + 1] += ptr[r];
-    std::vector<int64_t> fill(ptr.begin(), ptr.end() - 1);
-    idx.resize((size_t)E);
-    eid.resize((size_t)E);
-    for (int64_t e = 0; e < E; ++e) {
-        int64_t p = fill[(size_t)key[e]]++;
-        idx[(size_t)p] = other[e];
-        eid[(size_t)p] = (int32_t)e;
-    }
+// bits of a row id below n_rows
+int row_bits(int64_t n_rows) { return key_bits(n_rows > 1 ? (uint64_t)(n_rows - 1) : 0); }
+
+// one traversal direction's derived host state from its sorted degrees
+void schedule_host(Dir& d, int64_t S, std::vector<int32_t>& hub_off) {
+    d.max_deg = d.n_rows ? d.sorted_deg[0] : 0;
+    d.n_nz = d.count_above(0);
+    d.n_hub = d.count_above(S);
+    hub_off.assign((size_t)d.n_hub + 1, 0);
+    for (int64_t k = 0; k < d.n_hub; ++k)
+        hub_off[(size_t)k + 1] = hub_off[(size_t)k] + (int32_t)((d.sorted_deg[(size_t)k] + S - 1) / S);
+    d.n_seg = hub_off[(size_t)d.n_hub];
 }
 
-struct HostDir {
-    std::vector<int32_t> deg, perm, hub_off;
-    std::vector<int4> seg;
-    int64_t n_nz = 0, n_hub = 0, max_deg = 0;
+struct Builder {
+    gnnk_graph* g;
+    char* W;
+    Layout L;
+    uint32_t* scratch = nullptr;
+    hipStream_t s;
+    hipError_t err = hipSuccess;
+
+    void chk(hipError_t x) {
+        if (err == hipSuccess) err = x;
+    }
+    template <typename T>
+    T* at(size_t off) {
+        return reinterpret_cast<T*>(W + off);
+    }
+    int32_t read_flag() {
+        int32_t h = 0;
+        chk(hipMemcpyAsync(&h, g->flag, 4, hipMemcpyDeviceToHost, s));
+        chk(hipStreamSynchronize(s));
+        return h;
+    }
+
+    // radix scratch, plus four row-sized buffers for the degree order
+    bool get_scratch() {
+        const int64_t n = std::max(g->n_src, g->n_dst);
+        const size_t words = std::max(radix_scratch_words(g->n_edges), 4 * (size_t)(n + 64) + radix_scratch_words(n));
+        scratch = reinterpret_cast<uint32_t*>(graph_scratch(g, words * 4));
+        return scratch != nullptr;
+    }
+
+    // the reverse graph's CSR from the source and destination of every edge id
+    void build_reverse(const int32_t* src_of_e, const int32_t* dst_of_e) {
+        const int64_t E = g->n_edges;
+        Dir& d = g->out;
+        d.ptr = W + L.out_ptr;
+        d.idx = at<int32_t>(L.out_idx);
+        d.eid = at<int32_t>(L.out_eid);
+        d.row = at<int32_t>(L.out_row);
+        d.pos = at<int32_t>(L.out_pos);
+        chk(radix_sort_pairs(reinterpret_cast<const uint32_t*>(src_of_e), nullptr, E, row_bits(g->n_src),
+                             at<uint32_t>(L.out_row), at<uint32_t>(L.out_eid), at<uint32_t>(L.out_idx),
+                             at<uint32_t>(L.out_pos), scratch, s));
+        chk(launch_ptr_from_keys(at<uint32_t>(L.out_row), E, g->n_src, W + L.out_ptr, g->ptr64, s));
+        chk(launch_gather(dst_of_e, at<uint32_t>(L.out_eid), E, at<int32_t>(L.out_idx), s));
+        chk(launch_inverse(at<int32_t>(L.out_eid), E, at<int32_t>(L.out_pos), s));
+    }
+
+    // degrees and rows by descending degree (ties by row id) on the device;
+    // the sorted degrees are copied into d.sorted_deg (complete after the
+    // next synchronisation of s)
+    void order_rows(Dir& d, std::vector<uint32_t>& keys_h) {
+        const int64_t n = d.n_rows, E = g->n_edges;
+        const int64_t pad = (n + 63) / 64 * 64;
+        uint32_t* key = scratch;
+        uint32_t* sorted = key + pad;
+        uint32_t* tk = sorted + pad;
+        uint32_t* tv = tk + pad;
+        uint32_t* rs = tv + pad;
+        chk(launch_degrees(d.ptr, g->ptr64, n, d.deg, key, (uint32_t)E, s));
+        chk(radix_sort_pairs(key, nullptr, n, key_bits((uint64_t)E), sorted, reinterpret_cast<uint32_t*>(d.perm), tk,
+                             tv, rs, s));
+        keys_h.resize((size_t)n);
+        if (n > 0) chk(hipMemcpyAsync(keys_h.data(), sorted, (size_t)n * 4, hipMemcpyDeviceToHost, s));
+    }
+
+    // common tail: degree order, identity flag, hub tables
+    gnnk_status finish(size_t ws_bytes, bool check_identity) {
+        const int64_t E = g->n_edges;
+        Dir& in = g->in;
+        Dir& out = g->out;
+        in.n_rows = g->n_dst;
+        out.n_rows = g->n_src;
+        in.deg = at<int32_t>(L.in_deg);
+        out.deg = at<int32_t>(L.out_deg);
+        in.perm = at<int32_t>(L.in_perm);
+        out.perm = at<int32_t>(L.out_perm);
+        std::vector<uint32_t> kin, kout;
+        order_rows(in, kin);
+        order_rows(out, kout);
+        const int32_t h = read_flag();  // also completes the two copies above
+        if (err != hipSuccess) return hip_fail(err, "graph build");
+        if (check_identity) {
+            g->identity_eids = !(h & FLAG_NOT_IDENT);
+            if (g->identity_eids) in.eid = nullptr;
+        }
+        in.sorted_deg.resize(kin.size());
+        for (size_t k = 0; k < kin.size(); ++k) in.sorted_deg[k] = (int32_t)((uint32_t)E - kin[k]);
+        out.sorted_deg.resize(kout.size());
+        for (size_t k = 0; k < kout.size(); ++k) out.sorted_deg[k] = (int32_t)((uint32_t)E - kout[k]);
+        std::vector<int32_t> hin, hout;
+        schedule_host(in, g->seg_edges, hin);
+        schedule_host(out, g->seg_edges, hout);
+        L = make_layout(g->n_src, g->n_dst, E, g->ptr64 ? 8 : 4, in.n_hub, out.n_hub, in.n_seg, out.n_seg);
+        if (ws_bytes < L.total)
+            return fail(GNNK_ENOMEM, "workspace of %zu bytes is smaller than the %zu bytes this graph needs",
+                        ws_bytes, L.total);
+        in.hub_off = at<int32_t>(L.in_hub);
+        out.hub_off = at<int32_t>(L.out_hub);
+        in.seg = at<int4>(L.in_seg);
+        out.seg = at<int4>(L.out_seg);
+        chk(hipMemcpyAsync(in.hub_off, hin.data(), hin.size() * 4, hipMemcpyHostToDevice, s));
+        chk(hipMemcpyAsync(out.hub_off, hout.data(), hout.size() * 4, hipMemcpyHostToDevice, s));
+        chk(launch_hub_segments(in.ptr, g->ptr64, in.perm, in.hub_off, in.n_hub, g->seg_edges, in.seg, s));
+        chk(launch_hub_segments(out.ptr, g->ptr64, out.perm, out.hub_off, out.n_hub, g->seg_edges, out.seg, s));
+        chk(hipMemsetAsync(g->flag, 0, 4, s));
+        chk(hipStreamSynchronize(s));  // hin/hout are about to go away
+        if (err != hipSuccess) return hip_fail(err, "graph build");
+        g->ws_used = L.total;
+        return GNNK_OK;
+    }
 };
 
-void schedule_dir(const std::vector<int64_t>& ptr, int64_t n_rows, int64_t S, HostDir& h, Dir& d) {
-    h.deg.resize((size_t)n_rows);
-    for (int64_t r = 0; r < n_rows; ++r) h.deg[(size_t)r] = (int32_t)(ptr[r + 1] - ptr[r]);
-    h.perm.resize((size_t)n_rows);
-    std::iota(h.perm.begin(), h.perm.end(), 0);
-    std::stable_sort(h.perm.begin(), h.perm.end(),
-                     [&](int32_t a, int32_t b) { return h.deg[(size_t)a] > h.deg[(size_t)b]; });
-    d.sorted_deg.resize((size_t)n_rows);
-    for (int64_t k = 0; k < n_rows; ++k) d.sorted_deg[(size_t)k] = h.deg[(size_t)h.perm[(size_t)k]];
-    h.max_deg = n_rows ? d.sorted_deg[0] : 0;
-    h.n_nz = d.count_above(0);
-    h.n_hub = d.count_above(S);
-    h.hub_off.assign((size_t)h.n_hub + 1, 0);
-    h.seg.clear();
-    for (int64_t k = 0; k < h.n_hub; ++k) {
-        int32_t r = h.perm[(size_t)k];
-        int64_t b = ptr[r], e = ptr[r + 1];
-        h.hub_off[(size_t)k] = (int32_t)h.seg.size();
-        for (int64_t s = b; s < e; s += S)
-            h.seg.push_back(make_int4(r, (int32_t)s, (int32_t)std::min(e, s + S), (int32_t)k));
+void free_graph(gnnk_graph* g) {
+    if (g->scratch2) {
+        (void)hipDeviceSynchronize();
+        (void)hipFree(g->scratch2);
     }
-    h.hub_off[(size_t)h.n_hub] = (int32_t)h.seg.size();
-    d.n_rows = n_rows;
-    d.n_nz = h.n_nz;
-    d.n_hub = h.n_hub;
-    d.n_seg = (int64_t)h.seg.size();
-    d.max_deg = h.max_deg;
+    if (g->scratch) {
+        (void)hipDeviceSynchronize();
+        (void)hipFree(g->scratch);
+    }
+    delete g;
 }
 
-template <typename T>
-hipError_t upload(void* dst, const T* src, size_t n, hipStream_t s) {
-    if (n == 0) return hipSuccess;
-    return hipMemcpyAsync(dst, src, n * sizeof(T), hipMemcpyHostToDevice, s);
+gnnk_graph* new_graph(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_itype ptr_t) {
+    gnnk_graph* g = new gnnk_graph();
+    g->n_src = num_src;
+    g->n_dst = num_dst;
+    g->n_edges = num_edges;
+    g->ptr64 = ptr_t == GNNK_I64;
+    g->seg_edges = options().seg_edges;
+    return g;
 }
 
-hipError_t upload_ptr(void* dst, const std::vector<int64_t>& p, int ptr64, hipStream_t s) {
-    if (ptr64) return upload(dst, p.data(), p.size(), s);
-    std::vector<int32_t> q(p.begin(), p.end());
-    hipError_t e = upload(dst, q.data(), q.size(), s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);  // q is about to go away
-    return e;
-}
-
-template <typename T>
-hipError_t download(std::vector<T>& dst, const void* src, size_t n, hipStream_t s) {
-    dst.resize(n);
-    if (n == 0) return hipSuccess;
-    hipError_t e = hipMemcpyAsync(dst.data(), src, n * sizeof(T), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    return e;
-}
-
-// Build everything from edges given by id (src_of_e, dst_of_e) and upload.
-// in_ptr/in_idx/in_eid_h describe the in-CSR to traverse (own == true: built
-// here and uploaded; false: the caller's arrays, device pointers given).
-gnnk_status finish_build(gnnk_graph* g, const std::vector<int32_t>& src_of_e, const std::vector<int32_t>& dst_of_e,
-                         const std::vector<int64_t>& in_ptr, bool own_in, const std::vector<int32_t>* in_idx_h,
-                         const std::vector<int32_t>* in_eid_h, bool in_eid_needed, const void* user_ptr,
-                         const int32_t* user_idx, const int32_t* user_eid, void* ws, size_t ws_bytes,
-                         hipStream_t s) {
-    const int64_t E = g->n_edges;
-    const size_t ps = g->ptr64 ? 8 : 4;
-    std::vector<int64_t> out_ptr;
-    std::vector<int32_t> out_idx, out_eid;
-    counting_csr(g->n_src, E, src_of_e.data(), dst_of_e.data(), out_ptr, out_idx, out_eid);
-
-    HostDir hin, hout;
-    schedule_dir(in_ptr, g->n_dst, g->seg_edges, hin, g->in);
-    schedule_dir(out_ptr, g->n_src, g->seg_edges, hout, g->out);
-
-    Layout L = make_layout(g->n_src, g->n_dst, E, ps, own_in, own_in && in_eid_needed, g->in.n_seg, g->out.n_seg,
-                           g->in.n_hub, g->out.n_hub);
-    if (!ws || ws_bytes < L.total)
+// workspace checks shared by both constructors; fills b.W, b.L, g->flag
+gnnk_status begin_build(Builder& b, void* ws, size_t ws_bytes) {
+    gnnk_graph* g = b.g;
+    b.L = make_layout(g->n_src, g->n_dst, g->n_edges, g->ptr64 ? 8 : 4, 0, 0, 0, 0);
+    if (!ws || ws_bytes < b.L.total)
         return fail(GNNK_ENOMEM, "workspace of %zu bytes is smaller than the %zu bytes this graph needs", ws_bytes,
-                    L.total);
-    char* W = reinterpret_cast<char*>(ws);
-    if ((uintptr_t)W % ALIGN) return fail(GNNK_EINVAL, "workspace must be 256-byte aligned");
-    hipError_t e = hipSuccess;
-    auto chk = [&](hipError_t x) {
-        if (e == hipSuccess) e = x;
-    };
-    if (own_in) {
-        chk(upload_ptr(W + L.in_ptr, in_ptr, g->ptr64, s));
-        chk(upload(W + L.in_idx, in_idx_h->data(), (size_t)E, s));
-        g->in.ptr = W + L.in_ptr;
-        g->in.idx = reinterpret_cast<int32_t*>(W + L.in_idx);
-        if (in_eid_needed) {
-            chk(upload(W + L.in_eid, in_eid_h->data(), (size_t)E, s));
-            g->in.eid = reinterpret_cast<int32_t*>(W + L.in_eid);
-        } else {
-            g->in.eid = nullptr;
-        }
-    } else {
-        g->in.ptr = user_ptr;
-        g->in.idx = user_idx;
-        g->in.eid = user_eid;
-    }
-    chk(upload_ptr(W + L.out_ptr, out_ptr, g->ptr64, s));
-    chk(upload(W + L.out_idx, out_idx.data(), (size_t)E, s));
-    chk(upload(W + L.out_eid, out_eid.data(), (size_t)E, s));
-    g->out.ptr = W + L.out_ptr;
-    g->out.idx = reinterpret_cast<int32_t*>(W + L.out_idx);
-    g->out.eid = reinterpret_cast<int32_t*>(W + L.out_eid);
-
-    g->in.deg = reinterpret_cast<int32_t*>(W + L.in_deg);
-    g->out.deg = reinterpret_cast<int32_t*>(W + L.out_deg);
-    g->in.perm = reinterpret_cast<int32_t*>(W + L.in_perm);
-    g->out.perm = reinterpret_cast<int32_t*>(W + L.out_perm);
-    g->in.seg = reinterpret_cast<int4*>(W + L.in_seg);
-    g->out.seg = reinterpret_cast<int4*>(W + L.out_seg);
-    g->in.hub_off = reinterpret_cast<int32_t*>(W + L.in_hub);
-    g->out.hub_off = reinterpret_cast<int32_t*>(W + L.out_hub);
-    g->in.row = reinterpret_cast<int32_t*>(W + L.in_row);
-    g->out.row = reinterpret_cast<int32_t*>(W + L.out_row);
-    g->out.pos = reinterpret_cast<int32_t*>(W + L.out_pos);
-    g->flag = reinterpret_cast<int32_t*>(W + L.flag);
-    chk(launch_fill_rows(g->in.ptr, g->ptr64, g->n_dst, E, g->in.row, s));
-    chk(launch_fill_rows(g->out.ptr, g->ptr64, g->n_src, E, g->out.row, s));
-    chk(launch_inverse(g->out.eid, E, g->out.pos, s));
-    chk(upload(g->in.deg, hin.deg.data(), hin.deg.size(), s));
-    chk(upload(g->out.deg, hout.deg.data(), hout.deg.size(), s));
-    chk(upload(g->in.perm, hin.perm.data(), hin.perm.size(), s));
-    chk(upload(g->out.perm, hout.perm.data(), hout.perm.size(), s));
-    chk(upload(g->in.seg, hin.seg.data(), hin.seg.size(), s));
-    chk(upload(g->out.seg, hout.seg.data(), hout.seg.size(), s));
-    chk(upload(g->in.hub_off, hin.hub_off.data(), hin.hub_off.size(), s));
-    chk(upload(g->out.hub_off, hout.hub_off.data(), hout.hub_off.size(), s));
-    chk(hipMemsetAsync(g->flag, 0, 4, s));
-    chk(hipStreamSynchronize(s));
-    if (e != hipSuccess) return hip_fail(e, "graph upload");
-    g->ws_used = L.total;
+                    b.L.total);
+    b.W = reinterpret_cast<char*>(ws);
+    if ((uintptr_t)b.W % ALIGN) return fail(GNNK_EINVAL, "workspace must be 256-byte aligned");
+    g->flag = b.at<int32_t>(b.L.flag);
+    b.chk(hipMemsetAsync(g->flag, 0, 4, b.s));
     return GNNK_OK;
+}
+
+gnnk_status create_coo(Builder& b, const int32_t* src, const int32_t* dst, void* ws, size_t ws_bytes) {
+    gnnk_graph* g = b.g;
+    const int64_t E = g->n_edges;
+    gnnk_status st = begin_build(b, ws, ws_bytes);
+    if (st != GNNK_OK) return st;
+    b.chk(launch_validate(src, E, g->n_src, g->flag, b.s));
+    b.chk(launch_validate(dst, E, g->n_dst, g->flag, b.s));
+    const int32_t h = b.read_flag();
+    if (b.err != hipSuccess) return hip_fail(b.err, "checking the edge list");
+    if (h & FLAG_INDEX) return fail(GNNK_EINVAL, "an edge has an endpoint out of range");
+    if (!b.get_scratch()) return fail(GNNK_ENOMEM, "scratch allocation for the graph build failed");
+    const Layout& L = b.L;
+    Dir& in = g->in;
+    in.ptr = b.W + L.in_ptr;
+    in.idx = b.at<int32_t>(L.in_idx);
+    in.eid = b.at<int32_t>(L.in_eid);
+    in.row = b.at<int32_t>(L.in_row);
+    // in-CSR: edges sorted by destination, ties in edge-id order
+    b.chk(radix_sort_pairs(reinterpret_cast<const uint32_t*>(dst), nullptr, E, row_bits(g->n_dst),
+                           b.at<uint32_t>(L.in_row), b.at<uint32_t>(L.in_eid), b.at<uint32_t>(L.out_row),
+                           b.at<uint32_t>(L.out_pos), b.scratch, b.s));
+    b.chk(launch_ptr_from_keys(b.at<uint32_t>(L.in_row), E, g->n_dst, b.W + L.in_ptr, g->ptr64, b.s));
+    b.chk(launch_gather(src, b.at<uint32_t>(L.in_eid), E, b.at<int32_t>(L.in_idx), b.s));
+    b.chk(launch_check_identity(b.at<int32_t>(L.in_eid), E, g->flag, FLAG_NOT_IDENT, b.s));
+    b.build_reverse(src, dst);
+    return b.finish(ws_bytes, true);
+}
+
+gnnk_status create_csr(Builder& b, const void* indptr, const int32_t* indices, const int32_t* eids, void* ws,
+                       size_t ws_bytes) {
+    gnnk_graph* g = b.g;
+    const int64_t E = g->n_edges;
+    gnnk_status st = begin_build(b, ws, ws_bytes);
+    if (st != GNNK_OK) return st;
+    const Layout& L = b.L;
+    b.chk(launch_validate_ptr(indptr, g->ptr64, g->n_dst, E, g->flag, b.s));
+    b.chk(launch_validate(indices, E, g->n_src, g->flag, b.s));
+    if (eids) {
+        b.chk(launch_check_permutation(eids, E, b.at<uint32_t>(L.out_pos), g->flag, FLAG_PERM, b.s));
+        b.chk(launch_check_identity(eids, E, g->flag, FLAG_NOT_IDENT, b.s));
+    }
+    const int32_t h = b.read_flag();
+    if (b.err != hipSuccess) return hip_fail(b.err, "checking the CSR");
+    if (h & FLAG_PTR)
+        return fail(GNNK_EINVAL, "indptr must start at 0, end at num_edges and never decrease");
+    if (h & FLAG_INDEX) return fail(GNNK_EINVAL, "an index is out of range");
+    if (h & FLAG_PERM) return fail(GNNK_EINVAL, "eids is not a permutation of 0..num_edges-1");
+    if (!b.get_scratch()) return fail(GNNK_ENOMEM, "scratch allocation for the graph build failed");
+    const bool identity = !eids || !(h & FLAG_NOT_IDENT);
+    g->identity_eids = identity;
+    Dir& in = g->in;
+    in.ptr = indptr;
+    in.idx = indices;
+    in.eid = identity ? nullptr : eids;
+    in.row = b.at<int32_t>(L.in_row);
+    b.chk(launch_fill_rows(indptr, g->ptr64, g->n_dst, E, in.row, b.s));
+    if (identity) {
+        b.build_reverse(indices, in.row);
+    } else {
+        int32_t* src_of_e = b.at<int32_t>(L.in_idx);
+        int32_t* dst_of_e = b.at<int32_t>(L.in_eid);
+        b.chk(launch_edge_ends(indices, eids, in.row, E, src_of_e, dst_of_e, b.s));
+        b.build_reverse(src_of_e, dst_of_e);
+    }
+    return b.finish(ws_bytes, false);
 }
 
 }  // namespace
@@ -293,9 +372,11 @@ gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_
     if (!bytes) return fail(GNNK_EINVAL, "bytes is NULL");
     if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (int32 ids)");
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
+    // hub rows have more than S edges: at most E / S of them, and at most
+    // E / S + (hub rows) <= 2 E / S segments
     int64_t S = options().seg_edges;
-    int64_t seg = 2 * num_edges / S + 2, hub = num_edges / S + 1;
-    Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, true, true, seg, seg, hub, hub);
+    int64_t hub = num_edges / S + 1, seg = 2 * num_edges / S + 2;
+    Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, hub, hub, seg, seg);
     *bytes = L.total;
     return GNNK_OK;
 }
@@ -309,33 +390,13 @@ gnnk_status graph_create_coo(int64_t num_src, int64_t num_dst, int64_t num_edges
     if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (int32 ids)");
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
     if (num_edges > 0 && (!src || !dst)) return fail(GNNK_EINVAL, "src/dst is NULL");
-    std::vector<int32_t> hs, hd;
-    hipError_t e = download(hs, src, (size_t)num_edges, stream);
-    if (e == hipSuccess) e = download(hd, dst, (size_t)num_edges, stream);
-    if (e != hipSuccess) return hip_fail(e, "reading the edge list");
-    for (int64_t i = 0; i < num_edges; ++i) {
-        if (hs[(size_t)i] < 0 || hs[(size_t)i] >= num_src || hd[(size_t)i] < 0 || hd[(size_t)i] >= num_dst)
-            return fail(GNNK_EINVAL, "edge %lld has an endpoint out of range", (long long)i);
-    }
-    gnnk_graph* g = new gnnk_graph();
-    g->n_src = num_src;
-    g->n_dst = num_dst;
-    g->n_edges = num_edges;
-    g->ptr64 = ptr_t == GNNK_I64;
-    g->seg_edges = options().seg_edges;
-    std::vector<int64_t> in_ptr;
-    std::vector<int32_t> in_idx, in_eid;
-    counting_csr(num_dst, num_edges, hd.data(), hs.data(), in_ptr, in_idx, in_eid);
-    bool identity = true;
-    for (int64_t p = 0; p < num_edges && identity; ++p) identity = in_eid[(size_t)p] == (int32_t)p;
-    g->identity_eids = identity;
-    gnnk_status st = finish_build(g, hs, hd, in_ptr, true, &in_idx, &in_eid, !identity, nullptr, nullptr, nullptr,
-                                  workspace, ws_bytes, stream);
+    Builder b{new_graph(num_src, num_dst, num_edges, ptr_t), nullptr, {}, nullptr, stream};
+    gnnk_status st = create_coo(b, src, dst, workspace, ws_bytes);
     if (st != GNNK_OK) {
-        delete g;
+        free_graph(b.g);
         return st;
     }
-    *out = g;
+    *out = b.g;
     return GNNK_OK;
 }
 
@@ -348,56 +409,13 @@ gnnk_status graph_create_csr(int64_t num_src, int64_t num_dst, int64_t num_edges
     if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (int32 ids)");
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
     if (!indptr || (num_edges > 0 && !indices)) return fail(GNNK_EINVAL, "indptr/indices is NULL");
-    std::vector<int64_t> hp;
-    std::vector<int32_t> hi, he;
-    hipError_t e;
-    if (ptr_t == GNNK_I64) {
-        e = download(hp, indptr, (size_t)num_dst + 1, stream);
-    } else {
-        std::vector<int32_t> t;
-        e = download(t, indptr, (size_t)num_dst + 1, stream);
-        hp.assign(t.begin(), t.end());
-    }
-    if (e == hipSuccess) e = download(hi, indices, (size_t)num_edges, stream);
-    if (e == hipSuccess && eids) e = download(he, eids, (size_t)num_edges, stream);
-    if (e != hipSuccess) return hip_fail(e, "reading the CSR");
-    if (hp[0] != 0 || hp[(size_t)num_dst] != num_edges)
-        return fail(GNNK_EINVAL, "indptr must start at 0 and end at num_edges");
-    for (int64_t r = 0; r < num_dst; ++r)
-        if (hp[(size_t)r + 1] < hp[(size_t)r]) return fail(GNNK_EINVAL, "indptr decreases at row %lld", (long long)r);
-    std::vector<int32_t> src_of_e((size_t)num_edges), dst_of_e((size_t)num_edges);
-    std::vector<uint8_t> seen(eids ? (size_t)num_edges : 0, 0);
-    bool identity = true;
-    for (int64_t r = 0; r < num_dst; ++r) {
-        for (int64_t p = hp[(size_t)r]; p < hp[(size_t)r + 1]; ++p) {
-            int32_t u = hi[(size_t)p];
-            if (u < 0 || u >= num_src) return fail(GNNK_EINVAL, "index %lld out of range", (long long)p);
-            int64_t eid = p;
-            if (eids) {
-                eid = he[(size_t)p];
-                if (eid < 0 || eid >= num_edges || seen[(size_t)eid])
-                    return fail(GNNK_EINVAL, "eids is not a permutation of 0..num_edges-1");
-                seen[(size_t)eid] = 1;
-                identity = identity && eid == p;
-            }
-            src_of_e[(size_t)eid] = u;
-            dst_of_e[(size_t)eid] = (int32_t)r;
-        }
-    }
-    gnnk_graph* g = new gnnk_graph();
-    g->n_src = num_src;
-    g->n_dst = num_dst;
-    g->n_edges = num_edges;
-    g->ptr64 = ptr_t == GNNK_I64;
-    g->seg_edges = options().seg_edges;
-    g->identity_eids = identity;
-    gnnk_status st = finish_build(g, src_of_e, dst_of_e, hp, false, nullptr, nullptr, false, indptr, indices,
-                                  identity ? nullptr : eids, workspace, ws_bytes, stream);
+    Builder b{new_graph(num_src, num_dst, num_edges, ptr_t), nullptr, {}, nullptr, stream};
+    gnnk_status st = create_csr(b, indptr, indices, eids, workspace, ws_bytes);
     if (st != GNNK_OK) {
-        delete g;
+        free_graph(b.g);
         return st;
     }
-    *out = g;
+    *out = b.g;
     return GNNK_OK;
 }
 
@@ -477,15 +495,7 @@ gnnk_status graph_validate(gnnk_graph_t g, hipStream_t stream) {
 gnnk_status graph_destroy(gnnk_graph_t g) {
     clear_error();
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
-    if (g->scratch2) {
-        (void)hipDeviceSynchronize();
-        (void)hipFree(g->scratch2);
-    }
-    if (g->scratch) {
-        (void)hipDeviceSynchronize();
-        (void)hipFree(g->scratch);
-    }
-    delete g;
+    free_graph(g);
     return GNNK_OK;
 }
 

@@ -150,7 +150,7 @@ enum SpecId : int32_t {
     SP_VU = 7,       // a: own row; b: neighbour row            (edge gradient dZ[v] . X[u])
 };
 
-// ----- host-side launchers (spmm.hip, sddmm.hip, softmax.hip, misc.hip) -----
+// ----- host-side launchers (spmm.hip, sddmm.hip, edge.hip, gat.hip, softmax.hip, misc.hip) -----
 // dtype: 0 fp32, 1 bf16; opk: 0 copy-a, 1 mul-ab, 2 generic; gc: lane groups
 // of a fast spec
 bool fast_vec(int dtype, int vec);
@@ -184,5 +184,37 @@ hipError_t launch_inverse(const int32_t* perm, int64_t n, int32_t* pos, hipStrea
 hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, const int32_t* pos_of_edge,
                               uint32_t* bits, int64_t n_edges, int32_t words, hipStream_t s);
 hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int64_t n, hipStream_t s);
+
+// ----- device construction of the graph formats (build.hip) -----
+// bits needed for keys in [0, max_key]
+int key_bits(uint64_t max_key);
+// uint32 words of scratch radix_sort_pairs needs for n pairs
+size_t radix_scratch_words(int64_t n);
+// Stable sort of (key, value) pairs by the low `bits` bits of the key; vals_in
+// == nullptr stands for 0..n-1.  Inputs are only read; the result lands in
+// keys_out/vals_out; tmp_keys/tmp_vals (n entries each) and scratch are
+// clobbered.  No buffer may alias another.
+hipError_t radix_sort_pairs(const uint32_t* keys_in, const uint32_t* vals_in, int64_t n, int bits,
+                            uint32_t* keys_out, uint32_t* vals_out, uint32_t* tmp_keys, uint32_t* tmp_vals,
+                            uint32_t* scratch, hipStream_t s);
+// ptr[r] = first position of the sorted keys that is >= r, r in [0, n_rows]
+hipError_t launch_ptr_from_keys(const uint32_t* keys, int64_t n_keys, int64_t n_rows, void* ptr, int ptr64,
+                                hipStream_t s);
+// deg[r] = ptr[r + 1] - ptr[r]; deg_key[r] = cap - deg[r]
+hipError_t launch_degrees(const void* ptr, int ptr64, int64_t n_rows, int32_t* deg, uint32_t* deg_key, uint32_t cap,
+                          hipStream_t s);
+// out[p] = table[idx[p]]
+hipError_t launch_gather(const int32_t* table, const uint32_t* idx, int64_t n, int32_t* out, hipStream_t s);
+// flag |= bit unless eid[p] == p for every p
+hipError_t launch_check_identity(const int32_t* eid, int64_t n, int32_t* flag, int32_t bit, hipStream_t s);
+// flag |= bit unless eid is a permutation of 0..n-1 (counts: n words of scratch)
+hipError_t launch_check_permutation(const int32_t* eid, int64_t n, uint32_t* counts, int32_t* flag, int32_t bit,
+                                    hipStream_t s);
+// src_of_e[eid[p]] = idx[p], dst_of_e[eid[p]] = row[p]
+hipError_t launch_edge_ends(const int32_t* idx, const int32_t* eid, const int32_t* row, int64_t n, int32_t* src_of_e,
+                            int32_t* dst_of_e, hipStream_t s);
+// segments of the hub rows perm[0, n_hub), starting at seg[hub_off[k]]
+hipError_t launch_hub_segments(const void* ptr, int ptr64, const int32_t* perm, const int32_t* hub_off, int64_t n_hub,
+                               int64_t seg_edges, int4* seg, hipStream_t s);
 
 }  // namespace gnnk

@@ -79,3 +79,32 @@ def assert_exact(gpu, ref, name="result"):
     else:
         bad = g != ref
     assert not bad.any(), report(name, g, ref, bad, 0)
+
+
+def check_formats(p, seg_edges=2048):
+    """Both CSRs, degrees and the schedule counts of a handle against the
+    oracle's CSR (stable counting sort by row, ascending edge id in a row)."""
+    ip, ii, ie = orc.csr(p.o, reverse=False)
+    rp, ri, re_ = orc.csr(p.o, reverse=True)
+    gp, gi, ge = p.g.csr_export(reverse=False)
+    hp, hi, he = p.g.csr_export(reverse=True)
+    assert_exact(host(gp).astype(np.int64), ip, "in indptr")
+    assert_exact(gi, ii, "in indices")
+    assert_exact(ge, ie, "in eids")
+    assert_exact(host(hp).astype(np.int64), rp, "reverse indptr")
+    assert_exact(hi, ri, "reverse indices")
+    assert_exact(he, re_, "reverse eids")
+    ind, outd = orc.degrees(p.o)
+    assert_exact(p.g.in_degrees(), ind.astype(np.int32), "in-degrees")
+    assert_exact(p.g.out_degrees(), outd.astype(np.int32), "out-degrees")
+    info = p.g.info()
+    assert info["max_in_degree"] == (ind.max() if ind.size else 0)
+    assert info["max_out_degree"] == (outd.max() if outd.size else 0)
+    assert info["empty_dst_rows"] == int((ind == 0).sum())
+    assert info["empty_src_rows"] == int((outd == 0).sum())
+    for deg, hub, seg in ((ind, "hub_dst_rows", "segments_in"), (outd, "hub_src_rows", "segments_out")):
+        big = deg[deg > seg_edges].astype(np.int64)
+        assert info[hub] == big.size, hub
+        assert info[seg] == int(((big + seg_edges - 1) // seg_edges).sum()), seg
+    assert info["identity_eids"] == int(np.array_equal(ie, np.arange(p.o.n_edges, dtype=np.int32)))
+    p.g.validate()

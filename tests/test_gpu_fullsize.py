@@ -4,6 +4,8 @@ graph), in the launch configuration bench.py times (default schedule).  The
 oracle computes sampled rows / edges one by one: the largest hub rows, random
 rows of every degree class, empty rows, and their edges.  Tolerances are in
 tests/_gpu.py."""
+import time
+
 import numpy as np
 import pytest
 import torch
@@ -58,8 +60,13 @@ class Workload:
         log(f"{sg.name}: building handle for N={sg.n_dst} E={sg.n_edges}")
         self.sg = sg
         self.o = orc.OGraph.of(sg)
-        self.g = gnnk.Graph.from_coo(dev(sg.src), dev(sg.dst), sg.n_src, sg.n_dst, ptr64=ptr64)
+        s, d = dev(sg.src), dev(sg.dst)
         torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        self.g = gnnk.Graph.from_coo(s, d, sg.n_src, sg.n_dst, ptr64=ptr64)
+        torch.cuda.synchronize()
+        log(f"{sg.name}: device graph build {1e3 * (time.perf_counter() - t0):.1f} ms")
+        del s, d
         self.indeg = np.bincount(sg.dst, minlength=sg.n_dst)
         self.outdeg = np.bincount(sg.src, minlength=sg.n_src)
         # in-CSR positions = edge ids (edges are sorted by destination)

@@ -7,7 +7,7 @@ import torch
 
 import oracle as orc
 from paper_1909_01315_amd import gnnk, synth
-from _gpu import Pair, assert_close, assert_exact, dev, host
+from _gpu import Pair, assert_close, assert_exact, check_formats, dev, host
 
 pytestmark = pytest.mark.gpu
 
@@ -44,27 +44,6 @@ def feats(seed, name, shape, lo=None, hi=None):
 
 # ---------------------------------------------------------------------------
 # A0: graph formats
-
-
-def check_formats(p):
-    ip, ii, ie = orc.csr(p.o, reverse=False)
-    rp, ri, re_ = orc.csr(p.o, reverse=True)
-    gp, gi, ge = p.g.csr_export(reverse=False)
-    hp, hi, he = p.g.csr_export(reverse=True)
-    assert_exact(host(gp).astype(np.int64), ip, "in indptr")
-    assert_exact(gi, ii, "in indices")
-    assert_exact(ge, ie, "in eids")
-    assert_exact(host(hp).astype(np.int64), rp, "reverse indptr")
-    assert_exact(hi, ri, "reverse indices")
-    assert_exact(he, re_, "reverse eids")
-    ind, outd = orc.degrees(p.o)
-    assert_exact(p.g.in_degrees(), ind.astype(np.int32), "in-degrees")
-    assert_exact(p.g.out_degrees(), outd.astype(np.int32), "out-degrees")
-    info = p.g.info()
-    assert info["max_in_degree"] == (ind.max() if ind.size else 0)
-    assert info["empty_dst_rows"] == int((ind == 0).sum())
-    assert info["empty_src_rows"] == int((outd == 0).sum())
-    p.g.validate()
 
 
 def test_graph_formats_c1_c2(c1, c2):
