@@ -651,14 +651,23 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
                 flags |= F_NEGATE;
             }
         }
-        if (bt) ms.push_back({bt, K_FULL});
+        // a product is commutative (one IEEE multiplication either way): the
+        // node operand goes first, the layout of the fast kernels
+        const bool swap = bt && A.op == M_MUL;
+        if (swap) ms.insert(ms.begin(), {bt, K_FULL});
+        else if (bt) ms.push_back({bt, K_FULL});
         if (ct) ms.push_back({ct, K_FULL});
         ms.push_back({gx, K_FULL});
         Geo geo;
         gnnk_status st = choose_geo(Hm, Fm, ms, {}, geo);
         if (st != GNNK_OK) return st;
-        A.a = operand(grad_out, ms[0].kind, tg(GNNK_EDGE));
-        if (bt) A.b = operand(bt, ms[1].kind, tg(b_target));
+        if (swap) {
+            A.a = operand(bt, ms[0].kind, tg(b_target));
+            A.b = operand(grad_out, ms[1].kind, tg(GNNK_EDGE));
+        } else {
+            A.a = operand(grad_out, ms[0].kind, tg(GNNK_EDGE));
+            if (bt) A.b = operand(bt, ms[1].kind, tg(b_target));
+        }
         if (ct) A.c = operand(ct, ms[2].kind, tg(c_target));
         st = out_desc(gx, ms.back().kind, geo, A.out);
         if (st != GNNK_OK) return st;

@@ -154,6 +154,11 @@ __device__ __forceinline__ double dpp_d(double x) {
     return *reinterpret_cast<double*>(&v);
 }
 
+// e^x for x <= 0 (or -inf) from the hardware base-2 exponential (v_exp_f32,
+// 1 ulp).  Rounding x * log2(e) once adds |x| * 2^-24 relative error: 1e-6 at
+// x = -16, where the term is already 1e-7 of a row's largest.
+__device__ __forceinline__ float exp_le0(float x) { return __builtin_amdgcn_exp2f(x * 1.44269504088896341f); }
+
 constexpr int DPP_QUAD_1032 = 0xB1;  // quad_perm [1,0,3,2]
 constexpr int DPP_QUAD_2301 = 0x4E;  // quad_perm [2,3,0,1]
 constexpr int DPP_ROR4 = 0x124;      // row_ror:4 (within 16 lanes)
@@ -333,7 +338,12 @@ template <int VEC, int OPK, int EXT>
 __device__ __forceinline__ void combine_f64(const EngineArgs& A, const Raw<VEC>& r, int32_t ed, double* m) {
     double ad[VEC];
 #pragma unroll
-    for (int i = 0; i < VEC; ++i) ad[i] = r.a[i];
+    for (int i = 0; i < VEC; ++i) {
+        // EXT_BITS: columns this edge did not win contribute zero (masked
+        // before widening: one 32-bit select per column)
+        if constexpr (EXT == EXT_BITS) ad[i] = (double)(((r.kb >> i) & 1u) ? r.a[i] : 0.0f);
+        else ad[i] = r.a[i];
+    }
     if constexpr (EXT == EXT_SCALE) {
         // one reciprocal per edge, not one division per column: the hardware
         // estimate refined by one Newton step (within an ulp of 1/deg in fp64)
@@ -346,10 +356,6 @@ __device__ __forceinline__ void combine_f64(const EngineArgs& A, const Raw<VEC>&
     if constexpr (EXT == EXT_MASK) {
 #pragma unroll
         for (int i = 0; i < VEC; ++i) ad[i] = (r.k[i] == ed) ? ad[i] : 0.0;
-    }
-    if constexpr (EXT == EXT_BITS) {
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) ad[i] = ((r.kb >> i) & 1u) ? ad[i] : 0.0;
     }
     if constexpr (OPK == 0) {
 #pragma unroll

@@ -42,7 +42,7 @@ struct Online {
     // add one edge with score s and source row x
     __device__ __forceinline__ void add(float s, const float* x) {
         const float mn = fmaxf(m, s);
-        const double f = (double)expf(fminf(m, s) - mn);  // exp of a non-positive number
+        const double f = (double)exp_le0(fminf(m, s) - mn);
         const bool up = s > m;
         const double c_old = up ? f : 1.0;
         const double c_new = up ? 1.0 : f;
@@ -54,8 +54,8 @@ struct Online {
     // merge another state (in segment or lane-group order)
     __device__ __forceinline__ void merge(float om, double ol, const double* oacc) {
         const float mn = fmaxf(m, om);
-        const double f1 = m == -INFINITY ? 0.0 : (double)expf(m - mn);
-        const double f2 = om == -INFINITY ? 0.0 : (double)expf(om - mn);
+        const double f1 = m == -INFINITY ? 0.0 : (double)exp_le0(m - mn);
+        const double f2 = om == -INFINITY ? 0.0 : (double)exp_le0(om - mn);
         l = l * f1 + ol * f2;
 #pragma unroll
         for (int i = 0; i < VEC; ++i) acc[i] = acc[i] * f1 + oacc[i] * f2;
@@ -85,6 +85,7 @@ __device__ __forceinline__ void gat_write_attn(const EngineArgs& A, const GatArg
     const int32_t b = (int32_t)b64, e = (int32_t)e64;
     const T* el = reinterpret_cast<const T*>(A.b.data);
     T* out = reinterpret_cast<T*>(G.attn);
+    const float inv = (float)(1.0 / l);
     for (int32_t p0 = b + (int32_t)start; p0 < e; p0 += stride * UNR) {
         int32_t nb[UNR], ed[UNR], ps[UNR];
         bool ok[UNR];
@@ -98,7 +99,7 @@ __device__ __forceinline__ void gat_write_attn(const EngineArgs& A, const GatArg
             const float s = gat_score<T>(x[u], er_h, G.slope);
             if (ok[u] & writer)
                 IO<T, 1>::store1(out + (uint64_t)(uint32_t)ed[u] * (uint32_t)G.attn_stride + h,
-                                 (float)((double)expf(s - m) / l));
+                                 exp_le0(s - m) * inv);
         }
     }
 }

@@ -26,7 +26,10 @@ namespace gnnk {
 
 enum OperandTarget : int32_t { T_NBR = 0, T_EDGE = 1, T_SELF = 2 };
 
-constexpr int ENGINE_UNR = 4;  // edges in flight per lane group and batch
+#ifndef GNNK_ENGINE_UNR
+#define GNNK_ENGINE_UNR 4
+#endif
+constexpr int ENGINE_UNR = GNNK_ENGINE_UNR;  // edges in flight per lane group and batch
 
 // message kinds (fused op of up to three operands a, b, c)
 enum MsgOp : int32_t {

@@ -99,15 +99,37 @@ __global__ void zero_words_kernel(uint32_t* w, int64_t n) {
         w[i] = 0u;
 }
 
-// one thread per (row, column) of the arg array; OR is order-free, so the
-// mask does not depend on the order of the atomics
-__global__ void winner_bits_kernel(const int32_t* arg_e, int64_t n, int32_t D, const int32_t* pos_of_edge,
-                                   uint32_t* bits, int32_t words, int64_t n_edges) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t e = arg_e[i];
-        if (e < 0 || e >= n_edges) continue;  // empty rows (-1); ids outside the graph are ignored
-        const int32_t c = (int32_t)(i % D);
-        atomicOr(bits + (int64_t)pos_of_edge[e] * words + (c >> 5), 1u << (c & 31));
+// Winner masks: half a wavefront per (row, 32-column word) of the arg array.
+// Lanes whose columns have the same winning edge merge their bits, and the
+// first of them stores the whole word.  The word of an edge belongs to the
+// edge's one destination row, so no other lane writes it: plain stores, no
+// atomics, and the result does not depend on any ordering.
+__global__ __launch_bounds__(256) void winner_bits_kernel(const int32_t* arg_e, int64_t n_rows, int32_t D,
+                                                          const int32_t* pos_of_edge, uint32_t* bits, int32_t words,
+                                                          int64_t n_edges) {
+    const int lane = __lane_id();
+    const int half = lane >> 5, b = lane & 31;
+    const int64_t n_units = n_rows * words;
+    const int64_t wave = (blockIdx.x * (int64_t)blockDim.x + threadIdx.x) >> 6;
+    const int64_t stride = ((int64_t)gridDim.x * blockDim.x) >> 6;
+    for (int64_t u0 = 2 * wave; u0 < n_units; u0 += 2 * stride) {
+        const int64_t unit = u0 + half;
+        const int64_t v = unit / words;
+        const int32_t w = (int32_t)(unit - v * words);
+        const int32_t c = w * 32 + b;
+        int32_t e = -1;
+        if (unit < n_units && c < D) e = arg_e[v * D + c];
+        const bool ok = e >= 0 && e < n_edges;  // empty rows (-1); ids outside the graph are ignored
+        const int32_t pos = ok ? pos_of_edge[e] : 0;  // every lane's lookup in flight at once
+        uint64_t todo = __ballot(ok);
+        while (todo) {
+            const int l0 = __builtin_ctzll(todo);
+            const int32_t e0 = __builtin_amdgcn_readlane(e, l0);
+            const int h0 = l0 >> 5;
+            const uint64_t m = __ballot(ok && e == e0 && half == h0);
+            if (lane == l0) bits[(int64_t)pos * words + w] = (uint32_t)(m >> (32 * h0));
+            todo &= ~m;
+        }
     }
 }
 
@@ -210,8 +232,8 @@ hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, c
     const int64_t nw = n_edges * words, n = n_rows * D;
     if (nw > 0) hipLaunchKernelGGL(zero_words_kernel, dim3(grid_1d(nw)), dim3(256), 0, s, bits, nw);
     if (n > 0)
-        hipLaunchKernelGGL(winner_bits_kernel, dim3(grid_1d(n)), dim3(256), 0, s, arg_e, n, D, pos_of_edge, bits,
-                           words, n_edges);
+        hipLaunchKernelGGL(winner_bits_kernel, dim3(grid_1d(n_rows * words * 32)), dim3(256), 0, s, arg_e, n_rows,
+                           D, pos_of_edge, bits, words, n_edges);
     return hipGetLastError();
 }
 

@@ -26,7 +26,7 @@ __device__ __forceinline__ void softmax_pass_online(const EngineArgs& A, int64_t
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
             const float mn = fmaxf(mx[i], s[i]);
-            const double f = (double)expf(fminf(mx[i], s[i]) - mn);  // exp of a non-positive number
+            const double f = (double)exp_le0(fminf(mx[i], s[i]) - mn);
             sum[i] = s[i] > mx[i] ? sum[i] * f + 1.0 : sum[i] + f;
             mx[i] = mn;
         }
@@ -36,8 +36,8 @@ __device__ __forceinline__ void softmax_pass_online(const EngineArgs& A, int64_t
 // merge another (max, sum) pair into this one
 __device__ __forceinline__ void softmax_merge(float& m, double& s, float om, double os) {
     const float mn = fmaxf(m, om);
-    const double f1 = m == -INFINITY ? 0.0 : (double)expf(m - mn);
-    const double f2 = om == -INFINITY ? 0.0 : (double)expf(om - mn);
+    const double f1 = m == -INFINITY ? 0.0 : (double)exp_le0(m - mn);
+    const double f2 = om == -INFINITY ? 0.0 : (double)exp_le0(om - mn);
     s = s * f1 + os * f2;
     m = mn;
 }
@@ -56,7 +56,7 @@ __device__ __forceinline__ void softmax_pass_sum(const EngineArgs& A, int64_t b,
             for (int i = 0; i < VEC; ++i) sum[i] += (double)s[i] * (double)gg[i];
         } else {
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) sum[i] += (double)expf(s[i] - mx[i]);
+            for (int i = 0; i < VEC; ++i) sum[i] += (double)exp_le0(s[i] - mx[i]);
         }
     }
 }
@@ -65,6 +65,11 @@ template <typename T, int VEC>
 __device__ __forceinline__ void softmax_pass_write(const EngineArgs& A, int64_t b, int64_t e, int start,
                                                    int stride, int col0, bool active, const float* mx,
                                                    const double* sum, bool backward) {
+    // forward: a = exp(s - max) times the reciprocal of the fp64 sum, both
+    // rounded to fp32 (3 roundings, well inside the fp32 tolerance)
+    float inv[VEC];
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) inv[i] = backward ? 0.0f : (float)(1.0 / sum[i]);
     for (int64_t p = b + start; p < e; p += stride) {
         const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
         float s[VEC], v[VEC];
@@ -76,7 +81,7 @@ __device__ __forceinline__ void softmax_pass_write(const EngineArgs& A, int64_t 
             for (int i = 0; i < VEC; ++i) v[i] = (float)((double)s[i] * ((double)gg[i] - sum[i]));
         } else {
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) v[i] = (float)((double)expf(s[i] - mx[i]) / sum[i]);
+            for (int i = 0; i < VEC; ++i) v[i] = exp_le0(s[i] - mx[i]) * inv[i];
         }
         if (active) IO<T, VEC>::store(reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0, v);
     }
@@ -179,7 +184,7 @@ __global__ __launch_bounds__(256) void softmax_finish_kernel(EngineArgs A) {
                 double part = P[(int64_t)s * 2 * D + D + col0 + i];
                 if (!BWD) {
                     const float ms = (float)P[(int64_t)s * 2 * D + col0 + i];
-                    part *= (double)expf(ms - mx[i]);  // rescale the segment's sum to the row maximum
+                    part *= (double)exp_le0(ms - mx[i]);  // rescale the segment's sum to the row maximum
                 }
                 sum[i] += part;
             }

@@ -51,6 +51,9 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
             Pre<VEC> pre;
             load_pre<T, VEC, OPK, S>(A, (int32_t)r, col0, h, pre);
             auto sink = [&](const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
+                // winner masks: most slots of a wavefront won no column at all
+                if constexpr (EXT == EXT_BITS)
+                    if (__ballot(rw.kb != 0u) == 0ull) return;
                 double m[VEC];
                 combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
 #pragma unroll
@@ -89,6 +92,9 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
             Pre<VEC> pre;
             load_pre<T, VEC, OPK, S>(A, self, col0, h, pre);
             auto sink = [&](const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
+                // winner masks: most slots of a wavefront won no column at all
+                if constexpr (EXT == EXT_BITS)
+                    if (__ballot(rw.kb != 0u) == 0ull) return;
                 double m[VEC];
                 combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
 #pragma unroll
@@ -158,10 +164,27 @@ __global__ __launch_bounds__(256) void spmm_sum_combine_kernel(EngineArgs A) {
 // ---------------------------------------------------------------------------
 // max / min with the winning edge and neighbour
 
+// identity of max / min: a running best starts here, so the first message
+// that is not -inf (+inf for min) replaces it by a strict comparison
+__device__ __forceinline__ float cmp_identity(bool is_min) { return is_min ? INFINITY : -INFINITY; }
+
+// Output of one row.  first: the row's first CSR position (-1 for an empty
+// row).  With identity edge ids (ids == positions) be holds positions and a
+// row whose messages are all -inf (+inf for min) kept be = -1: its first edge
+// wins, as a scan with strict comparisons from the first edge gives; the
+// neighbour of the winner is read from the CSR here.  With explicit edge ids
+// be and bn come from the walk.
 template <typename T, int VEC>
-__device__ __forceinline__ void write_cmp_row(const EngineArgs& A, int64_t row, bool active, int col0,
-                                              const float* best, const int32_t* be, const int32_t* bn) {
+__device__ __forceinline__ void write_cmp_row(const EngineArgs& A, int64_t row, bool active, int col0, float* best,
+                                              int32_t* be, int32_t* bn, int64_t first) {
     if (!active || row < 0) return;
+    if (A.csr.eid == nullptr) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            if (be[i] < 0 && first >= 0) be[i] = (int32_t)first;
+            bn[i] = be[i] >= 0 ? A.csr.idx[be[i]] : -1;
+        }
+    }
     float v[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) v[i] = be[i] < 0 ? 0.0f : best[i];
@@ -172,13 +195,14 @@ __device__ __forceinline__ void write_cmp_row(const EngineArgs& A, int64_t row, 
 }
 
 // Running max/min of one lane group.  The group sees its edges in ascending
-// position, which is ascending edge id when the CSR has identity ids or
-// rows kept in id order; TIES = true adds the explicit smaller-id test for
-// any other order.
-template <int VEC, int OPK, bool TIES>
+// position.  TIES = false (identity edge ids): ascending position is
+// ascending edge id, so a strict comparison keeps the smallest id among
+// equal messages, and only the value and the position are tracked.  TIES =
+// true (explicit ids, in any order) tests the smaller id explicitly and
+// tracks the edge and the neighbour.
+template <int VEC, int OPK, bool TIES, bool MIN>
 struct CmpSink {
     const EngineArgs& A;
-    bool is_min;
     float best[VEC];
     int32_t be[VEC], bn[VEC];
     __device__ __forceinline__ void operator()(const Raw<VEC>& rw, int32_t ed, int32_t nb, bool ok) {
@@ -186,13 +210,16 @@ struct CmpSink {
         combine_f32<VEC, OPK>(A, rw, m);
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
-            bool upd;
-            if constexpr (TIES) upd = better(m[i], ed, best[i], be[i], is_min);
-            else upd = (be[i] < 0) | (is_min ? (m[i] < best[i]) : (m[i] > best[i]));
-            upd = upd & ok;
-            best[i] = upd ? m[i] : best[i];
-            be[i] = upd ? ed : be[i];
-            bn[i] = upd ? nb : bn[i];
+            if constexpr (TIES) {
+                const bool upd = ok & better(m[i], ed, best[i], be[i], MIN);
+                best[i] = upd ? m[i] : best[i];
+                be[i] = upd ? ed : be[i];
+                bn[i] = upd ? nb : bn[i];
+            } else {
+                const bool upd = ok & (MIN ? (m[i] < best[i]) : (m[i] > best[i]));
+                best[i] = upd ? m[i] : best[i];
+                be[i] = upd ? ed : be[i];
+            }
         }
     }
 };
@@ -207,6 +234,7 @@ __device__ __forceinline__ void cmp_row(const EngineArgs& A, const Lanes& ln, in
     const bool is_min = (A.flags & F_IS_MIN) != 0;
     const bool ties = A.csr.eid != nullptr;
     const int32_t self = r >= 0 ? (int32_t)r : 0;
+    const int64_t first = e > b ? b : -1;
     for (int ch = 0; ch < geo.nchunk; ++ch) {
         const int j = ch * L + ln.lig;
         const bool active = j < geo.NV;
@@ -217,21 +245,21 @@ __device__ __forceinline__ void cmp_row(const EngineArgs& A, const Lanes& ln, in
         Pre<VEC> pre;
         auto run = [&](auto& sk) {
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) { sk.best[i] = 0.0f; sk.be[i] = -1; sk.bn[i] = -1; }
+            for (int i = 0; i < VEC; ++i) { sk.best[i] = cmp_identity(is_min); sk.be[i] = -1; sk.bn[i] = -1; }
             if constexpr (WAVE_ROW) walk_row<T, VEC, OPK, EXT_NONE, S>(A, self, b, e, ln.g, G, col0, h, pre, sk);
             else walk_lane<T, VEC, OPK, EXT_NONE, S>(A, self, b, e, col0, h, pre, sk);
 #pragma unroll
             for (int i = 0; i < VEC; ++i) { best[i] = sk.best[i]; be[i] = sk.be[i]; bn[i] = sk.bn[i]; }
         };
         if (ties) {
-            CmpSink<VEC, OPK, true> sk{A, is_min, {}, {}, {}};
-            run(sk);
+            if (is_min) { CmpSink<VEC, OPK, true, true> sk{A, {}, {}, {}}; run(sk); }
+            else { CmpSink<VEC, OPK, true, false> sk{A, {}, {}, {}}; run(sk); }
         } else {
-            CmpSink<VEC, OPK, false> sk{A, is_min, {}, {}, {}};
-            run(sk);
+            if (is_min) { CmpSink<VEC, OPK, false, true> sk{A, {}, {}, {}}; run(sk); }
+            else { CmpSink<VEC, OPK, false, false> sk{A, {}, {}, {}}; run(sk); }
         }
         if constexpr (!WAVE_ROW) {
-            write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn);
+            write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn, first);
         } else {
             for (int s = L; s < WAVE; s <<= 1) {
 #pragma unroll
@@ -255,7 +283,7 @@ __device__ __forceinline__ void cmp_row(const EngineArgs& A, const Lanes& ln, in
                     for (int i = 0; i < VEC; ++i) { PV[i] = best[i]; PE[i] = be[i]; PN[i] = bn[i]; }
                 }
             } else if (ln.g == 0) {
-                write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn);
+                write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn, first);
             }
         }
     }
@@ -304,7 +332,7 @@ __global__ __launch_bounds__(256) void spmm_cmp_kernel(EngineArgs A) {
                 int32_t be[VEC], bn[VEC];
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) { best[i] = 0.0f; be[i] = -1; bn[i] = -1; }
-                write_cmp_row<T, VEC>(A, r, active, active ? j * VEC : 0, best, be, bn);
+                write_cmp_row<T, VEC>(A, r, active, active ? j * VEC : 0, best, be, bn, -1);
             }
         }
     }
@@ -346,7 +374,7 @@ __global__ __launch_bounds__(256) void spmm_cmp_combine_kernel(EngineArgs A) {
                 bn[i] = upd ? pn : bn[i];
             }
         }
-        write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn);
+        write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn, row_ok ? row_ptr(A.csr, r) : -1);
     }
 }
 
