@@ -243,12 +243,36 @@ gnnk_status edge_leaky_relu_backward(const gnnk_tensor* x, const gnnk_tensor* dy
  *   out[v, h] = sum over in-edges of softmax_v(s)[e, h] * feat[u, h, :]
  * feat: (num_src, H, F); el: (num_src, H, 1); er: (num_dst, H, 1); out:
  * (num_dst, H, F).  attn (nullable, (num_edges, H, 1)) receives the softmax,
- * which the backward pass (gspmm_backward, edge_softmax_backward, ...) needs.
- * The running maximum is tracked per destination and head and the fp64 sums
- * are rescaled when it grows; destinations without in-edges get 0.
- * Errors: GNNK_EINVAL on shapes or dtypes. */
+ * which the unfused backward (gspmm_backward, edge_softmax_backward, ...)
+ * needs.  stats (nullable, (num_dst, H, 2), always fp32) receives per
+ * destination and head the maximum score m and the reciprocal 1/l of the
+ * sum l of exp(s - m), from which gat_aggregate_backward recomputes the
+ * attention (a = exp(s - m) * (1/l), as attn holds it); rows without
+ * in-edges get (0, 0).  The running maximum is tracked per destination and
+ * head and the fp64 sums are rescaled when it grows; destinations without
+ * in-edges get 0.  Errors: GNNK_EINVAL on shapes or dtypes. */
 gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el, const gnnk_tensor* er,
-                          float slope, gnnk_tensor* out, gnnk_tensor* attn, hipStream_t stream);
+                          float slope, gnnk_tensor* out, gnnk_tensor* attn, gnnk_tensor* stats, hipStream_t stream);
+
+/* Backward of gat_aggregate (Theorem 1's gradients of the g-SpMM and the
+ * g-SDDMM, chained through the softmax and the leaky ReLU) without any
+ * tensor of num_edges elements: with a the attention recomputed from stats,
+ * da = grad_out[v, h, :] . feat[u, h, :] and lk the leaky ReLU's derivative
+ * at el[u, h] + er[v, h] (the slope at 0 and below),
+ *   grad_feat[u, h, :] = sum over out-edges of a * grad_out[v, h, :]
+ *   grad_el[u, h]      = sum over out-edges of a * (da - S[v, h]) * lk
+ *   grad_er[v, h]      = sum over in-edges of a * (da - S[v, h]) * lk
+ * where S[v, h] = sum over in-edges of a * da; every sum in fp64, rounded
+ * once.  feat, el, er, slope and stats as passed to (and written by)
+ * gat_aggregate; grad_out (num_dst, H, F); the three gradients are nullable
+ * and take their operand's shape; all tensors but stats share one dtype.
+ * Needs H * F / vec <= 64 (GNNK_EUNSUPPORTED otherwise).  Uses the handle's
+ * scratch: 16 bytes per (destination, head) plus per-segment partials of
+ * hub rows.  Errors: GNNK_EINVAL on shapes or dtypes. */
+gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
+                                   const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
+                                   const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,
+                                   gnnk_tensor* grad_er, hipStream_t stream);
 /* ------------------------------------------------------------------------ */
 /* Tuning knobs, for schedule comparisons (forcing node- or edge-balanced
  * schedules; the paper's Table 1 states both are valid for commutative and

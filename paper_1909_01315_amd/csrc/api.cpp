@@ -724,12 +724,18 @@ gnnk_status edge_softmax_backward(gnnk_graph_t g, const gnnk_tensor* out, const 
     return softmax_common(g, out, grad_out, grad_score, true, stream);
 }
 
+// (num_dst, H, 2) fp32 per-row statistics of the fused attention
+static bool stats_ok(const gnnk_graph* g, const gnnk_tensor* st, int H) {
+    return tensor_ok(st) && st->dtype == GNNK_F32 && st->rows == g->n_dst && st->heads == H && st->feat == 2;
+}
+
 gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el, const gnnk_tensor* er,
-                          float slope, gnnk_tensor* out, gnnk_tensor* attn, hipStream_t stream) {
+                          float slope, gnnk_tensor* out, gnnk_tensor* attn, gnnk_tensor* stats, hipStream_t stream) {
     clear_error();
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
     if (!tensor_ok(feat) || !tensor_ok(el) || !tensor_ok(er) || !tensor_ok(out) || (attn && !tensor_ok(attn)))
         return fail(GNNK_EINVAL, "malformed tensor");
+    if (stats && !stats_ok(g, stats, feat->heads)) return fail(GNNK_EINVAL, "stats must be (num_dst, H, 2) fp32");
     if (!same_dtype({feat, el, er, out, attn})) return fail(GNNK_EINVAL, "all tensors must share one dtype");
     const int H = feat->heads, F = feat->feat;
     if (feat->rows != g->n_src || el->rows != g->n_src || er->rows != g->n_dst || out->rows != g->n_dst)
@@ -767,8 +773,83 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
     const bool fast = !options().no_fast && fast_geo(geo, dt) && fits32(A.a, g->n_src, es) &&
                       fits32(A.b, g->n_src, es);
     return launch_status(launch_gat(A, er->data, er->row_stride, attn ? attn->data : nullptr,
-                                    attn ? attn->row_stride : 0, slope, row_ml, dt, geo.vec, fast ? geo.G : 0, stream),
+                                    attn ? attn->row_stride : 0, slope, row_ml,
+                                    stats ? reinterpret_cast<float*>(stats->data) : nullptr,
+                                    stats ? stats->row_stride : 0, dt, geo.vec, fast ? geo.G : 0, stream),
                          "fused attention launch");
+}
+
+gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
+                                   const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
+                                   const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,
+                                   gnnk_tensor* grad_er, hipStream_t stream) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (!tensor_ok(feat) || !tensor_ok(el) || !tensor_ok(er) || !tensor_ok(grad_out) || !stats ||
+        (grad_feat && !tensor_ok(grad_feat)) || (grad_el && !tensor_ok(grad_el)) || (grad_er && !tensor_ok(grad_er)))
+        return fail(GNNK_EINVAL, "malformed tensor");
+    if (!same_dtype({feat, el, er, grad_out, grad_feat, grad_el, grad_er}))
+        return fail(GNNK_EINVAL, "all tensors but stats must share one dtype");
+    const int H = feat->heads, F = feat->feat;
+    if (!stats_ok(g, stats, H)) return fail(GNNK_EINVAL, "stats must be (num_dst, H, 2) fp32");
+    if (feat->rows != g->n_src || el->rows != g->n_src || er->rows != g->n_dst || grad_out->rows != g->n_dst)
+        return fail(GNNK_EINVAL, "row counts must be num_src (feat, el) and num_dst (er, grad_out)");
+    if (el->heads != H || el->feat != 1 || er->heads != H || er->feat != 1 || grad_out->heads != H ||
+        grad_out->feat != F)
+        return fail(GNNK_EINVAL, "shapes must be feat (H, F), el and er (H, 1), grad_out (H, F)");
+    auto same = [](const gnnk_tensor* a, const gnnk_tensor* b) {
+        return !a || (a->rows == b->rows && a->heads == b->heads && a->feat == b->feat);
+    };
+    if (!same(grad_feat, feat) || !same(grad_el, el) || !same(grad_er, er))
+        return fail(GNNK_EINVAL, "each gradient must have its operand's shape");
+    std::vector<Member> ms{{feat, K_FULL}, {el, K_FULL}, {grad_out, K_FULL}};
+    Geo geo;
+    gnnk_status st = choose_geo(H, F, ms, {}, geo);
+    if (st != GNNK_OK) return st;
+    // a head's dot product is reduced across the lanes of one chunk
+    if (geo.nchunk != 1) return fail(GNNK_EUNSUPPORTED, "fused attention backward needs H * F / vec <= 64");
+    const int dt = dtype_code(grad_out);
+    EngineArgs ain{}, aout{};
+    ain.a = operand(feat, K_FULL, T_NBR);
+    ain.b = operand(el, ms[1].kind, T_NBR);
+    ain.op = M_MUL;
+    ain.csr = csr_of(g, g->in);
+    set_geo(ain, geo);
+    ain.sch = schedule(g->in, geo, true);
+    aout.csr = csr_of(g, g->out);
+    set_geo(aout, geo);
+    aout.sch = schedule(g->out, geo, true);
+    const size_t rec = (size_t)g->n_dst * H * 16, pa = (size_t)ain.sch.n_seg * 3 * H * 8,
+                 pb = (size_t)aout.sch.n_seg * (geo.D + H) * 8;
+    const size_t rec_al = (rec + 255) / 256 * 256;
+    char* p = reinterpret_cast<char*>(graph_scratch(g, rec_al + std::max(pa, pb) + 8));
+    if (!p) return fail(GNNK_ENOMEM, "scratch allocation failed");
+    GatBwdArgs B{};
+    B.er = er->data;
+    B.er_stride = er->row_stride;
+    B.stats = reinterpret_cast<const float*>(stats->data);
+    B.stats_stride = stats->row_stride;
+    B.dz = grad_out->data;
+    B.dz_stride = grad_out->row_stride;
+    B.d_er = grad_er ? grad_er->data : nullptr;
+    B.d_er_stride = grad_er ? grad_er->row_stride : 0;
+    B.d_el = grad_el ? grad_el->data : nullptr;
+    B.d_el_stride = grad_el ? grad_el->row_stride : 0;
+    B.d_feat = grad_feat ? grad_feat->data : nullptr;
+    B.d_feat_stride = grad_feat ? grad_feat->row_stride : 0;
+    B.el = el->data;
+    B.el_stride = el->row_stride;
+    B.feat = feat->data;
+    B.feat_stride = feat->row_stride;
+    B.rec = reinterpret_cast<float4*>(p);
+    B.part = reinterpret_cast<double*>(p + rec_al);
+    B.slope = slope;
+    B.H = H;
+    const int es = dt == 1 ? 2 : 4;
+    const bool fast = !options().no_fast && fast_geo(geo, dt) && fits32(ain.a, g->n_src, es) &&
+                      fits32(ain.b, g->n_src, es);
+    return launch_status(launch_gat_backward(ain, aout, B, dt, geo.vec, fast ? geo.G : 0, stream),
+                         "fused attention backward launch");
 }
 
 static gnnk_status leaky_common(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* y, float slope,

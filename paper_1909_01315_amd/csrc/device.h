@@ -161,15 +161,16 @@ __device__ __forceinline__ float exp_le0(float x) { return __builtin_amdgcn_exp2
 
 constexpr int DPP_QUAD_1032 = 0xB1;  // quad_perm [1,0,3,2]
 constexpr int DPP_QUAD_2301 = 0x4E;  // quad_perm [2,3,0,1]
-constexpr int DPP_ROR4 = 0x124;      // row_ror:4 (within 16 lanes)
-constexpr int DPP_ROR8 = 0x128;      // row_ror:8
+// row_ror:n hands lane i the value of lane (i - n) mod 16 of its 16-lane row
+constexpr int DPP_ROR12 = 0x12C;     // row_ror:12: lane i reads lane (i + 4) mod 16
+constexpr int DPP_ROR8 = 0x128;      // row_ror:8: lane i reads lane (i + 8) mod 16
 
 // Sum over aligned runs of `red` lanes (a power of two), correct in the first
 // lane of each run: DPP within 16-lane rows, swizzles beyond.
 __device__ __forceinline__ double run_sum(double v, int red) {
     if (red >= 2) v += dpp_d<DPP_QUAD_1032>(v);
     if (red >= 4) v += dpp_d<DPP_QUAD_2301>(v);
-    if (red >= 8) v += dpp_d<DPP_ROR4>(v);
+    if (red >= 8) v += dpp_d<DPP_ROR12>(v);  // lane i (i mod 8 < 4) adds the quad above it
     if (red >= 16) v += dpp_d<DPP_ROR8>(v);
     if (red >= 32) v += shfl_xor_d(v, 16);
     if (red >= 64) v += shfl_xor_d(v, 32);

@@ -169,7 +169,34 @@ hipError_t launch_sddmm_edge(const EngineArgs& a, int64_t n_pos, int dtype, int 
 // fused attention, gat.hip (a: feat at the neighbour, b: el at the neighbour;
 // row_ml: n_hub x 2 x D doubles when attn is written)
 hipError_t launch_gat(const EngineArgs& a, const void* er, int64_t er_stride, void* attn, int64_t attn_stride,
-                      float slope, void* row_ml, int dtype, int vec, int gc, hipStream_t s);
+                      float slope, void* row_ml, float* stats, int64_t stats_stride, int dtype, int vec, int gc,
+                      hipStream_t s);
+// backward of the fused attention, gat.hip: pass A walks the in-CSR (ain: a =
+// feat, b = el at the neighbour), pass B the reverse graph's CSR (aout)
+struct GatBwdArgs {
+    const void* er;          // (N_dst, H) T
+    int64_t er_stride;
+    const float* stats;      // (N_dst, H, 2) fp32 from the forward
+    int64_t stats_stride;
+    const void* dz;          // (N_dst, H, F) T
+    int64_t dz_stride;
+    void* d_er;              // (N_dst, H) T, nullable
+    int64_t d_er_stride;
+    void* d_el;              // (N_src, H) T, nullable
+    int64_t d_el_stride;
+    void* d_feat;            // (N_src, H, F) T, nullable
+    int64_t d_feat_stride;
+    const void* el;          // (N_src, H) T
+    int64_t el_stride;
+    const void* feat;        // (N_src, H, F) T
+    int64_t feat_stride;
+    float4* rec;             // (N_dst, H): er, max, 1 / sum, S
+    double* part;            // hub segments: pass A 3 x H, pass B D + H doubles per segment
+    float slope;
+    int32_t H;
+};
+hipError_t launch_gat_backward(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs& b, int dtype, int vec,
+                               int gc, hipStream_t s);
 hipError_t launch_fill_rows(const void* ptr, int ptr64, int64_t n_rows, int64_t n_edges, int32_t* row,
                             hipStream_t s);
 hipError_t launch_sddmm(const EngineArgs& a, int dtype, int vec, int opk, int spec, int gc, hipStream_t s);

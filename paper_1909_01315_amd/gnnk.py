@@ -81,7 +81,10 @@ SYMBOLS = {
     "edge_leaky_relu_backward": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
                                  ctypes.c_void_p],
     "gat_aggregate": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
-                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
+                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
+    "gat_aggregate_backward": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
+                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                               ctypes.c_void_p],
     "gnnk_set_option": [ctypes.c_char_p, ctypes.c_int64],
     "gnnk_last_error": [],
 }
@@ -366,18 +369,36 @@ def edge_softmax_backward(g: Graph, out, grad_out, grad_score=None, stream=None)
 
 
 def gat_aggregate(g: Graph, feat, el, er, slope: float = 0.2, out=None, attn=None, want_attn: bool = False,
-                  stream=None):
+                  stats=None, want_stats: bool = False, stream=None):
     """Fused attention: out[v, h] = sum over in-edges of softmax_v(leaky(el[u, h] + er[v, h])) * feat[u, h, :].
-    Returns out, or (out, attn) with want_attn (or attn given)."""
+    Returns out, followed by attn (with want_attn or attn given) and by the per-row statistics
+    (num_dst, H, 2) fp32 (with want_stats or stats given) that gat_aggregate_backward takes."""
     feat, el, er = _as3(feat), _as3(el), _as3(er)
     if out is None:
         out = torch.empty((g.num_dst, feat.shape[1], feat.shape[2]), dtype=feat.dtype, device=feat.device)
     if want_attn and attn is None:
         attn = torch.empty((g.num_edges, feat.shape[1], 1), dtype=feat.dtype, device=feat.device)
-    d = [_desc(x) for x in (feat, el, er, out, attn)]
+    if want_stats and stats is None:
+        stats = torch.empty((g.num_dst, feat.shape[1], 2), dtype=torch.float32, device=feat.device)
+    d = [_desc(x) for x in (feat, el, er, out, attn, stats)]
     _check(load().gat_aggregate(g.handle, _ref(d[0]), _ref(d[1]), _ref(d[2]), ctypes.c_float(slope), _ref(d[3]),
-                                _ref(d[4]), _stream(stream)))
-    return (out, attn) if attn is not None else out
+                                _ref(d[4]), _ref(d[5]), _stream(stream)))
+    res = (out,) + ((attn,) if attn is not None else ()) + ((stats,) if stats is not None else ())
+    return res if len(res) > 1 else out
+
+
+def gat_aggregate_backward(g: Graph, feat, el, er, slope: float, stats, grad_out, want_feat: bool = True,
+                           want_el: bool = True, want_er: bool = True, stream=None):
+    """(grad_feat, grad_el, grad_er) of gat_aggregate from its per-row statistics (any may be None)."""
+    feat, el, er, grad_out = _as3(feat), _as3(el), _as3(er), _as3(grad_out)
+    gf = torch.empty(feat.shape, dtype=feat.dtype, device=feat.device) if want_feat else None
+    gl = torch.empty(el.shape, dtype=feat.dtype, device=feat.device) if want_el else None
+    gr = torch.empty(er.shape, dtype=feat.dtype, device=feat.device) if want_er else None
+    d = [_desc(x) for x in (feat, el, er, stats, grad_out, gf, gl, gr)]
+    _check(load().gat_aggregate_backward(g.handle, _ref(d[0]), _ref(d[1]), _ref(d[2]), ctypes.c_float(slope),
+                                         _ref(d[3]), _ref(d[4]), _ref(d[5]), _ref(d[6]), _ref(d[7]),
+                                         _stream(stream)))
+    return gf, gl, gr
 
 
 def edge_leaky_relu(x, slope: float = 0.2, y=None, stream=None):

@@ -115,27 +115,29 @@ class _LeakyReLU(torch.autograd.Function):
 
 
 class _FusedGAT(torch.autograd.Function):
-    """gat_aggregate forward (one pass per destination, attention kept for
-    backward); backward as the chain of the unfused gradients, recomputing
-    the pre-activation scores for the leaky ReLU."""
+    """gat_aggregate forward (one pass per destination) keeping only the
+    per-row statistics (max score, 1 / sum); backward by
+    gat_aggregate_backward, which recomputes the attention from them, so no
+    tensor of E x H elements is formed in either direction.  Both this
+    backward and the unfused one need H * F / vector width <= 64 (the
+    attention gradient is a per-head reduction across one lane group)."""
 
     @staticmethod
     def forward(ctx, g, feat, el, er, slope):
-        out, a = gnnk.gat_aggregate(g, feat, el, er, slope, want_attn=True)
+        out, stats = gnnk.gat_aggregate(g, feat, el, er, slope, want_stats=True)
         ctx.g, ctx.slope = g, slope
-        ctx.save_for_backward(feat, el, er, a)
+        ctx.save_for_backward(feat, el, er, stats)
         return out
 
     @staticmethod
     def backward(ctx, dout):
-        feat, el, er, a = ctx.saved_tensors
+        feat, el, er, stats = ctx.saved_tensors
         g = ctx.g
-        dfeat, da = gnnk.gspmm_backward(g, "mul", "sum", feat, a, _c(dout))
-        ds = gnnk.edge_softmax_backward(g, a, da)
-        s = gnnk.gsddmm(g, "add", el, "u", er, "v")
-        ds = gnnk.edge_leaky_relu_backward(s, ds, ctx.slope)
-        d_el, d_er = gnnk.gsddmm_backward(g, "add", el, "u", er, "v", ds)
-        return None, dfeat.view(feat.shape), d_el.view(el.shape), d_er.view(er.shape), None
+        nf = ctx.needs_input_grad
+        dfeat, d_el, d_er = gnnk.gat_aggregate_backward(g, feat, el, er, ctx.slope, stats, _c(dout),
+                                                        want_feat=nf[1], want_el=nf[2], want_er=nf[3])
+        view = lambda t, like: t.view(like.shape) if t is not None else None
+        return None, view(dfeat, feat), view(d_el, el), view(d_er, er), None
 
 
 # ---------------------------------------------------------------------------

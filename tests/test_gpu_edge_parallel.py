@@ -97,6 +97,17 @@ def test_gspmm_backward_edge_parallel_c1(c1, schedule, op, reduce):
 
 
 @pytest.mark.parametrize("schedule", SCHEDULES)
+@pytest.mark.parametrize("shape", [(2, 32), (1, 64), (1, 128)])
+def test_gsddmm_dot_wide_heads_c1(c1, schedule, shape):
+    """dot products reduced over 8, 16 and 32 lanes per head"""
+    gnnk.set_option("schedule", schedule)
+    L = feats(S, f"wL{shape}", (c1.o.n_src,) + shape)
+    R = feats(S, f"wR{shape}", (c1.o.n_dst,) + shape)
+    assert_close(gnnk.gsddmm(c1.g, "dot", dev(L), "u", dev(R), "v"), orc.gsddmm(c1.o, "dot", L, "u", R, "v"),
+                 name=f"dot {shape}")
+
+
+@pytest.mark.parametrize("schedule", SCHEDULES)
 @pytest.mark.parametrize("op", ["add", "sub", "mul", "div", "dot", "copy_lhs"])
 @pytest.mark.parametrize("lt,rt", [("u", "v"), ("v", "u"), ("u", "e"), ("e", "v")])
 def test_gsddmm_edge_parallel_c1(c1, schedule, op, lt, rt):

@@ -181,6 +181,51 @@ def test_c3_fused_gat(c3):
     assert_close(host(out)[c3.rows], ref, name="c3 fused attention output")
 
 
+def test_c3_fused_gat_backward(c3):
+    """gat_aggregate_backward on c3 (hub rows in both directions): d feat on
+    sampled sources and d er on sampled destinations against the oracle's
+    chain in fp64; d el against the unfused GPU chain (each of its steps
+    checked at this size above) at the chain tolerance."""
+    N, E = c3.sg.n_dst, c3.sg.n_edges
+    fs = synth.feat_seed(3)
+    X = synth.normal(fs, "X", (N, 8, 16))
+    el = synth.normal(fs, "el", (N, 8, 1))
+    er = synth.normal(fs, "er", (N, 8, 1))
+    dz = synth.normal(synth.grad_seed(3), "gatdz", (N, 8, 16))
+    Xd, eld, erd, dzd = dev(X), dev(el), dev(er), dev(dz)
+    _, st = gnnk.gat_aggregate(c3.g, Xd, eld, erd, 0.2, want_stats=True)
+    gf, gl, gr = gnnk.gat_aggregate_backward(c3.g, Xd, eld, erd, 0.2, st, dzd)
+    log("c3 fused attention backward: oracle chain in fp64 on sampled rows")
+    X64, el64, er64, dz64 = (a.astype(np.float64) for a in (X, el, er, dz))
+    s = orc.gsddmm(c3.o, "add", el64, "u", er64, "v")
+    a = orc.edge_softmax(c3.o, orc.leaky_relu(s, 0.2))
+    rf, _ = orc.gspmm_backward(c3.o, "mul", "sum", X64, a, dz64, want_rhs=False, sel=c3.srows)
+    assert_close(host(gf)[c3.srows], rf, name="c3 fused d feat")
+    er_rows = edges_of_rows(c3.indptr, c3.rows, cap=E)
+    full = np.zeros((E, 8, 1), np.float64)
+    full[er_rows] = orc.gsddmm(c3.o, "dot", X64, "u", dz64, "v", edges=er_rows)
+    ds2, eids = orc.edge_softmax_backward(c3.o, a, full, rows=c3.rows)
+    del a
+    full[:] = 0.0
+    full[eids] = orc.leaky_relu_backward(s[eids], ds2, 0.2)
+    del s
+    _, rr = orc.gsddmm_backward(c3.o, "add", el64, "u", er64, "v", full, want_lhs=False, sel=c3.rows)
+    del full
+    assert_close(host(gr)[c3.rows], rr, name="c3 fused d er")
+    # d el: the unfused chain on the GPU
+    sg_ = gnnk.gsddmm(c3.g, "add", eld, "u", erd, "v")
+    au = gnnk.edge_softmax(c3.g, gnnk.edge_leaky_relu(sg_, 0.2))
+    _, da = gnnk.gspmm_backward(c3.g, "mul", "sum", Xd, au, dzd, want_lhs=False)
+    ds = gnnk.edge_leaky_relu_backward(sg_, gnnk.edge_softmax_backward(c3.g, au, da), 0.2)
+    del au, da
+    ul, _ = gnnk.gsddmm_backward(c3.g, "add", eld, "u", erd, "v", ds, want_rhs=False)
+    del ds, sg_
+    ref = host(ul).astype(np.float64)
+    got = host(gl).astype(np.float64)
+    tol = 1e-4 * np.abs(ref) + 1e-5 * np.abs(ref).max()
+    assert np.all(np.abs(got - ref) <= tol), f"c3 fused d el: max err {np.abs(got - ref).max()}"
+
+
 def test_c3_sage_mean_and_max(c3):
     N = c3.sg.n_dst
     X = synth.normal(synth.feat_seed(3), "X", (N, 1, 128))
@@ -331,9 +376,11 @@ def test_c3_layers_gat_and_sage(c3):
         gat.zero_grad()
         Xg = X.clone().requires_grad_(True)
         out, peak = _fwd_bwd_peak(gat, c3.g, Xg)
-        log(f"c3 GAT layer fused={fused}: peak {peak / 1e9:.1f} GB over forward + backward, E x D x 4 = "
+        log(f"c3 GAT layer fused={fused}: peak {peak / 1e9:.2f} GB over forward + backward, E x D x 4 = "
             f"{ed_bytes / 1e9:.1f} GB")
-        assert peak < 0.5 * ed_bytes
+        # unfused: a few E x H tensors (scores, attention and their
+        # gradients); fused: none (per-row statistics only)
+        assert peak < (0.02 if fused else 0.5) * ed_bytes
         _close_layer(out.view(N, H, F)[torch.from_numpy(c3.rows).cuda()], ref, f"GAT forward fused={fused}")
         assert torch.isfinite(Xg.grad).all()
         grads[fused] = (Xg.grad.clone(), gat.fc.weight.grad.clone(), gat.attn_l.grad.clone())

@@ -9,7 +9,7 @@ import pytest
 
 import oracle as orc
 from paper_1909_01315_amd import gnnk, nn, synth
-from _gpu import Pair, assert_close, dev
+from _gpu import Pair, assert_close, assert_exact, dev, host
 
 pytestmark = pytest.mark.gpu
 
@@ -114,3 +114,129 @@ def test_gatconv_fused_matches_unfused(c2):
     (out_b * g).sum().backward()
     ga, gb = Xa.grad.cpu().numpy().astype(np.float64), Xb.grad.cpu().numpy().astype(np.float64)
     assert np.all(np.abs(ga - gb) <= 1e-5 + 1e-4 * np.abs(ga)), "fused backward"
+
+
+# ---------------------------------------------------------------------------
+# backward of the fused attention (gat_aggregate_backward) from the per-row
+# statistics, against the oracle's chain of the four steps' gradients run in
+# fp64 on the same (exactly widened) inputs: fp32 tolerance of tests/_gpu.py
+# (the fused kernels round the attention to fp32 as the forward does and sum
+# in fp64; the fp64 chain rounds nothing)
+
+
+def oracle_gat_backward(o, feat, el, er, slope, dz):
+    f, l, r, z = (np.asarray(x, np.float64) for x in (feat, el, er, dz))
+    s = orc.gsddmm(o, "add", l, "u", r, "v")
+    a = orc.edge_softmax(o, orc.leaky_relu(s, slope))
+    dfeat, da = orc.gspmm_backward(o, "mul", "sum", f, a, z)
+    ds = orc.leaky_relu_backward(s, orc.edge_softmax_backward(o, a, da), slope)
+    d_el, d_er = orc.gsddmm_backward(o, "add", l, "u", r, "v", ds)
+    return dfeat, d_el, d_er
+
+
+def row_stats(o, el, er, slope):
+    """per destination and head: the max of the oracle's fp32 scores and the
+    fp64 sum of exp(score - max) (the definition, grouped with numpy)"""
+    s = orc.leaky_relu(orc.gsddmm(o, "add", el, "u", er, "v"), slope)[:, :, 0]
+    H = s.shape[1]
+    m = np.full((o.n_dst, H), -np.inf, np.float32)
+    np.maximum.at(m, o.dst, s)
+    l = np.zeros((o.n_dst, H), np.float64)
+    np.add.at(l, o.dst, np.exp(s.astype(np.float64) - m[o.dst].astype(np.float64)))
+    return m, l
+
+
+@pytest.mark.parametrize("H,F", [(1, 16), (4, 4), (8, 16), (2, 32)])
+def test_gat_stats_and_backward_c1(c1, H, F):
+    N = c1.o.n_src
+    feat = synth.normal(S, f"bf{H}{F}", (N, H, F))
+    el = synth.normal(S, f"bel{H}", (N, H, 1))
+    er = synth.normal(S, f"ber{H}", (c1.o.n_dst, H, 1))
+    dz = synth.normal(synth.grad_seed(21), f"bdz{H}{F}", (c1.o.n_dst, H, F))
+    out, st = gnnk.gat_aggregate(c1.g, dev(feat), dev(el), dev(er), 0.2, want_stats=True)
+    m, l = row_stats(c1.o, el, er, 0.2)
+    nz = l[:, 0] > 0
+    assert_exact(host(st)[nz, :, 0], m[nz], "row max")
+    assert_close(host(st)[nz, :, 1], 1.0 / l[nz], name="row 1/sum")
+    gf, gl, gr = gnnk.gat_aggregate_backward(c1.g, dev(feat), dev(el), dev(er), 0.2, st, dev(dz))
+    rf, rl, rr = oracle_gat_backward(c1.o, feat, el, er, 0.2, dz)
+    assert_close(gf, rf, name="d feat")
+    assert_close(gl, rl, name="d el")
+    assert_close(gr, rr, name="d er")
+
+
+@pytest.mark.parametrize("seg", [2048, 64, 32])
+@pytest.mark.parametrize("no_fast", [0, 1])
+def test_gat_backward_hub_rows_c2(seg, no_fast):
+    gnnk.set_option("seg_edges", seg)
+    gnnk.set_option("no_fast", no_fast)
+    p = Pair.of(synth.graph_c2())
+    if seg < 2048:
+        info = p.g.info()
+        assert info["hub_dst_rows"] > 0 and info["hub_src_rows"] > 0
+    N = p.o.n_src
+    feat = synth.normal(S, "c2bf", (N, 8, 16))
+    el = synth.normal(S, "c2bel", (N, 8, 1))
+    er = synth.normal(S, "c2ber", (p.o.n_dst, 8, 1))
+    dz = synth.normal(synth.grad_seed(21), "c2bdz", (p.o.n_dst, 8, 16))
+    _, st = gnnk.gat_aggregate(p.g, dev(feat), dev(el), dev(er), 0.2, want_stats=True)
+    gf, gl, gr = gnnk.gat_aggregate_backward(p.g, dev(feat), dev(el), dev(er), 0.2, st, dev(dz))
+    rf, rl, rr = oracle_gat_backward(p.o, feat, el, er, 0.2, dz)
+    assert_close(gf, rf, name=f"d feat seg={seg}")
+    assert_close(gl, rl, name=f"d el seg={seg}")
+    assert_close(gr, rr, name=f"d er seg={seg}")
+
+
+def test_gat_backward_empty_rows_partial_grads_and_bf16():
+    # destinations 0, 2, 4 and sources 1, 4 have no edges
+    src = np.array([0, 2, 2, 3, 0], dtype=np.int32)
+    dst = np.array([1, 1, 3, 3, 3], dtype=np.int32)
+    p = Pair(src, dst, 5, 5)
+    feat = synth.normal(S, "ebf", (5, 2, 8))
+    el = synth.normal(S, "ebl", (5, 2, 1))
+    er = synth.normal(S, "ebr", (5, 2, 1))
+    dz = synth.normal(synth.grad_seed(21), "ebz", (5, 2, 8))
+    _, st = gnnk.gat_aggregate(p.g, dev(feat), dev(el), dev(er), 0.1, want_stats=True)
+    assert np.all(host(st)[[0, 2, 4]] == 0.0)
+    gf, gl, gr = gnnk.gat_aggregate_backward(p.g, dev(feat), dev(el), dev(er), 0.1, st, dev(dz))
+    rf, rl, rr = oracle_gat_backward(p.o, feat, el, er, 0.1, dz)
+    assert_close(gf, rf, name="d feat")
+    assert_close(gl, rl, name="d el")
+    assert_close(gr, rr, name="d er")
+    assert np.all(host(gf)[[1, 4]] == 0.0) and np.all(host(gr)[[0, 2, 4]] == 0.0)
+    # only some gradients
+    gf2, gl2, gr2 = gnnk.gat_aggregate_backward(p.g, dev(feat), dev(el), dev(er), 0.1, st, dev(dz), want_feat=False,
+                                                want_el=False)
+    assert gf2 is None and gl2 is None
+    assert_close(gr2, rr, name="d er alone")
+    # bf16 inputs: fp32/fp64 inside, outputs rounded once
+    c1 = Pair.of(synth.graph_c1())
+    fb = synth.to_bf16_bits(synth.normal(S, "bbf", (c1.o.n_src, 4, 8)))
+    lb = synth.to_bf16_bits(synth.normal(S, "bbl", (c1.o.n_src, 4, 1)))
+    rb = synth.to_bf16_bits(synth.normal(S, "bbr", (c1.o.n_dst, 4, 1)))
+    zb = synth.to_bf16_bits(synth.normal(synth.grad_seed(21), "bbz", (c1.o.n_dst, 4, 8)))
+    _, st = gnnk.gat_aggregate(c1.g, dev(fb), dev(lb), dev(rb), 0.2, want_stats=True)
+    gf, gl, gr = gnnk.gat_aggregate_backward(c1.g, dev(fb), dev(lb), dev(rb), 0.2, st, dev(zb))
+    w = orc.bf16_to_f32
+    rf, rl, rr = oracle_gat_backward(c1.o, w(fb), w(lb), w(rb), 0.2, w(zb))
+    assert_close(gf, rf, kind="bf16", name="bf16 d feat")
+    assert_close(gl, rl, kind="bf16", name="bf16 d el")
+    assert_close(gr, rr, kind="bf16", name="bf16 d er")
+
+
+def test_gat_backward_wide_rows_unsupported(c1):
+    """H * F / 4 > 64 columns per lane group: the fused backward declines
+    with GNNK_EUNSUPPORTED, as the unfused attention gradient (a reduction
+    over F across the lane group) does."""
+    N = c1.o.n_src
+    feat = synth.normal(S, "wf", (N, 4, 100))
+    el = synth.normal(S, "wl", (N, 4, 1))
+    er = synth.normal(S, "wr", (c1.o.n_dst, 4, 1))
+    _, st = gnnk.gat_aggregate(c1.g, dev(feat), dev(el), dev(er), 0.2, want_stats=True)
+    with pytest.raises(gnnk.GnnkError) as e:
+        gnnk.gat_aggregate_backward(c1.g, dev(feat), dev(el), dev(er), 0.2, st, dev(feat[: c1.o.n_dst]))
+    assert e.value.status == gnnk.EUNSUPPORTED
+    a = dev(synth.uniform(S, "wa", (c1.o.n_edges, 4, 1), 0.0, 1.0))
+    with pytest.raises(gnnk.GnnkError) as e:
+        gnnk.gspmm_backward(c1.g, "mul", "sum", dev(feat), a, dev(feat[: c1.o.n_dst]))
+    assert e.value.status == gnnk.EUNSUPPORTED

@@ -176,7 +176,8 @@ def test_gsddmm_elementwise_bit_exact(c1, op, lt, rt):
     assert_exact(out, ref, f"{lt}_{op}_{rt}")
 
 
-@pytest.mark.parametrize("shape", [(1, 16), (2, 8), (4, 4), (1, 13)])
+# F / 4 lanes per head: 4, 2, 1, (13 columns: one per lane), 8, 16, 32
+@pytest.mark.parametrize("shape", [(1, 16), (2, 8), (4, 4), (1, 13), (2, 32), (1, 64), (1, 128)])
 @pytest.mark.parametrize("lt,rt", [("u", "v"), ("u", "e"), ("v", "u")])
 def test_gsddmm_dot(c1, shape, lt, rt):
     rows = {"u": c1.o.n_src, "e": c1.o.n_edges, "v": c1.o.n_dst}
@@ -221,7 +222,10 @@ def test_leaky_relu_bit_exact(c1):
 
 @pytest.mark.parametrize("op", OPS)
 @pytest.mark.parametrize("reduce", ["sum", "mean", "max", "min"])
-@pytest.mark.parametrize("shapes", [((1, 16), (1, 1)), ((1, 16), (1, 16)), ((4, 4), (4, 1)), ((4, 1), (4, 4))])
+# ((2, 32), (2, 1)) and ((1, 64), (1, 1)): the edge gradient sums 8 and 16
+# lanes per head (the DPP steps of the lane reductions)
+@pytest.mark.parametrize("shapes", [((1, 16), (1, 1)), ((1, 16), (1, 16)), ((4, 4), (4, 1)), ((4, 1), (4, 4)),
+                                    ((2, 32), (2, 1)), ((1, 64), (1, 1))])
 def test_gspmm_backward_c1(c1, op, reduce, shapes):
     (xh, xf), (wh, wf) = shapes
     if op == "copy_lhs":
