@@ -296,14 +296,23 @@ void set_edge_chunks(EngineArgs& A, int64_t E, const Geo& geo) {
 }
 
 // A row-reduction (g-SpMM) pass: sums, with hub partials and their combine.
+// fused_dw (nullable): the caller set A.x2 / A.out2 / A.red2 / A.per_head2
+// for a u_mul_e/sum backward and asks for the edge gradient in this pass;
+// *fused_dw tells whether it was written (else the caller runs its g-SDDMM)
 gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& geo, int dtype, int opk,
-                         hipStream_t s) {
+                         hipStream_t s, bool* fused_dw = nullptr) {
     A.csr = csr_of(g, d);
     set_geo(A, geo);
     A.sch = schedule(d, geo, true);
     A.partial_stride = geo.D;
     const Pick pk = pick_spmm(g, d, A, geo, dtype, opk, false);
     const int walk = pick_walk(d, A.out.reduce != 0);
+    if (fused_dw) {
+        const int r2 = A.red2;
+        *fused_dw = walk == 0 && (pk.spec == SP_UE_H || pk.spec == SP_UE_R) &&
+                    (pk.gc == 1 || pk.gc == 2 || pk.gc == 4) && geo.nchunk == 1 && r2 >= 1 &&
+                    (r2 & (r2 - 1)) == 0 && r2 <= geo.L;
+    }
     if (walk) {
         set_edge_chunks(A, g->n_edges, geo);
         const size_t need = walk == 3 ? (size_t)d.n_rows * geo.D * 8 : (size_t)2 * A.n_sub * geo.D * 8;
@@ -331,7 +340,11 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
         A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 8);
         if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
     }
-    gnnk_status st = launch_status(launch_spmm(A, dtype, geo.vec, false, opk, pk.spec, pk.gc, s), "g-SpMM launch");
+    gnnk_status st = (fused_dw && *fused_dw)
+                         ? launch_status(launch_spmm_dw(A, dtype, geo.vec, pk.spec, pk.gc, s),
+                                         "g-SpMM launch (with the edge gradient)")
+                         : launch_status(launch_spmm(A, dtype, geo.vec, false, opk, pk.spec, pk.gc, s),
+                                         "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
         st = launch_status(launch_spmm_combine(A, dtype, geo.vec, false, s), "g-SpMM combine launch");
     return st;
@@ -508,6 +521,7 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
         return fail(GNNK_EINVAL, "grad_rhs must have rhs's shape");
     const int dt = dtype_code(grad_out);
     const int32_t scale_flags = (reduce == GNNK_MEAN ? F_SCALE_A_DEG : 0) | (cmp ? F_MASK_A : 0);
+    bool dw_done = false;
 
     if (grad_lhs && g->n_src > 0) {
         // Lemma complex_dspmm_dx: a g-SpMM on the reverse graph, message dZ[v] * d phi / d x
@@ -547,10 +561,23 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
             A.mask_arg = reinterpret_cast<const int32_t*>(bits);
             A.mask_ld = words;
         }
-        st = run_spmm_sum(g, g->out, A, geo, dt, opk, stream);
+        // u_mul_e/sum with a per-head or per-edge weight: the weight's
+        // gradient dZ[v] . X[u] in the same reverse pass (the pass has dZ[v]
+        // in its lanes and X[u] is the row's own), written at the edge id
+        const bool want_dw = grad_rhs && g->n_edges > 0 && op == GNNK_MUL && reduce == GNNK_SUM && rhs->feat == 1 &&
+                             (rhs->heads == Hm || rhs->heads == 1) && lhs->heads == Hm && lhs->feat == Fm;
+        if (want_dw) {
+            A.x2 = lhs->data;
+            A.x2_stride = lhs->row_stride;
+            A.out2 = grad_rhs->data;
+            A.out2_stride = grad_rhs->row_stride;
+            A.per_head2 = rhs->heads > 1 ? 1 : 0;
+            A.red2 = A.per_head2 ? Fm / geo.vec : (int32_t)geo.NV;
+        }
+        st = run_spmm_sum(g, g->out, A, geo, dt, opk, stream, want_dw ? &dw_done : nullptr);
         if (st != GNNK_OK) return st;
     }
-    if (grad_rhs && g->n_edges > 0) {
+    if (grad_rhs && g->n_edges > 0 && !dw_done) {
         // the lemma on dL/dW of g-SpMM: a g-SDDMM, message dZ[v] * d phi / d w
         std::vector<Member> ms{{grad_out, K_FULL}};
         if (op == GNNK_MUL || op == GNNK_DIV) ms.push_back({lhs, K_FULL});

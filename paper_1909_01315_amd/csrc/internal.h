@@ -137,6 +137,14 @@ struct EngineArgs {
     int32_t sub_edges;       // edge-parallel walks: positions per lane group (a sub-chunk)
     int32_t n_sub;           // edge-parallel walks: number of sub-chunks
     int32_t pad2;
+    // fused edge gradient of a reverse-graph g-SpMM (u_mul_e/sum backward):
+    // out2[edge] = sum over runs of red2 lanes of a . x2[row], per head or per row
+    const void* x2;          // the walked row's own operand (lhs of the forward), full rows
+    int64_t x2_stride;
+    void* out2;              // per-edge output (grad of the edge weight)
+    int64_t out2_stride;
+    int32_t red2;            // lanes summed per output value (a power of two)
+    int32_t per_head2;       // 1: one value per head, 0: one per edge
 };
 
 // Operand layouts with kernels specialised at compile time (the host picks
@@ -159,6 +167,9 @@ enum SpecId : int32_t {
 bool fast_vec(int dtype, int vec);
 hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, int spec, int gc,
                        hipStream_t s);
+// u_mul_e/sum backward in one reverse pass: dX as launch_spmm with spec
+// SP_UE_H or SP_UE_R (gc 1, 2 or 4), and the edge gradient into a.out2
+hipError_t launch_spmm_dw(const EngineArgs& a, int dtype, int vec, int spec, int gc, hipStream_t s);
 hipError_t launch_spmm_combine(const EngineArgs& a, int dtype, int vec, bool maxmin, hipStream_t s);
 // edge-parallel (COO) walks, edge.hip: mode 0 = partials of split rows combined
 // in order afterwards, mode 1 = fp64 atomics into scratch (a.partial, rows x D)

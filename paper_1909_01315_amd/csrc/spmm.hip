@@ -9,6 +9,8 @@
 // and min compare fp32 messages and break ties toward the smaller edge id.
 // The edge loop loads the next batch's indices while the current batch's
 // gathers are in flight.
+#include <type_traits>
+
 #include "walk.h"
 
 namespace gnnk {
@@ -16,7 +18,30 @@ namespace gnnk {
 // ---------------------------------------------------------------------------
 // sums
 
-template <typename T, int VEC, int OPK, int EXT, class S>
+// DW: also write, per edge, the dot of a (dZ[v]) with the row's own x2
+// (X[u]) over runs of red2 lanes -- the edge-weight gradient of u_mul_e/sum,
+// computed in the reverse pass that gathers dZ[v] anyway
+template <typename T, int VEC, bool DW>
+struct EdgeDot {
+    float x[VEC];
+    __device__ __forceinline__ void load(const EngineArgs& A, int32_t self, int col0) {
+        if constexpr (DW) IO<T, VEC>::load(reinterpret_cast<const T*>(A.x2) + (int64_t)self * A.x2_stride + col0, x);
+    }
+    __device__ __forceinline__ void put(const EngineArgs& A, const Raw<VEC>& rw, int32_t ed, bool ok, int lig,
+                                        int h, bool active) {
+        if constexpr (DW) {
+            double dp = 0.0;
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) dp = fma((double)rw.a[i], (double)x[i], dp);
+            dp = run_sum(dp, A.red2);
+            if (ok & active & ((lig & (A.red2 - 1)) == 0))
+                IO<T, 1>::store1(reinterpret_cast<T*>(A.out2) + (int64_t)ed * A.out2_stride + (A.per_head2 ? h : 0),
+                                 (float)dp);
+        }
+    }
+};
+
+template <typename T, int VEC, int OPK, int EXT, class S, bool DW = false>
 __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
     const int w = wave_id();
     if (w >= A.sch.w_total) return;
@@ -50,6 +75,8 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
             for (int i = 0; i < VEC; ++i) acc[i] = 0.0;
             Pre<VEC> pre;
             load_pre<T, VEC, OPK, S>(A, (int32_t)r, col0, h, pre);
+            EdgeDot<T, VEC, DW> dw;
+            dw.load(A, (int32_t)r, col0);
             auto sink = [&](const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
                 // winner masks: most slots of a wavefront won no column at all
                 if constexpr (EXT == EXT_BITS)
@@ -58,6 +85,7 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
                 combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) acc[i] += ok ? m[i] : 0.0;
+                dw.put(A, rw, ed, ok, ln.lig, h, active);
             };
             walk_row<T, VEC, OPK, EXT, S>(A, (int32_t)r, b, e, ln.g, G, col0, h, pre, sink);
             sum_groups<S::GC, VEC>(geo, acc);
@@ -91,6 +119,8 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
             for (int i = 0; i < VEC; ++i) acc[i] = 0.0;
             Pre<VEC> pre;
             load_pre<T, VEC, OPK, S>(A, self, col0, h, pre);
+            EdgeDot<T, VEC, DW> dw;
+            dw.load(A, self, col0);
             auto sink = [&](const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
                 // winner masks: most slots of a wavefront won no column at all
                 if constexpr (EXT == EXT_BITS)
@@ -99,6 +129,7 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
                 combine_f64<VEC, OPK, EXT>(A, rw, ed, m);
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) acc[i] += ok ? m[i] : 0.0;
+                dw.put(A, rw, ed, ok, ln.lig, h, active);
             };
             walk_lane<T, VEC, OPK, EXT, S>(A, self, b, e, col0, h, pre, sink);
             write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, true, !S::FAST);
@@ -436,7 +467,34 @@ void launch_cmp_t(const EngineArgs& a, int opk, int spec, int gc, dim3 grid, dim
     GNNK_OPK_DISPATCH(opk, { hipLaunchKernelGGL((spmm_cmp_kernel<T, V, K, SpecDyn>), grid, block, 0, s, a); })
 }
 
+template <typename T, int V>
+void launch_dw_t(const EngineArgs& a, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
+    if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
+        auto go = [&](auto cg) {
+            constexpr int C = decltype(cg)::value;
+            if (spec == SP_UE_H)
+                hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUEH<C, false>, true>), grid, block, 0, s, a);
+            else
+                hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUER<C, false>, true>), grid, block, 0, s, a);
+        };
+        if (gc == 1) go(std::integral_constant<int, 1>{});
+        else if (gc == 2) go(std::integral_constant<int, 2>{});
+        else go(std::integral_constant<int, 4>{});
+    }
+}
+
 }  // namespace
+
+hipError_t launch_spmm_dw(const EngineArgs& a, int dtype, int vec, int spec, int gc, hipStream_t s) {
+    if (a.sch.w_total <= 0) return hipSuccess;
+    const dim3 grid(blocks_for_waves(a.sch.w_total)), block(WAVE * WPB);
+    if (dtype == 0) {
+        GNNK_VEC_DISPATCH_F32(vec, launch_dw_t<float, V>(a, spec, gc, grid, block, s))
+    } else {
+        GNNK_VEC_DISPATCH_BF16(vec, launch_dw_t<bf16_t, V>(a, spec, gc, grid, block, s))
+    }
+    return hipGetLastError();
+}
 
 hipError_t launch_spmm(const EngineArgs& a, int dtype, int vec, bool maxmin, int opk, int spec, int gc,
                        hipStream_t s) {

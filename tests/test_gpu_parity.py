@@ -188,6 +188,28 @@ def test_gsddmm_dot(c1, shape, lt, rt):
     assert_close(out, ref, name="dot")
 
 
+@pytest.mark.parametrize("shapes", [((2, 32), (2, 1)), ((1, 64), (1, 1)), ((8, 16), (8, 1)), ((8, 16), (1, 1))])
+@pytest.mark.parametrize("seg", [2048, 64])
+def test_edge_gradient_in_the_reverse_pass_is_bit_identical(shapes, seg):
+    """u_mul_e/sum backward with both gradients computes the edge-weight
+    gradient inside the reverse pass (64+ columns); alone it is a g-SDDMM.
+    Both sum the same fp64 products in the same lane order: bit-identical."""
+    gnnk.set_option("seg_edges", seg)
+    sg = synth.graph_c2()
+    p = Pair.of(sg)
+    (xh, xf), (wh, wf) = shapes
+    X = feats(S1, f"fX{xh}{xf}", (p.o.n_src, xh, xf))
+    W = feats(S1, f"fW{wh}", (p.o.n_edges, wh, wf), 0.5, 1.5)
+    dZ = feats(G1, f"fdZ{xh}{xf}", (p.o.n_dst, xh, xf))
+    dX, dW = gnnk.gspmm_backward(p.g, "mul", "sum", dev(X), dev(W), dev(dZ))
+    _, dW1 = gnnk.gspmm_backward(p.g, "mul", "sum", dev(X), dev(W), dev(dZ), want_lhs=False)
+    assert torch.equal(dW, dW1)
+    _, ref = orc.gspmm_backward(p.o, "mul", "sum", X, W, dZ, want_lhs=False)
+    assert_close(dW, ref, name="edge gradient")
+    gl, _ = orc.gspmm_backward(p.o, "mul", "sum", X, W, dZ, want_rhs=False)
+    assert_close(dX, gl, name="dX")
+
+
 def test_gsddmm_u_add_v_scores(c1):
     el = feats(S1, "el", (c1.o.n_src, 4, 1))
     er = feats(S1, "er", (c1.o.n_dst, 4, 1))
