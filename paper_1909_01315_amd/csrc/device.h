@@ -60,6 +60,8 @@ struct IO<float, VEC> {
         }
     }
     static __device__ __forceinline__ void store1(float* p, float v) { *p = v; }
+    // streaming store: scattered outputs that no later load of the kernel reads
+    static __device__ __forceinline__ void store1_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
 };
 
 template <int VEC>
@@ -97,6 +99,9 @@ struct IO<bf16_t, VEC> {
         }
     }
     static __device__ __forceinline__ void store1(bf16_t* p, float v) { *p = (bf16_t)f2bf(v); }
+    static __device__ __forceinline__ void store1_nt(bf16_t* p, float v) {
+        __builtin_nontemporal_store((bf16_t)f2bf(v), p);
+    }
 };
 
 template <int VEC>

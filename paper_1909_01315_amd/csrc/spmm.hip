@@ -35,8 +35,8 @@ struct EdgeDot {
             for (int i = 0; i < VEC; ++i) dp = fma((double)rw.a[i], (double)x[i], dp);
             dp = run_sum(dp, A.red2);
             if (ok & active & ((lig & (A.red2 - 1)) == 0))
-                IO<T, 1>::store1(reinterpret_cast<T*>(A.out2) + (int64_t)ed * A.out2_stride + (A.per_head2 ? h : 0),
-                                 (float)dp);
+                IO<T, 1>::store1_nt(reinterpret_cast<T*>(A.out2) + (int64_t)ed * A.out2_stride +
+                                        (A.per_head2 ? h : 0), (float)dp);
         }
     }
 };
