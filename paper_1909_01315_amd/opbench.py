@@ -137,6 +137,13 @@ def c3(R: Rows):
           lambda: gnnk.edge_softmax(g, S2, out=S3))
     R.add("c3", "fused attention (u_add_v, leaky, softmax, u_mul_e/sum) H=8 F=16", "f32", "fwd",
           E * (512 + 32 + 4) + N * (512 + 32) + off, D, E, lambda: gnnk.gat_aggregate(g, X, el, er, 0.2, out=Z))
+    _, stats = gnnk.gat_aggregate(g, X, el, er, 0.2, want_stats=True)
+    # pass A gathers feat and el per edge (dZ, er, stats per row); pass B
+    # gathers dZ and a 16-byte record per edge (feat, el per row)
+    R.add("c3", "fused attention backward (two passes, no E-sized tensor)", "f32", "bwd",
+          E * (512 + 32 + 4) + N * (512 + 32 + 64 + 32 + 128) + off +
+          E * (512 + 128 + 4) + N * (512 + 32 + 512 + 32) + off, D, E,
+          lambda: gnnk.gat_aggregate_backward(g, X, el, er, 0.2, stats, dZ))
     # backward passes
     R.add("c3", "u_mul_e/sum H=8: d feat (reverse graph)", "f32", "bwd",
           E * (512 + 32 + 4 + 4) + N * 512 + off, D, E,
@@ -144,6 +151,9 @@ def c3(R: Rows):
     R.add("c3", "u_mul_e/sum H=8: d attention (per-head u_dot_v)", "f32", "bwd",
           E * (512 + 4 + 32) + N * 512 + off, D, E,
           lambda: gnnk.gspmm_backward(g, "mul", "sum", X, a, dZ, want_lhs=False, grad_rhs=M8))
+    R.add("c3", "u_mul_e/sum H=8: d feat and d attention in one reverse pass", "f32", "bwd",
+          E * (512 + 32 + 4 + 4 + 32) + N * (512 + 512) + off, D, E,
+          lambda: gnnk.gspmm_backward(g, "mul", "sum", X, a, dZ, grad_lhs=dX, grad_rhs=M8))
     R.add("c3", "copy_u/mean D=128: dX (reverse graph)", "f32", "bwd",
           E * (512 + 4) + N * (512 + 4) + off, D, E,
           lambda: gnnk.gspmm_backward(g, "copy_lhs", "mean", X1, None, dZ1, grad_lhs=Z1))
