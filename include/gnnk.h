@@ -118,8 +118,10 @@ typedef struct {
  * back the sorted degrees) and may allocate the handle's scratch buffer. */
 
 /* Upper bound of the workspace for a graph of this size; ptr_t is the width
- * of the CSR row offsets the handle builds (GNNK_I64 needed when
- * num_edges >= 2^31). */
+ * of the CSR row offsets the handle builds (either width for any size).
+ * Node counts must be below 2^31 - 1 and num_edges at most 2^31 - 2^16 - 1
+ * (edge ids and CSR positions are int32, and the walks step positions past a
+ * row's end before testing them); GNNK_EINVAL otherwise. */
 gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_itype ptr_t,
                                   size_t* bytes);
 

@@ -126,8 +126,13 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t h
     return L;
 }
 
+// Edge ids and CSR positions are int32.  The walks advance a position past a
+// row's end by at most 64 lane groups x 4 slots before testing it, so edge
+// counts stay 2^16 below the int32 limit and no position arithmetic wraps.
+constexpr int64_t MAX_EDGES = (int64_t)INT32_MAX - 65536;
+
 bool sizes_ok(int64_t n_src, int64_t n_dst, int64_t E) {
-    return n_src >= 0 && n_dst >= 0 && E >= 0 && n_src < INT32_MAX && n_dst < INT32_MAX && E < INT32_MAX;
+    return n_src >= 0 && n_dst >= 0 && E >= 0 && n_src < INT32_MAX && n_dst < INT32_MAX && E <= MAX_EDGES;
 }
 
 // bits of a row id below n_rows
@@ -370,7 +375,7 @@ gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_
                                   size_t* bytes) {
     clear_error();
     if (!bytes) return fail(GNNK_EINVAL, "bytes is NULL");
-    if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (int32 ids)");
+    if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (node counts < 2^31 - 1, edges <= 2^31 - 2^16 - 1)");
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
     // hub rows have more than S edges: at most E / S of them, and at most
     // E / S + (hub rows) <= 2 E / S segments
@@ -387,7 +392,7 @@ gnnk_status graph_create_coo(int64_t num_src, int64_t num_dst, int64_t num_edges
     clear_error();
     if (!out) return fail(GNNK_EINVAL, "out is NULL");
     *out = nullptr;
-    if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (int32 ids)");
+    if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (node counts < 2^31 - 1, edges <= 2^31 - 2^16 - 1)");
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
     if (num_edges > 0 && (!src || !dst)) return fail(GNNK_EINVAL, "src/dst is NULL");
     Builder b{new_graph(num_src, num_dst, num_edges, ptr_t), nullptr, {}, nullptr, stream};
@@ -406,7 +411,7 @@ gnnk_status graph_create_csr(int64_t num_src, int64_t num_dst, int64_t num_edges
     clear_error();
     if (!out) return fail(GNNK_EINVAL, "out is NULL");
     *out = nullptr;
-    if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (int32 ids)");
+    if (!sizes_ok(num_src, num_dst, num_edges)) return fail(GNNK_EINVAL, "sizes out of range (node counts < 2^31 - 1, edges <= 2^31 - 2^16 - 1)");
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
     if (!indptr || (num_edges > 0 && !indices)) return fail(GNNK_EINVAL, "indptr/indices is NULL");
     Builder b{new_graph(num_src, num_dst, num_edges, ptr_t), nullptr, {}, nullptr, stream};

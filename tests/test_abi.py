@@ -62,3 +62,8 @@ def test_workspace_bound_grows_with_size(lib):
     assert b2.value > b1.value >= 10000 * 4 * 4
     assert lib.graph_workspace_bytes(-1, 10, 10, gnnk.I32, ctypes.byref(b1)) == gnnk.EINVAL
     assert lib.graph_workspace_bytes(10, 10, 10, 7, ctypes.byref(b1)) == gnnk.EINVAL
+    # edge counts up to 2^31 - 2^16 - 1 (int32 positions never wrap in the walks)
+    top = (1 << 31) - (1 << 16) - 1
+    assert lib.graph_workspace_bytes(10, 10, top, gnnk.I64, ctypes.byref(b1)) == gnnk.OK
+    assert lib.graph_workspace_bytes(10, 10, top + 1, gnnk.I64, ctypes.byref(b1)) == gnnk.EINVAL
+    assert lib.graph_workspace_bytes((1 << 31) - 1, 10, 10, gnnk.I32, ctypes.byref(b1)) == gnnk.EINVAL

@@ -159,3 +159,45 @@ def test_build_is_deterministic_and_timed():
             assert torch.equal(x, y)
     g1.destroy()
     g2.destroy()
+
+
+def test_graphs_without_nodes_or_edges():
+    """zero sources, zero destinations, or both: the build and every pass
+    accept empty operands and write nothing out of range"""
+    z = torch.zeros(0, dtype=torch.int32, device="cuda")
+    for ns, nd in ((0, 0), (0, 7), (5, 0)):
+        g = gnnk.Graph.from_coo(z, z, ns, nd)
+        info = g.info()
+        assert info["num_edges"] == 0 and info["max_in_degree"] == 0 and info["max_out_degree"] == 0
+        X = torch.randn(ns, 1, 8, device="cuda")
+        out = gnnk.gspmm(g, "copy_lhs", "sum", X)
+        assert out.shape == (nd, 1, 8) and torch.all(out == 0)
+        m, au, ae = gnnk.gspmm(g, "copy_lhs", "max", X, want_args=True)
+        assert torch.all(ae == -1)
+        dz = torch.randn(nd, 1, 8, device="cuda")
+        dx, _ = gnnk.gspmm_backward(g, "copy_lhs", "sum", X, None, dz)
+        assert dx.shape == (ns, 1, 8) and torch.all(dx == 0)
+        hp, hi, he = g.csr_export(reverse=True)
+        assert hp.numel() == ns + 1 and torch.all(hp == 0)
+        g.destroy()
+
+
+def test_maximum_edge_count():
+    """2^31 - 2^16 - 1 edges, the largest count int32 edge ids and positions
+    allow (4,096 nodes, every row a hub row of about 2^19 edges): the device
+    build and g-SpMM copy_u/sum of ones give the exact in- and out-degrees
+    (torch.bincount; degrees stay below 2^24, exact in fp32)."""
+    E = (1 << 31) - (1 << 16) - 1
+    n = 4096
+    gen = torch.Generator(device="cuda").manual_seed(7)
+    src = torch.randint(0, n, (E,), dtype=torch.int32, device="cuda", generator=gen)
+    dst = torch.randint(0, n, (E,), dtype=torch.int32, device="cuda", generator=gen)
+    g = gnnk.Graph.from_coo(src, dst, n, n, ptr64=True)
+    assert g.info()["num_edges"] == E
+    ones = torch.ones(n, 1, 1, device="cuda")
+    indeg = torch.bincount(dst.long(), minlength=n).float()
+    assert torch.equal(gnnk.gspmm(g, "copy_lhs", "sum", ones).view(-1), indeg)
+    outdeg = torch.bincount(src.long(), minlength=n).float()
+    dx, _ = gnnk.gspmm_backward(g, "copy_lhs", "sum", ones, None, ones)
+    assert torch.equal(dx.view(-1), outdeg)
+    g.destroy()
