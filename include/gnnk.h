@@ -21,7 +21,9 @@
  *    the caller; the library never frees them.  A NULL tensor pointer means
  *    "absent" where the argument is documented nullable.
  *  - Work is enqueued on `stream` and runs asynchronously; calls return before
- *    the kernels finish.  Only graph_create_* and graph_validate synchronise.
+ *    the kernels finish.  Only graph_create_* and graph_validate synchronise,
+ *    and a call that has to grow the handle's scratch buffer (its first call
+ *    of a larger kind; warm up once before capturing a HIP graph).
  *  - Outputs are fully overwritten, never accumulated into.  Inputs may alias
  *    each other; outputs must not alias inputs or each other.
  *  - Edge tensors are indexed by edge id.  Node tensors by node id.
