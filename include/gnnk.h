@@ -282,7 +282,10 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
  * schedules; the paper's Table 1 states both are valid for commutative and
  * associative reducers).  Process-wide; "seg_edges" applies to graphs created
  * afterwards, the others to calls issued afterwards.  Keys:
- *   "seg_edges"   edges per hub-row segment (>= 32; default 2048)
+ *   "seg_edges"   edges per hub-row segment: 0 (default) chooses per graph
+ *                 the next power of two of num_edges / 2048 within [64, 2048]
+ *                 (small graphs split their long rows across more
+ *                 wavefronts); otherwise a fixed value in [32, 2^30]
  *   "no_split"    1: never split a row across waves (hub rows run whole)
  *   "small_deg"   rows of at most this in-degree share a wave (-1 = auto)
  *   "schedule"    0 auto (the row engine), 1 the row engine (node-parallel over the degree-

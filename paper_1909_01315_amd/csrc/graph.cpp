@@ -42,6 +42,13 @@ Options& options() {
     return o;
 }
 
+int64_t seg_edges_for(int64_t E) {
+    if (options().seg_edges > 0) return options().seg_edges;
+    int64_t S = 64;
+    while (S < 2048 && S * 2048 < E) S <<= 1;
+    return S;
+}
+
 int64_t Dir::count_above(int64_t t) const {
     // sorted_deg is descending: the first position whose degree is <= t is the
     // first x with t >= x
@@ -279,7 +286,7 @@ gnnk_graph* new_graph(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_
     g->n_dst = num_dst;
     g->n_edges = num_edges;
     g->ptr64 = ptr_t == GNNK_I64;
-    g->seg_edges = options().seg_edges;
+    g->seg_edges = seg_edges_for(num_edges);
     return g;
 }
 
@@ -379,7 +386,7 @@ gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
     // hub rows have more than S edges: at most E / S of them, and at most
     // E / S + (hub rows) <= 2 E / S segments
-    int64_t S = options().seg_edges;
+    int64_t S = seg_edges_for(num_edges);
     int64_t hub = num_edges / S + 1, seg = 2 * num_edges / S + 2;
     Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, hub, hub, seg, seg);
     *bytes = L.total;
@@ -509,7 +516,8 @@ gnnk_status gnnk_set_option(const char* key, int64_t value) {
     if (!key) return fail(GNNK_EINVAL, "NULL key");
     std::string k(key);
     if (k == "seg_edges") {
-        if (value < 32 || value > (1 << 30)) return fail(GNNK_EINVAL, "seg_edges must be in [32, 2^30]");
+        if (value != 0 && (value < 32 || value > (1 << 30)))
+            return fail(GNNK_EINVAL, "seg_edges is 0 (per graph, from its edge count) or in [32, 2^30]");
         options().seg_edges = value;
     } else if (k == "no_split") {
         if (value != 0 && value != 1) return fail(GNNK_EINVAL, "no_split is 0 or 1");

@@ -53,7 +53,7 @@ struct gnnk_graph {
 namespace gnnk {
 
 struct Options {
-    int64_t seg_edges = 2048;
+    int64_t seg_edges = 0;  // 0: chosen per graph from its edge count (seg_edges_for)
     int64_t no_split = 0;
     int64_t small_deg = -1;
     int64_t no_fast = 0;  // 1: every call uses the runtime-layout kernels
@@ -61,6 +61,11 @@ struct Options {
     int64_t edge_chunk = 0; // positions per lane group of edge-parallel walks, 0 = auto
 };
 Options& options();
+
+// edges per hub-row segment for a graph of E edges: the option when set, else
+// the next power of two of E / 2048 within [64, 2048] -- small graphs split
+// their long rows so that enough wavefronts share the work
+int64_t seg_edges_for(int64_t E);
 
 gnnk_status fail(gnnk_status st, const char* fmt, ...);
 gnnk_status hip_fail(hipError_t e, const char* what);

@@ -81,9 +81,10 @@ def assert_exact(gpu, ref, name="result"):
     assert not bad.any(), report(name, g, ref, bad, 0)
 
 
-def check_formats(p, seg_edges=2048):
+def check_formats(p, seg_edges=None):
     """Both CSRs, degrees and the schedule counts of a handle against the
-    oracle's CSR (stable counting sort by row, ascending edge id in a row)."""
+    oracle's CSR (stable counting sort by row, ascending edge id in a row);
+    seg_edges defaults to the handle's own segment size."""
     ip, ii, ie = orc.csr(p.o, reverse=False)
     rp, ri, re_ = orc.csr(p.o, reverse=True)
     gp, gi, ge = p.g.csr_export(reverse=False)
@@ -98,6 +99,8 @@ def check_formats(p, seg_edges=2048):
     assert_exact(p.g.in_degrees(), ind.astype(np.int32), "in-degrees")
     assert_exact(p.g.out_degrees(), outd.astype(np.int32), "out-degrees")
     info = p.g.info()
+    if seg_edges is None:
+        seg_edges = info["seg_edges"]
     assert info["max_in_degree"] == (ind.max() if ind.size else 0)
     assert info["max_out_degree"] == (outd.max() if outd.size else 0)
     assert info["empty_dst_rows"] == int((ind == 0).sum())

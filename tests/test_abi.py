@@ -52,6 +52,7 @@ def test_host_side_errors(lib):
     assert lib.gnnk_set_option(b"no_such_option", 1) == gnnk.EINVAL
     assert b"unknown option" in lib.gnnk_last_error()
     assert lib.gnnk_set_option(b"seg_edges", 1) == gnnk.EINVAL
+    assert lib.gnnk_set_option(b"seg_edges", 0) == gnnk.OK  # per graph (the default)
     assert lib.edge_leaky_relu(None, None, ctypes.c_float(0.2), None) == gnnk.EINVAL
 
 

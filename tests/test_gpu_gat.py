@@ -29,7 +29,7 @@ def c2():
 @pytest.fixture(autouse=True)
 def reset_options():
     yield
-    gnnk.set_option("seg_edges", 2048)
+    gnnk.set_option("seg_edges", 0)
     gnnk.set_option("no_fast", 0)
 
 

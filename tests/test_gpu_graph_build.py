@@ -19,7 +19,7 @@ pytestmark = pytest.mark.gpu
 @pytest.fixture(autouse=True)
 def reset_options():
     yield
-    gnnk.set_option("seg_edges", 2048)
+    gnnk.set_option("seg_edges", 0)
 
 
 def random_edges(seed, n_src, n_dst, E, sort_by_dst=False):
@@ -201,3 +201,16 @@ def test_maximum_edge_count():
     dx, _ = gnnk.gspmm_backward(g, "copy_lhs", "sum", ones, None, ones)
     assert torch.equal(dx.view(-1), outdeg)
     g.destroy()
+
+
+def test_segment_size_follows_the_edge_count():
+    """seg_edges 0 (the default): the next power of two of E / 2048 within
+    [64, 2048]; a fixed option overrides it"""
+    for E, S in ((1000, 64), (200_000, 128), (1_000_000, 512), (9_000_000, 2048)):
+        src, dst = random_edges(E, 5000, 5000, E)
+        p = Pair(src, dst, 5000, 5000)
+        assert p.g.info()["seg_edges"] == S, E
+        check_formats(p)
+    gnnk.set_option("seg_edges", 300)
+    src, dst = random_edges(1, 50, 50, 1000)
+    assert Pair(src, dst, 50, 50).g.info()["seg_edges"] == 300
