@@ -287,7 +287,9 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
  *                 (small graphs split their long rows across more
  *                 wavefronts); otherwise a fixed value in [32, 2^30]
  *   "no_split"    1: never split a row across waves (hub rows run whole)
- *   "small_deg"   rows of at most this in-degree share a wave (-1 = auto)
+ *   "small_deg"   rows of at most this many edges take one lane group each
+ *                 and share a wavefront (-1 = auto: 32, or the lane groups
+ *                 per wavefront if more; none when a wavefront is one group)
  *   "schedule"    0 auto (the row engine), 1 the row engine (node-parallel over the degree-
  *                 sorted rows), 2 the edge-parallel walk over the COO form
  *                 (equal edges per lane group; split rows combined in a fixed

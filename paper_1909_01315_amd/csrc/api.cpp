@@ -150,7 +150,9 @@ SchedDev schedule(const Dir& d, const Geo& geo, bool fill_empty) {
     const bool split = o.no_split == 0;
     const int64_t n_hub = split ? d.n_hub : 0;
     const int64_t n_seg = split ? d.n_seg : 0;
-    int64_t T = o.small_deg >= 0 ? o.small_deg : (geo.G > 1 ? geo.G : 0);
+    // rows of at most T edges take one lane group each; automatic: 32 (at
+    // least the lane groups of a wavefront), none when a wavefront is one group
+    int64_t T = o.small_deg >= 0 ? o.small_deg : (geo.G > 1 ? std::max<int64_t>(geo.G, 32) : 0);
     int64_t n_big = std::max(d.count_above(T), n_hub);
     n_big = std::min(n_big, d.n_nz);
     const int fr = 4;
