@@ -31,6 +31,10 @@
  *  - All floating-point tensors of one call share one dtype.  Sums and dot
  *    products accumulate in fp64 and are rounded once to the output dtype
  *    (bf16 outputs: to fp32, then to bf16 round-to-nearest-even).
+ *  - Rows of any width: a sum over the features of a message (DOT, or the
+ *    gradient of an operand broadcast over features) wider than one pass of a
+ *    wavefront (64 lanes of 4 fp32 or 8 bf16 values) adds its passes in fp64
+ *    in order, and per-head sums of such rows run as slices of heads.
  *  - Calls that use the same graph handle must be ordered (one stream, or
  *    synchronised): the handle owns the scratch space of hub-row partials.
  */
@@ -270,7 +274,10 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
  * once.  feat, el, er, slope and stats as passed to (and written by)
  * gat_aggregate; grad_out (num_dst, H, F); the three gradients are nullable
  * and take their operand's shape; all tensors but stats share one dtype.
- * Needs H * F / vec <= 64 (GNNK_EUNSUPPORTED otherwise).  Uses the handle's
+ * A head must fit one pass of a wavefront, F / vec <= 64 (vec: 4 fp32 or 8
+ * bf16 values per lane as F and the row strides allow; GNNK_EUNSUPPORTED
+ * otherwise); rows of several heads wider than a pass run as slices of
+ * heads.  Uses the handle's
  * scratch: 16 bytes per (destination, head) plus per-segment partials of
  * hub rows.  Errors: GNNK_EINVAL on shapes or dtypes. */
 gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,

@@ -50,8 +50,11 @@ int pow2ceil(int x) {
 
 // Choose the canonical geometry of an (Hm, Fm) message read and written by
 // `ms`.  When no tensor broadcasts over features only, heads and features
-// merge into one row of Hm * Fm columns.
-gnnk_status choose_geo(int Hm, int Fm, std::vector<Member>& ms, const std::vector<const void*>& int_arrays, Geo& g) {
+// merge into one row of Hm * Fm columns, unless keep_heads (a kernel that
+// needs each lane's head, as the fused attention does; with Fm = 1 its
+// per-head scores have the shape of a full operand).
+gnnk_status choose_geo(int Hm, int Fm, std::vector<Member>& ms, const std::vector<const void*>& int_arrays, Geo& g,
+                       bool keep_heads = false) {
     for (auto& m : ms) {
         m.kind = kind_of(m.t, Hm, Fm);
         if (m.kind == K_BAD)
@@ -60,7 +63,7 @@ gnnk_status choose_geo(int Hm, int Fm, std::vector<Member>& ms, const std::vecto
     }
     bool any_heads = false;
     for (auto& m : ms) any_heads = any_heads || (m.kind == K_HEADS);
-    g.merged = !any_heads;
+    g.merged = !any_heads && !keep_heads;
     g.H = g.merged ? 1 : Hm;
     g.F = g.merged ? Hm * Fm : Fm;
     g.D = (int64_t)Hm * Fm;
@@ -118,8 +121,9 @@ gnnk_status out_desc(const gnnk_tensor* t, Kind k, const Geo& g, OutDev& o) {
         return GNNK_OK;
     }
     o.reduce = 1;
-    if (g.nchunk > 1) return fail(GNNK_EUNSUPPORTED, "reduced outputs need D / vec <= 64");
     if (k == K_HEADS && g.F != g.D) {
+        // the entry points split the heads into slices of at most one pass
+        if (g.nchunk > 1) return fail(GNNK_EUNSUPPORTED, "per-head sums wider than one pass of the wavefront");
         o.red = g.F / g.vec;
         o.per_head = 1;
     } else {
@@ -357,7 +361,13 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
     set_geo(A, geo);
     A.sch = schedule(g->in, geo, false);
     const Pick pk = pick_sddmm(g, A, geo, dtype, opk);
-    if (pick_walk(g->in, false)) {
+    const bool multi = A.out.reduce && geo.nchunk > 1;
+    if (multi) {
+        // running per-edge sums between the passes of a row wider than the wavefront
+        A.xacc = reinterpret_cast<double*>(graph_scratch(g, (size_t)g->n_edges * 8));
+        if (!A.xacc) return fail(GNNK_ENOMEM, "scratch allocation failed");
+    }
+    if (pick_walk(g->in, multi)) {
         set_edge_chunks(A, g->n_edges, geo);
         return launch_status(launch_sddmm_edge(A, g->n_edges, dtype, geo.vec, opk, pk.spec, pk.gc, s),
                              "edge-parallel g-SDDMM launch");
@@ -367,6 +377,38 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
 
 int32_t tgt_in(int t) { return t == GNNK_SRC ? T_NBR : (t == GNNK_EDGE ? T_EDGE : T_SELF); }   // in-CSR walk
 int32_t tgt_out(int t) { return t == GNNK_SRC ? T_SELF : (t == GNNK_EDGE ? T_EDGE : T_NBR); }  // reverse walk
+
+// Heads [h0, h0 + hc) of a (rows, Hm, F) tensor (a view: same rows and row
+// stride); a tensor broadcast over heads is shared by every slice.
+gnnk_tensor head_slice(const gnnk_tensor* t, int Hm, int h0, int hc) {
+    gnnk_tensor s = *t;
+    if (t->heads == Hm && Hm > 1) {
+        const size_t es = t->dtype == GNNK_BF16 ? 2 : 4;
+        if (s.data) s.data = static_cast<char*>(t->data) + (size_t)h0 * t->feat * es;
+        s.heads = hc;
+    }
+    return s;
+}
+
+// Heads per slice of a call with a per-head sum (an output holding one value
+// per head of an (Hm, Fm) message, Fm > 1) that would need more than one pass
+// of the wavefront: Fm / vec lanes per head, 64 lanes per pass; one head per
+// slice when a head alone is wider (its sum then runs over several passes).
+// 0: the call runs whole.
+int heads_per_slice(int Hm, int Fm, std::initializer_list<const gnnk_tensor*> all,
+                    std::initializer_list<const gnnk_tensor*> outs, const void* int_array = nullptr) {
+    if (Hm <= 1 || Fm <= 1) return 0;
+    bool per_head = false;
+    for (const gnnk_tensor* t : outs)
+        if (t && t->heads == Hm && t->feat == 1) per_head = true;
+    if (!per_head) return 0;
+    std::vector<Member> ms;
+    for (const gnnk_tensor* t : all)
+        if (t) ms.push_back({t, K_FULL});
+    Geo geo;
+    if (choose_geo(Hm, Fm, ms, {int_array}, geo) != GNNK_OK || geo.merged || geo.nchunk == 1) return 0;
+    return std::max(1, 64 / (Fm / geo.vec));
+}
 
 }  // namespace
 }  // namespace gnnk
@@ -465,6 +507,19 @@ gnnk_status gsddmm(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_t
     } else if (out->heads != Hm || out->feat != Fm) {
         return fail(GNNK_EINVAL, "out must have the message shape (%d, %d)", Hm, Fm);
     }
+    if (const int hs = heads_per_slice(Hm, Fm, {lhs, rhs, out}, {out})) {
+        // per-head dots wider than one pass: slices of heads, one call each
+        for (int h0 = 0; h0 < Hm; h0 += hs) {
+            const int hc = std::min(hs, Hm - h0);
+            gnnk_tensor l = use_l ? head_slice(lhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor r = use_r ? head_slice(rhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor o = head_slice(out, Hm, h0, hc);
+            gnnk_status st = gsddmm(g, op, use_l ? &l : nullptr, lhs_target, use_r ? &r : nullptr, rhs_target, &o,
+                                    stream);
+            if (st != GNNK_OK) return st;
+        }
+        return GNNK_OK;
+    }
     std::vector<Member> ms;
     if (use_l) ms.push_back({lhs, K_FULL});
     if (use_r) ms.push_back({rhs, K_FULL});
@@ -491,12 +546,11 @@ gnnk_status gsddmm(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_t
     return run_sddmm(g, A, geo, dtype_code(out), opk, stream);
 }
 
-gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
-                           const gnnk_tensor* rhs, const int32_t* arg_lhs, const int32_t* arg_rhs,
-                           const gnnk_tensor* grad_out, gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs,
-                           hipStream_t stream) {
-    clear_error();
-    (void)arg_lhs;
+// arg_ld: elements per row of arg_rhs (-1: H * F of the call; a head slice
+// keeps the stride of the whole array)
+static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                                 const gnnk_tensor* rhs, const int32_t* arg_rhs, const gnnk_tensor* grad_out,
+                                 gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs, hipStream_t stream, int64_t arg_ld) {
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
     if (op < GNNK_COPY_LHS || op > GNNK_DIV) return fail(GNNK_EINVAL, "gspmm op must be COPY_LHS..DIV");
     if (reduce < GNNK_SUM || reduce > GNNK_MIN) return fail(GNNK_EINVAL, "bad reduce");
@@ -521,6 +575,23 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
         return fail(GNNK_EINVAL, "grad_lhs must have lhs's shape");
     if (grad_rhs && (grad_rhs->rows != g->n_edges || grad_rhs->heads != rhs->heads || grad_rhs->feat != rhs->feat))
         return fail(GNNK_EINVAL, "grad_rhs must have rhs's shape");
+    const int64_t ld = arg_ld >= 0 ? arg_ld : (int64_t)Hm * Fm;
+    if (const int hs = heads_per_slice(Hm, Fm, {lhs, rhs, grad_out, grad_lhs, grad_rhs}, {grad_lhs, grad_rhs}, arg_rhs)) {
+        // per-head gradients wider than one pass: slices of heads, one call each
+        for (int h0 = 0; h0 < Hm; h0 += hs) {
+            const int hc = std::min(hs, Hm - h0);
+            gnnk_tensor l = use_l ? head_slice(lhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor r = use_r ? head_slice(rhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor go = head_slice(grad_out, Hm, h0, hc);
+            gnnk_tensor gl = grad_lhs ? head_slice(grad_lhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor gr = grad_rhs ? head_slice(grad_rhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_status st = spmm_backward(g, op, reduce, use_l ? &l : nullptr, use_r ? &r : nullptr,
+                                           arg_rhs ? arg_rhs + (size_t)h0 * Fm : nullptr, &go,
+                                           grad_lhs ? &gl : nullptr, grad_rhs ? &gr : nullptr, stream, ld);
+            if (st != GNNK_OK) return st;
+        }
+        return GNNK_OK;
+    }
     const int dt = dtype_code(grad_out);
     const int32_t scale_flags = (reduce == GNNK_MEAN ? F_SCALE_A_DEG : 0) | (cmp ? F_MASK_A : 0);
     bool dw_done = false;
@@ -546,7 +617,7 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
         A.flags = scale_flags;
         A.deg = g->in.deg;
         A.mask_arg = arg_rhs;
-        A.mask_ld = geo.D;
+        A.mask_ld = ld;
         if (cmp && g->n_edges > 0) {
             // the argmax scatter as a masked g-SpMM on the reverse graph: the
             // winning columns of each edge are marked once in a bit mask laid
@@ -555,8 +626,8 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
             const int32_t words = (int32_t)((geo.D + 31) / 32);
             uint32_t* bits = reinterpret_cast<uint32_t*>(graph_scratch(g, (size_t)g->n_edges * words * 4, 1));
             if (!bits) return fail(GNNK_ENOMEM, "scratch allocation failed");
-            st = launch_status(launch_winner_bits(arg_rhs, g->n_dst, (int32_t)geo.D, g->out.pos, bits, g->n_edges,
-                                                  words, stream),
+            st = launch_status(launch_winner_bits(arg_rhs, g->n_dst, (int32_t)geo.D, ld, g->out.pos, bits,
+                                                  g->n_edges, words, stream),
                                "winner mask launch");
             if (st != GNNK_OK) return st;
             A.flags = (scale_flags & ~F_MASK_A) | F_BITS_A;
@@ -606,11 +677,20 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
         A.flags = scale_flags | (op == GNNK_SUB ? F_NEGATE : 0);
         A.deg = g->in.deg;
         A.mask_arg = arg_rhs;
-        A.mask_ld = geo.D;
+        A.mask_ld = ld;
         st = run_sddmm(g, A, geo, dt, opk, stream);
         if (st != GNNK_OK) return st;
     }
     return GNNK_OK;
+}
+
+gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                           const gnnk_tensor* rhs, const int32_t* arg_lhs, const int32_t* arg_rhs,
+                           const gnnk_tensor* grad_out, gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs,
+                           hipStream_t stream) {
+    clear_error();
+    (void)arg_lhs;
+    return spmm_backward(g, op, reduce, lhs, rhs, arg_rhs, grad_out, grad_lhs, grad_rhs, stream, -1);
 }
 
 gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
@@ -643,6 +723,22 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
         return fail(GNNK_EINVAL, "grad_lhs must have lhs's shape");
     if (grad_rhs && (grad_rhs->rows != rhs->rows || grad_rhs->heads != rhs->heads || grad_rhs->feat != rhs->feat))
         return fail(GNNK_EINVAL, "grad_rhs must have rhs's shape");
+    if (const int hs = heads_per_slice(Hm, Fm, {lhs, rhs, grad_out, grad_lhs, grad_rhs}, {grad_lhs, grad_rhs})) {
+        // per-head gradients wider than one pass: slices of heads, one call each
+        for (int h0 = 0; h0 < Hm; h0 += hs) {
+            const int hc = std::min(hs, Hm - h0);
+            gnnk_tensor l = use_l ? head_slice(lhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor r = use_r ? head_slice(rhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor go = head_slice(grad_out, Hm, h0, hc);
+            gnnk_tensor gl = grad_lhs ? head_slice(grad_lhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_tensor gr = grad_rhs ? head_slice(grad_rhs, Hm, h0, hc) : gnnk_tensor{};
+            gnnk_status st = gsddmm_backward(g, op, use_l ? &l : nullptr, lhs_target, use_r ? &r : nullptr,
+                                             rhs_target, &go, grad_lhs ? &gl : nullptr, grad_rhs ? &gr : nullptr,
+                                             stream);
+            if (st != GNNK_OK) return st;
+        }
+        return GNNK_OK;
+    }
     const int dt = dtype_code(grad_out);
 
     for (int which = 0; which < 2; ++which) {
@@ -776,7 +872,7 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
     // el and er broadcast over features: keep heads separate (F per head)
     std::vector<Member> ms{{feat, K_FULL}, {el, K_FULL}, {out, K_FULL}};
     Geo geo;
-    gnnk_status st = choose_geo(H, F, ms, {}, geo);
+    gnnk_status st = choose_geo(H, F, ms, {}, geo, true);
     if (st != GNNK_OK) return st;
     if (g->n_dst == 0) return GNNK_OK;
     EngineArgs A{};
@@ -833,10 +929,26 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
         return fail(GNNK_EINVAL, "each gradient must have its operand's shape");
     std::vector<Member> ms{{feat, K_FULL}, {el, K_FULL}, {grad_out, K_FULL}};
     Geo geo;
-    gnnk_status st = choose_geo(H, F, ms, {}, geo);
+    gnnk_status st = choose_geo(H, F, ms, {}, geo, true);
     if (st != GNNK_OK) return st;
-    // a head's dot product is reduced across the lanes of one chunk
-    if (geo.nchunk != 1) return fail(GNNK_EUNSUPPORTED, "fused attention backward needs H * F / vec <= 64");
+    // a head's dot products are reduced across the lanes of one pass: rows
+    // wider than a pass run as slices of heads (heads are independent)
+    if (geo.nchunk != 1) {
+        if (F / geo.vec > 64) return fail(GNNK_EUNSUPPORTED, "fused attention backward needs F / vec <= 64");
+        const int hs = 64 / (F / geo.vec);
+        for (int h0 = 0; h0 < H; h0 += hs) {
+            const int hc = std::min(hs, H - h0);
+            gnnk_tensor f = head_slice(feat, H, h0, hc), l = head_slice(el, H, h0, hc), r = head_slice(er, H, h0, hc);
+            gnnk_tensor sts = head_slice(stats, H, h0, hc), go = head_slice(grad_out, H, h0, hc);
+            gnnk_tensor gf = grad_feat ? head_slice(grad_feat, H, h0, hc) : gnnk_tensor{};
+            gnnk_tensor gl = grad_el ? head_slice(grad_el, H, h0, hc) : gnnk_tensor{};
+            gnnk_tensor gr = grad_er ? head_slice(grad_er, H, h0, hc) : gnnk_tensor{};
+            st = gat_aggregate_backward(g, &f, &l, &r, slope, &sts, &go, grad_feat ? &gf : nullptr,
+                                        grad_el ? &gl : nullptr, grad_er ? &gr : nullptr, stream);
+            if (st != GNNK_OK) return st;
+        }
+        return GNNK_OK;
+    }
     const int dt = dtype_code(grad_out);
     EngineArgs ain{}, aout{};
     ain.a = operand(feat, K_FULL, T_NBR);

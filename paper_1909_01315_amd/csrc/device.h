@@ -449,10 +449,13 @@ __device__ __forceinline__ bool better(float m, int32_t e, float best, int32_t b
 // ---------------------------------------------------------------------------
 // output of one reduced row (sums)
 
+// A reduced output of a row wider than one pass of the wavefront (nchunk > 1,
+// so one lane group of 64 lanes, whole-row sums only) adds each pass's total
+// into *carry (lane 0) and is written after the last pass; ch is the pass.
 template <typename T, int VEC>
 __device__ __forceinline__ void write_sum_row(const EngineArgs& A, int64_t row, bool active, int lig, int col0,
                                               int h, double* acc, int64_t deg, bool write_lane,
-                                              bool may_reduce = true) {
+                                              bool may_reduce = true, int ch = 0, double* carry = nullptr) {
     if (A.flags & F_OWN_MEAN) {
         const double d = deg > 0 ? (double)deg : 1.0;
 #pragma unroll
@@ -474,6 +477,11 @@ __device__ __forceinline__ void write_sum_row(const EngineArgs& A, int64_t row, 
 #pragma unroll
         for (int i = 0; i < VEC; ++i) s += acc[i];
         s = seg_sum(active ? s : 0.0, lig, A.out.red);
+        if (A.geo.nchunk > 1 && carry) {
+            *carry += s;
+            if (ch + 1 < A.geo.nchunk) return;
+            s = *carry;
+        }
         if (active && write_lane && row >= 0 && (lig % A.out.red) == 0) {
             const int64_t o = A.out.per_head ? h : 0;
             IO<T, VEC>::store1(reinterpret_cast<T*>(A.out.data) + row * A.out.stride + o, (float)s);

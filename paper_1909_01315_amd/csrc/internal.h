@@ -145,6 +145,9 @@ struct EngineArgs {
     int64_t out2_stride;
     int32_t red2;            // lanes summed per output value (a power of two)
     int32_t per_head2;       // 1: one value per head, 0: one per edge
+    // g-SDDMM whose per-edge sum over the whole row spans several passes of
+    // the wavefront (nchunk > 1): fp64 running sum per edge between passes
+    double* xacc;
 };
 
 // Operand layouts with kernels specialised at compile time (the host picks
@@ -221,9 +224,10 @@ hipError_t launch_iota(int32_t* out, int64_t n, hipStream_t s);
 // pos[perm[q]] = q for q < n
 hipError_t launch_inverse(const int32_t* perm, int64_t n, int32_t* pos, hipStream_t s);
 // Winner masks of max/min: bits[pos_of_edge[e] * words + c / 32] has bit c % 32
-// set iff arg_e[v * D + c] == e for some row v (zeroed first).
-hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, const int32_t* pos_of_edge,
-                              uint32_t* bits, int64_t n_edges, int32_t words, hipStream_t s);
+// set iff arg_e[v * ld + c] == e for some row v and column c < D (zeroed first).
+hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, int64_t ld,
+                              const int32_t* pos_of_edge, uint32_t* bits, int64_t n_edges, int32_t words,
+                              hipStream_t s);
 hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int64_t n, hipStream_t s);
 
 // ----- device construction of the graph formats (build.hip) -----

@@ -105,8 +105,8 @@ __global__ void zero_words_kernel(uint32_t* w, int64_t n) {
 // edge's one destination row, so no other lane writes it: plain stores, no
 // atomics, and the result does not depend on any ordering.
 __global__ __launch_bounds__(256) void winner_bits_kernel(const int32_t* arg_e, int64_t n_rows, int32_t D,
-                                                          const int32_t* pos_of_edge, uint32_t* bits, int32_t words,
-                                                          int64_t n_edges) {
+                                                          int64_t ld, const int32_t* pos_of_edge, uint32_t* bits,
+                                                          int32_t words, int64_t n_edges) {
     const int lane = __lane_id();
     const int half = lane >> 5, b = lane & 31;
     const int64_t n_units = n_rows * words;
@@ -118,7 +118,7 @@ __global__ __launch_bounds__(256) void winner_bits_kernel(const int32_t* arg_e, 
         const int32_t w = (int32_t)(unit - v * words);
         const int32_t c = w * 32 + b;
         int32_t e = -1;
-        if (unit < n_units && c < D) e = arg_e[v * D + c];
+        if (unit < n_units && c < D) e = arg_e[v * ld + c];
         const bool ok = e >= 0 && e < n_edges;  // empty rows (-1); ids outside the graph are ignored
         const int32_t pos = ok ? pos_of_edge[e] : 0;  // every lane's lookup in flight at once
         uint64_t todo = __ballot(ok);
@@ -227,13 +227,14 @@ hipError_t launch_inverse(const int32_t* perm, int64_t n, int32_t* pos, hipStrea
     return hipGetLastError();
 }
 
-hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, const int32_t* pos_of_edge,
-                              uint32_t* bits, int64_t n_edges, int32_t words, hipStream_t s) {
+hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, int64_t ld,
+                              const int32_t* pos_of_edge, uint32_t* bits, int64_t n_edges, int32_t words,
+                              hipStream_t s) {
     const int64_t nw = n_edges * words, n = n_rows * D;
     if (nw > 0) hipLaunchKernelGGL(zero_words_kernel, dim3(grid_1d(nw)), dim3(256), 0, s, bits, nw);
     if (n > 0)
         hipLaunchKernelGGL(winner_bits_kernel, dim3(grid_1d(n_rows * words * 32)), dim3(256), 0, s, arg_e, n_rows,
-                           D, pos_of_edge, bits, words, n_edges);
+                           D, ld, pos_of_edge, bits, words, n_edges);
     return hipGetLastError();
 }
 

@@ -12,11 +12,14 @@ namespace gnnk {
 
 // Output of one edge: VEC columns (RM = 0), or the sum over runs of
 // out.red lanes (a head for dot, or the whole row): RM = 1 for power-of-two
-// runs (DPP within 16-lane rows), RM = -1 reads the mode at run time.
+// runs (DPP within 16-lane rows), RM = -1 reads the mode at run time.  A
+// whole-row sum of a row wider than one pass (nchunk > 1: one lane group,
+// lane 0 writes every edge) keeps its running fp64 total per edge in xacc
+// between passes ch and writes the output in the last one.
 template <typename T, int VEC, int OPK, int EXT, int RM>
 struct SddmmSink {
     const EngineArgs& A;
-    int lig, col0, h;
+    int lig, col0, h, ch;
     bool active;
     __device__ __forceinline__ void operator()(const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
         double m[VEC];
@@ -40,6 +43,14 @@ struct SddmmSink {
             if constexpr (RM > 0) s = run_sum(s, red);
             else s = (red & (red - 1)) == 0 ? run_sum(s, red) : seg_sum(s, lig, red);
             const bool writer = RM > 0 ? ((lig & (red - 1)) == 0) : ((lig % red) == 0);
+            if (A.geo.nchunk > 1 && (ok & active & writer)) {
+                double* x = A.xacc + (uint32_t)ed;
+                if (ch > 0) s += *x;
+                if (ch + 1 < A.geo.nchunk) {
+                    *x = s;
+                    return;
+                }
+            }
             if (ok & active & writer) {
                 const int o = A.out.per_head ? h : 0;
                 IO<T, VEC>::store1(row + o, (float)(neg ? -s : s));
@@ -62,7 +73,7 @@ __device__ __forceinline__ void sddmm_row(const EngineArgs& A, const Lanes& ln, 
         const int h = col0 / geo.F;
         Pre<VEC> pre;
         if (r >= 0) load_pre<T, VEC, OPK, S>(A, self, col0, h, pre);
-        SddmmSink<T, VEC, OPK, EXT, RM> sink{A, ln.lig, col0, h, active};
+        SddmmSink<T, VEC, OPK, EXT, RM> sink{A, ln.lig, col0, h, ch, active};
         if constexpr (WAVE_ROW) walk_row<T, VEC, OPK, EXT, S>(A, self, b, e, ln.g, G, col0, h, pre, sink);
         else walk_lane<T, VEC, OPK, EXT, S>(A, self, b, e, col0, h, pre, sink);
     }

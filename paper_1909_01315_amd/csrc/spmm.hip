@@ -65,6 +65,7 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
         r = uniform64(r);
         b = uniform64(b);
         e = uniform64(e);
+        double carry = 0.0;
         for (int ch = 0; ch < geo.nchunk; ++ch) {
             const int j = ch * L + ln.lig;
             const bool active = j < geo.NV;
@@ -96,7 +97,7 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
                     for (int i = 0; i < VEC; ++i) P[i] = acc[i];
                 }
             } else {
-                write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, ln.g == 0, !S::FAST);
+                write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, ln.g == 0, !S::FAST, ch, &carry);
             }
         }
     } else if (w < A.sch.w_small_end) {
@@ -109,6 +110,7 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
             e = row_ptr(A.csr, r + 1);
         }
         const int32_t self = r >= 0 ? (int32_t)r : 0;
+        double carry = 0.0;
         for (int ch = 0; ch < geo.nchunk; ++ch) {
             const int j = ch * L + ln.lig;
             const bool active = j < geo.NV;
@@ -132,7 +134,7 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
                 dw.put(A, rw, ed, ok, ln.lig, h, active);
             };
             walk_lane<T, VEC, OPK, EXT, S>(A, self, b, e, col0, h, pre, sink);
-            write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, true, !S::FAST);
+            write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, e - b, true, !S::FAST, ch, &carry);
         }
     } else {
         // empty rows: the empty reduction is 0 (no mean, no negation)
@@ -175,6 +177,7 @@ __global__ __launch_bounds__(256) void spmm_sum_combine_kernel(EngineArgs A) {
     const int s0 = row_ok ? A.csr.hub_off[k] : 0;
     const int s1 = row_ok ? A.csr.hub_off[k + 1] : 0;
     const int64_t deg = row_ok ? row_ptr(A.csr, r + 1) - row_ptr(A.csr, r) : 0;
+    double carry = 0.0;
     for (int ch = 0; ch < geo.nchunk; ++ch) {
         const int j = ch * geo.L + ln.lig;
         const bool active = j < geo.NV && row_ok;
@@ -188,7 +191,7 @@ __global__ __launch_bounds__(256) void spmm_sum_combine_kernel(EngineArgs A) {
 #pragma unroll
             for (int i = 0; i < VEC; ++i) acc[i] += P[i];
         }
-        write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, deg, true);
+        write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, deg, true, true, ch, &carry);
     }
 }
 

@@ -140,6 +140,8 @@ def _desc(t):
     else:
         raise TypeError(f"unsupported dtype {t.dtype}")
     rows, h, f = t.shape
+    if t.numel() == 0:  # no element is addressed: any strides will do
+        return _Tensor(t.data_ptr(), rows, h, f, h * f, dt, 0)
     if (f > 1 and t.stride(2) != 1) or (h > 1 and t.stride(1) != f):
         raise ValueError("the last two dimensions must be contiguous")
     stride = t.stride(0) if rows > 1 else h * f

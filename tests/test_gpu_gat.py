@@ -39,7 +39,9 @@ def oracle_gat(o, feat, el, er, slope):
     return orc.gspmm(o, "mul", "sum", feat, a), a
 
 
-@pytest.mark.parametrize("H,F", [(1, 16), (4, 4), (8, 16), (2, 32), (4, 100)])
+# (8, 1) and (2, 1): el and er have the shape of feat; (4, 2), (2, 3): 2 and 1
+# values per lane
+@pytest.mark.parametrize("H,F", [(1, 16), (4, 4), (8, 16), (2, 32), (4, 100), (8, 1), (2, 1), (4, 2), (2, 3)])
 @pytest.mark.parametrize("want_attn", [False, True])
 def test_gat_aggregate_c1(c1, H, F, want_attn):
     N = c1.o.n_src
@@ -146,7 +148,7 @@ def row_stats(o, el, er, slope):
     return m, l
 
 
-@pytest.mark.parametrize("H,F", [(1, 16), (4, 4), (8, 16), (2, 32)])
+@pytest.mark.parametrize("H,F", [(1, 16), (4, 4), (8, 16), (2, 32), (8, 1), (1, 1), (4, 2), (2, 3)])
 def test_gat_stats_and_backward_c1(c1, H, F):
     N = c1.o.n_src
     feat = synth.normal(S, f"bf{H}{F}", (N, H, F))
@@ -224,19 +226,32 @@ def test_gat_backward_empty_rows_partial_grads_and_bf16():
     assert_close(gr, rr, kind="bf16", name="bf16 d er")
 
 
-def test_gat_backward_wide_rows_unsupported(c1):
-    """H * F / 4 > 64 columns per lane group: the fused backward declines
-    with GNNK_EUNSUPPORTED, as the unfused attention gradient (a reduction
-    over F across the lane group) does."""
+def test_gat_backward_wide_rows(c1):
+    """Rows of H * F / 4 > 64 lanes: the fused backward runs as slices of
+    heads and the unfused attention gradient (a per-head reduction over F)
+    as slices too, both against the oracle; a single head wider than one
+    pass (F / 4 > 64) is declined by the fused backward with
+    GNNK_EUNSUPPORTED."""
     N = c1.o.n_src
     feat = synth.normal(S, "wf", (N, 4, 100))
     el = synth.normal(S, "wl", (N, 4, 1))
     er = synth.normal(S, "wr", (c1.o.n_dst, 4, 1))
+    dz = synth.normal(synth.grad_seed(21), "wdz", (c1.o.n_dst, 4, 100))
     _, st = gnnk.gat_aggregate(c1.g, dev(feat), dev(el), dev(er), 0.2, want_stats=True)
+    gf, gl, gr = gnnk.gat_aggregate_backward(c1.g, dev(feat), dev(el), dev(er), 0.2, st, dev(dz))
+    rf, rl, rr = oracle_gat_backward(c1.o, feat, el, er, 0.2, dz)
+    assert_close(gf, rf, name="d feat")
+    assert_close(gl, rl, name="d el")
+    assert_close(gr, rr, name="d er")
+    a = synth.uniform(S, "wa", (c1.o.n_edges, 4, 1), 0.0, 1.0)
+    dx, da = gnnk.gspmm_backward(c1.g, "mul", "sum", dev(feat), dev(a), dev(dz))
+    ox, oa = orc.gspmm_backward(c1.o, "mul", "sum", feat, a, dz)
+    assert_close(dx, ox, name="unfused d feat")
+    assert_close(da, oa, name="unfused d attention")
+    f1 = synth.normal(S, "wf1", (N, 1, 300))
+    e1 = synth.normal(S, "wl1", (N, 1, 1))
+    r1 = synth.normal(S, "wr1", (c1.o.n_dst, 1, 1))
+    _, st1 = gnnk.gat_aggregate(c1.g, dev(f1), dev(e1), dev(r1), 0.2, want_stats=True)
     with pytest.raises(gnnk.GnnkError) as e:
-        gnnk.gat_aggregate_backward(c1.g, dev(feat), dev(el), dev(er), 0.2, st, dev(feat[: c1.o.n_dst]))
-    assert e.value.status == gnnk.EUNSUPPORTED
-    a = dev(synth.uniform(S, "wa", (c1.o.n_edges, 4, 1), 0.0, 1.0))
-    with pytest.raises(gnnk.GnnkError) as e:
-        gnnk.gspmm_backward(c1.g, "mul", "sum", dev(feat), a, dev(feat[: c1.o.n_dst]))
+        gnnk.gat_aggregate_backward(c1.g, dev(f1), dev(e1), dev(r1), 0.2, st1, dev(f1[: c1.o.n_dst]))
     assert e.value.status == gnnk.EUNSUPPORTED

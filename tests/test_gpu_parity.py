@@ -131,6 +131,67 @@ def test_gspmm_gcn_c2(c2, D):
     assert_close(out, ref, name=f"c2 D={D}")
 
 
+@pytest.fixture(scope="module")
+def hot():
+    """300 nodes, 4,000 edges, a third of them into destination 7 and a
+    quarter out of source 3 (rows of a thousand edges: hub segments)"""
+    rng = np.random.default_rng(44)
+    E = 4000
+    src = rng.integers(0, 300, E).astype(np.int32)
+    dst = rng.integers(0, 300, E).astype(np.int32)
+    dst[rng.random(E) < 0.33] = 7
+    src[rng.random(E) < 0.25] = 3
+    return Pair(src, dst, 300, 300)
+
+
+@pytest.mark.parametrize("H,F", [(1, 512), (1, 300), (2, 256), (8, 40), (3, 129), (4, 100)])
+@pytest.mark.parametrize("seg", [0, 64])
+def test_sums_over_rows_wider_than_a_wavefront(hot, H, F, seg):
+    """Sums over the features of rows wider than one pass of 64 lanes: the
+    u_dot_v score, the edge-weight gradient of u_mul_e/sum with a weight per
+    edge and per head (also for max, through the winner masks), the node
+    gradient of a per-head node operand, and the g-SDDMM backward of a dot;
+    with the automatic segment size and with 64-edge hub segments (fp32 and a
+    bf16 case)."""
+    gnnk.set_option("seg_edges", seg)
+    p = Pair(hot.o.src, hot.o.dst, 300, 300) if seg else hot
+    o, g = p.o, p.g
+    S = synth.feat_seed(40)
+    X = feats(S, f"wX{H}{F}", (o.n_src, H, F))
+    Y = feats(S, f"wY{H}{F}", (o.n_dst, H, F))
+    dM = feats(G1, f"wdM{H}", (o.n_edges, H, 1))
+    M = orc.gsddmm(o, "dot", X, "u", Y, "v")
+    assert_close(gnnk.gsddmm(g, "dot", dev(X), "u", dev(Y), "v"), M, name="dot")
+    gl, gr = orc.gsddmm_backward(o, "dot", X, "u", Y, "v", dM)
+    dl, dr = gnnk.gsddmm_backward(g, "dot", dev(X), "u", dev(Y), "v", dev(dM))
+    assert_close(dl, gl, name="dot grad lhs")
+    assert_close(dr, gr, name="dot grad rhs")
+    dZ = feats(G1, f"wdZ{H}{F}", (o.n_dst, H, F))
+    for wshape in ((H, 1), (1, 1)):
+        W = feats(S, f"wW{wshape}", (o.n_edges,) + wshape, 0.5, 1.5)
+        for red in ("sum", "mean", "max"):
+            ae = None
+            if red == "max":
+                _, _, ae = orc.gspmm(o, "mul", red, X, W)
+            rl, rr = orc.gspmm_backward(o, "mul", red, X, W, dZ, arg_e=ae)
+            ql, qr = gnnk.gspmm_backward(g, "mul", red, dev(X), dev(W), dev(dZ),
+                                         arg_rhs=dev(ae) if ae is not None else None)
+            assert_close(ql, rl, name=f"grad x {wshape} {red}")
+            assert_close(qr, rr, name=f"grad w {wshape} {red}")
+    # a per-head node operand times a full edge operand: its gradient sums
+    # each head's F columns on the reverse graph
+    Ln = feats(S, f"wL{H}", (o.n_src, H, 1))
+    We = feats(S, f"wWe{H}{F}", (o.n_edges, H, F), 0.5, 1.5)
+    rl, rr = orc.gspmm_backward(o, "div", "sum", Ln, We, dZ)
+    ql, qr = gnnk.gspmm_backward(g, "div", "sum", dev(Ln), dev(We), dev(dZ))
+    assert_close(ql, rl, name="grad per-head node operand")
+    assert_close(qr, rr, name="grad full edge operand")
+    if H == 2 and seg == 0:
+        Xb, Yb = synth.to_bf16_bits(X), synth.to_bf16_bits(Y)
+        assert_close(gnnk.gsddmm(g, "dot", dev(Xb), "u", dev(Yb), "v"), orc.gsddmm(o, "dot", Xb, "u", Yb, "v"),
+                     kind="bf16", name="bf16 dot")
+
+
 @pytest.mark.parametrize("op,reduce", [("copy_lhs", "max"), ("copy_lhs", "min"), ("mul", "max"), ("add", "min"),
                                        ("sub", "max"), ("div", "min"), ("copy_rhs", "max")])
 @pytest.mark.parametrize("wshape", [(1, 1), (1, 16)])
