@@ -4,19 +4,23 @@ are still covered.  Each case draws
 
   - a graph: 1-200 sources and destinations, 0-3000 edges, sometimes a hot
     source and a hot destination (hub rows), sometimes sorted by destination
-    (identity edge ids), int32 or int64 offsets;
+    (identity edge ids), int32 or int64 offsets, built from the edge list or
+    from the in-CSR (with or without explicit edge ids);
   - library options: hub segment size, small-row threshold, schedule
-    (row engine, edge-parallel ordered, edge-parallel with atomics) and the
-    runtime-layout kernels;
-  - shapes: H in {1, 2, 4, 8}, F from 1 to 40, each operand full (H, F),
-    per head (H, 1) or one value (1, 1); fp32 or bf16; node tables with a
-    padded row stride;
+    (row engine, edge-parallel ordered, edge-parallel with atomics), the
+    edge-parallel chunk and the runtime-layout kernels;
+  - shapes: H in {1, 2, 4, 8}, F from 1 to 40 (now and then a row wider than
+    one pass of the wavefront: F of 100-300), each operand full (H, F), per
+    head (H, 1) or one value (1, 1); fp32 or bf16; node tables with a padded
+    row stride;
+  - the stream: the current one or a second stream;
 
 then runs g-SpMM (op and reducer drawn), its backward, g-SDDMM (op and
-targets drawn), its backward, edge softmax and its backward, and the fused
-attention layer with its backward.  Tolerances are those of tests/_gpu.py;
+targets drawn), its backward, edge softmax and its backward, leaky ReLU and
+its backward, and the fused attention layer with its backward.  Tolerances are those of tests/_gpu.py;
 max/min values and their arg edges compare bit for bit.  The case number,
 seed and draws are printed before the GPU work of a case."""
+import contextlib
 import sys
 
 import numpy as np
@@ -38,7 +42,8 @@ TARGETS = ["u", "e", "v"]
 @pytest.fixture(autouse=True)
 def reset_options():
     yield
-    for k, v in (("seg_edges", 0), ("small_deg", -1), ("schedule", 0), ("no_fast", 0), ("no_split", 0)):
+    for k, v in (("seg_edges", 0), ("small_deg", -1), ("schedule", 0), ("no_fast", 0), ("no_split", 0),
+                 ("edge_chunk", 0)):
         gnnk.set_option(k, v)
 
 
@@ -59,7 +64,22 @@ def draw_graph(rng):
 
 def draw_options(rng):
     return {"seg_edges": int(rng.choice([0, 32, 64, 256])), "small_deg": int(rng.choice([-1, -1, 0, 4, 64])),
-            "schedule": int(rng.choice([0, 0, 0, 2, 3])), "no_fast": int(rng.choice([0, 0, 0, 1]))}
+            "schedule": int(rng.choice([0, 0, 0, 2, 3])), "no_fast": int(rng.choice([0, 0, 0, 1])),
+            "edge_chunk": int(rng.choice([0, 0, 8, 36]))}
+
+
+class CsrPair:
+    """The graph built from the oracle's in-CSR (graph_create_csr), with the
+    edge ids of its positions or, when they are the identity, none."""
+
+    def __init__(self, src, dst, n_src, n_dst, ptr64, with_eids):
+        self.o = orc.OGraph(src, dst, n_src, n_dst)
+        ip, ii, ie = orc.csr(self.o)
+        ident = np.array_equal(ie, np.arange(len(ie), dtype=ie.dtype))
+        eids = None if (ident and not with_eids) else dev(ie.astype(np.int32))
+        self.g = gnnk.Graph.from_csr(dev(ip.astype(np.int64 if ptr64 else np.int32)), dev(ii.astype(np.int32)),
+                                     eids, n_src)
+        torch.cuda.synchronize()
 
 
 def kind_shape(rng, H, F):
@@ -87,13 +107,57 @@ def check(kind, gpu, ref, name):
     assert_close(gpu, ref, kind=kind, name=name)
 
 
+def gat_grad_bounds(o, feat, el, er, dz, slope):
+    """Error bounds of the attention gradients from the magnitudes of the
+    terms they sum.  Both sides round the attention a to fp32 (the oracle
+    between its steps, the fused kernel from exp2 and 1/l), so the sum of a
+    row's attention is 1 only to within fp32 rounding, and d_er = P - S Q
+    (exactly 0 when the slope is the same over the row) keeps |S| times that
+    error.  A sum of terms t_e computed from fp32-rounded factors is within a
+    small multiple of 2^-24 sum |t_e| of the exact one: 2^-20 sum |t_e| is
+    used (16 units of fp32 rounding), per output, on top of the usual
+    tolerance."""
+    s = (el[o.src, :, 0].astype(np.float64) + er[o.dst, :, 0].astype(np.float64))
+    lk = np.where(s > 0, 1.0, slope)
+    a = orc.edge_softmax(o, orc.leaky_relu(orc.gsddmm(o, "add", el, "u", er, "v"), slope))[:, :, 0]
+    a = a.astype(np.float64)
+    dabs = np.einsum("ehf,ehf->eh", np.abs(feat[o.src]).astype(np.float64), np.abs(dz[o.dst]).astype(np.float64))
+    s_abs = np.zeros((o.n_dst, feat.shape[1]))
+    np.add.at(s_abs, o.dst, a * dabs)
+    t = a * (dabs + s_abs[o.dst]) * lk
+    b_er = np.zeros((o.n_dst, feat.shape[1]))
+    np.add.at(b_er, o.dst, t)
+    b_el = np.zeros((o.n_src, feat.shape[1]))
+    np.add.at(b_el, o.src, t)
+    b_feat = np.zeros(feat.shape)
+    np.add.at(b_feat, o.src, a[:, :, None] * np.abs(dz[o.dst]))
+    u = 2.0 ** -20
+    return u * b_feat, u * b_el[:, :, None], u * b_er[:, :, None]
+
+
+def check_bound(gpu, ref, bound, name):
+    """|gpu - ref| <= max(1e-6 + 1e-5 |ref|, bound) per element"""
+    g = host(gpu).astype(np.float64).reshape(ref.shape)
+    r = np.asarray(ref, np.float64)
+    tol = np.maximum(1e-6 + 1e-5 * np.abs(r), bound)
+    bad = ~(np.abs(g - r) <= tol)
+    assert not bad.any(), f"{name}: {int(bad.sum())} of {bad.size} out of bound; first at " \
+                          f"{np.argwhere(bad)[0]}: gpu {g[bad][0]} ref {r[bad][0]} tol {tol[bad][0]}"
+
+
 @pytest.mark.parametrize("case", range(N_CASES))
 def test_random_case(case):
     rng = np.random.default_rng(90_000 + case)
     src, dst, n_src, n_dst, ptr64 = draw_graph(rng)
     opts = draw_options(rng)
-    H = int(rng.choice([1, 2, 4, 8]))
-    F = int(rng.choice([1, 2, 3, 4, 5, 8, 13, 16, 32, 40]))
+    build = ["coo", "coo", "csr", "csr_eids"][int(rng.integers(4))]
+    side = bool(rng.random() < 0.3)
+    if rng.random() < 0.1:
+        H = int(rng.choice([1, 2, 3]))
+        F = int(rng.choice([100, 129, 300]))
+    else:
+        H = int(rng.choice([1, 2, 4, 8]))
+        F = int(rng.choice([1, 2, 3, 4, 5, 8, 13, 16, 32, 40]))
     bf16 = bool(rng.random() < 0.2)
     kind = "bf16" if bf16 else "f32"
     pad = int(rng.choice([0, 0, 1, 4]))
@@ -101,12 +165,24 @@ def test_random_case(case):
     red = ["sum", "mean", "max", "min"][int(rng.integers(4))]
     lt, rt = (TARGETS[int(i)] for i in rng.integers(0, 3, 2))
     sop = (OPS + ["dot"])[int(rng.integers(len(OPS) + 1))]
-    print(f"case {case}: n_src {n_src} n_dst {n_dst} E {len(src)} ptr64 {ptr64} {opts} H {H} F {F} {kind} "
-          f"pad {pad} gspmm {op}/{red} gsddmm {sop} {lt},{rt}", flush=True)
+    print(f"case {case}: n_src {n_src} n_dst {n_dst} E {len(src)} ptr64 {ptr64} {build} side stream {side} "
+          f"{opts} H {H} F {F} {kind} pad {pad} gspmm {op}/{red} gsddmm {sop} {lt},{rt}", flush=True)
     sys.stdout.flush()
     for k, v in opts.items():
         gnnk.set_option(k, v)
-    p = Pair(src, dst, n_src, n_dst, ptr64=ptr64)
+    stream = torch.cuda.Stream() if side else None
+    if stream is not None:
+        stream.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(stream) if stream is not None else contextlib.nullcontext():
+        run_case(rng, src, dst, n_src, n_dst, ptr64, build, opts, H, F, bf16, kind, pad, op, red, lt, rt, sop)
+    torch.cuda.synchronize()
+
+
+def run_case(rng, src, dst, n_src, n_dst, ptr64, build, opts, H, F, bf16, kind, pad, op, red, lt, rt, sop):
+    if build == "coo":
+        p = Pair(src, dst, n_src, n_dst, ptr64=ptr64)
+    else:
+        p = CsrPair(src, dst, n_src, n_dst, ptr64, build == "csr_eids")
     E = p.o.n_edges
     rows = {"u": n_src, "e": E, "v": n_dst}
 
@@ -136,7 +212,10 @@ def test_random_case(case):
 
     # g-SDDMM forward and backward
     if sop == "dot":
-        ls2 = rs2 = (H, F)
+        # a dot of a full operand with a full, per-head or single value
+        ls2, rs2 = (H, F), kind_shape(rng, H, F)
+        if rng.random() < 0.5:
+            ls2, rs2 = rs2, ls2
     else:
         ls2 = kind_shape(rng, H, F) if sop != "copy_rhs" else None
         rs2 = kind_shape(rng, H, F) if sop != "copy_lhs" else None
@@ -161,10 +240,18 @@ def test_random_case(case):
     check(kind, gnnk.edge_softmax_backward(p.g, dev(a), gd), orc.edge_softmax_backward(p.o, a, g_),
           "edge softmax backward")
 
-    # fused attention layer (fp32; a row of feat must fit one wavefront of
+    # leaky ReLU on an edge tensor (one fp32 operation: bit for bit), with a
+    # padded row stride sometimes
+    x, xd = table(rng, E, (H, F), bf16, pad=pad)
+    dy, dyd = table(rng, E, (H, F), bf16)
+    assert_exact(gnnk.edge_leaky_relu(xd, 0.2), orc.leaky_relu(x, 0.2), "leaky relu")
+    assert_exact(gnnk.edge_leaky_relu_backward(xd, dyd, 0.2), orc.leaky_relu_backward(x, dy, 0.2),
+                 "leaky relu backward")
+
+    # fused attention layer (fp32; a head of feat must fit one wavefront of
     # vectors: 4, 2 or 1 floats per lane as F and the row stride allow)
     vec = next(v for v in (4, 2, 1) if F % v == 0 and (pad == 0 or n_src < 2 or (H * F + pad) % v == 0))
-    if not bf16 and H * F // vec <= 64 and opts["schedule"] == 0:
+    if not bf16 and F // vec <= 64 and opts["schedule"] == 0:
         feat, featd = table(rng, n_src, (H, F), False, pad=pad)
         el, eld = table(rng, n_src, (H, 1), False)
         er, erd = table(rng, n_dst, (H, 1), False)
@@ -175,8 +262,8 @@ def test_random_case(case):
         dz, dzd = table(rng, n_dst, (H, F), False)
         rf, rl, rr = oracle_gat_backward(p.o, feat, el, er, 0.2, dz)
         gf, gl_, gr_ = gnnk.gat_aggregate_backward(p.g, featd, eld, erd, 0.2, st, dzd)
-        check(kind, gf, rf, "gat d feat")
-        check(kind, gl_, rl, "gat d el")
-        check(kind, gr_, rr, "gat d er")
-    torch.cuda.synchronize()
+        bf, bl, br = gat_grad_bounds(p.o, feat, el, er, dz, 0.2)
+        check_bound(gf, rf, bf, "gat d feat")
+        check_bound(gl_, rl, bl, "gat d el")
+        check_bound(gr_, rr, br, "gat d er")
     p.g.destroy()
