@@ -261,8 +261,9 @@ Pick pick_sddmm(const gnnk_graph* g, const EngineArgs& A, const Geo& geo, int dt
     Pick p;
     if (options().no_fast || !fast_geo(geo, dtype) || ext_of(A.flags) != EXT_NONE || opk == 0) return p;
     if (!A.a.full || !A.b.full) return p;
-    // reduced outputs need power-of-two runs of lanes (DPP sums)
-    if (A.out.reduce && (A.out.red & (A.out.red - 1)) != 0) return p;
+    // reduced outputs need power-of-two runs of lanes (DPP sums) within one
+    // pass of the wavefront
+    if (A.out.reduce && ((A.out.red & (A.out.red - 1)) != 0 || geo.nchunk > 1)) return p;
     const int es = dtype == 1 ? 2 : 4;
     if (A.a.target == T_NBR && A.b.target == T_SELF && fits32(A.a, g->n_src, es) && fits32(A.b, g->n_dst, es) &&
         (opk == 1 || A.op != M_NEGDIV2)) {

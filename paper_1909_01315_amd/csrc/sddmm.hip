@@ -43,7 +43,8 @@ struct SddmmSink {
             if constexpr (RM > 0) s = run_sum(s, red);
             else s = (red & (red - 1)) == 0 ? run_sum(s, red) : seg_sum(s, lig, red);
             const bool writer = RM > 0 ? ((lig & (red - 1)) == 0) : ((lig % red) == 0);
-            if (A.geo.nchunk > 1 && (ok & active & writer)) {
+            // (runtime-layout kernels only: the host picks them for such rows)
+            if (RM < 0 && A.geo.nchunk > 1 && (ok & active & writer)) {
                 double* x = A.xacc + (uint32_t)ed;
                 if (ch > 0) s += *x;
                 if (ch + 1 < A.geo.nchunk) {
