@@ -88,7 +88,10 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
                 for (int i = 0; i < VEC; ++i) acc[i] += ok ? m[i] : 0.0;
                 dw.put(A, rw, ed, ok, ln.lig, h, active);
             };
-            walk_row<T, VEC, OPK, EXT, S>(A, (int32_t)r, b, e, ln.g, G, col0, h, pre, sink);
+            if constexpr (EXT == EXT_BITS)
+                walk_winners<T, VEC, OPK, S>(A, (int32_t)r, b, e, ln.g, G, col0, h, pre, sink);
+            else
+                walk_row<T, VEC, OPK, EXT, S>(A, (int32_t)r, b, e, ln.g, G, col0, h, pre, sink);
             sum_groups<S::GC, VEC>(geo, acc);
             if (slot >= 0) {
                 if (ln.g == 0 && active) {

@@ -247,6 +247,61 @@ __device__ __forceinline__ void walk_row(const EngineArgs& A, int32_t self, int6
     }
 }
 
+// Winner-mask walk (the max/min backward, EXT_BITS): the wavefront reads the
+// masks of 64 positions of [b, e) at once (lane i: every word of position
+// p0 + i), keeps the positions where any column won, packs them in
+// ascending order into the low lanes (ds_permute of a stable partition),
+// and hands only those to the lane groups: slot u of group g is kept
+// position k + g + G * u.  On a graph whose rows are much longer than D,
+// most positions win no column, and this skips them at 64 per mask load.
+// b and e must be wave-uniform; every lane must take part.
+template <typename T, int VEC, int OPK, class S, class F>
+__device__ __forceinline__ void walk_winners(const EngineArgs& A, int32_t self, int64_t b64, int64_t e64, int g,
+                                             int G, int col0, int h, const Pre<VEC>& pre, F& consume) {
+    using SN = Spec<S::AT, S::AK, S::BT, S::BK, S::GC, false>;
+    const int32_t b = (int32_t)b64, e = (int32_t)e64;
+    const uint32_t* M = reinterpret_cast<const uint32_t*>(A.mask_arg);
+    const uint32_t words = (uint32_t)A.mask_ld;
+    const int lane = __lane_id();
+    for (int32_t p0 = b; p0 < e; p0 += WAVE) {
+        const int32_t p = p0 + lane;
+        uint32_t any = 0u;
+        if (p < e) {
+            const uint32_t* w = M + (uint64_t)(uint32_t)p * words;
+            for (uint32_t j = 0; j < words; ++j) any |= w[j];
+        }
+        const uint64_t m = __ballot(any != 0u);
+        if (m == 0ull) continue;
+        const int n = __popcll(m);
+        // kept lanes below this one; kept positions go to lanes 0..n-1 in
+        // order, the others after them (a permutation of the 64 lanes)
+        const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        const int dst = any != 0u ? below : n + (lane - below);
+        const int32_t cpos = __builtin_amdgcn_ds_permute(dst << 2, p);
+        for (int k = 0; k < n; k += G * UNR) {
+            int32_t nb[UNR], ed[UNR], ps[UNR];
+            bool ok[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) {
+                const int q = k + g + G * u;
+                ok[u] = q < n;
+                const int32_t pq = __shfl(cpos, ok[u] ? q : 0, WAVE);
+                ps[u] = ok[u] ? pq : b;
+                nb[u] = A.csr.idx[ps[u]];
+                ed[u] = A.csr.eid ? A.csr.eid[ps[u]] : ps[u];
+            }
+            Raw<VEC> r[UNR];
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) fetch_bits<VEC, EXT_BITS>(A, ps[u], col0, r[u]);
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) fetch<T, VEC, OPK, EXT_BITS, SN>(A, nb[u], ed[u], self, col0, h, pre, r[u]);
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) consume(r[u], ed[u], nb[u], ok[u]);
+        }
+    }
+}
+
 // One lane group walks its own row [b, e) (b == e for no row).
 template <typename T, int VEC, int OPK, int EXT, class S, class F>
 __device__ __forceinline__ void walk_lane(const EngineArgs& A, int32_t self, int64_t b, int64_t e, int col0, int h,
