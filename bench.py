@@ -20,7 +20,9 @@ The metric is edge-feature throughput: the sum over the step's g-SpMM /
 g-SDDMM / edge-softmax passes of E x (feature columns of that pass's message),
 divided by the step time.  The roofline object reports the gspmm u_mul_e/sum
 call (the dominant kernel) against the HBM peak, from HIP events recorded on
-the stream it runs on; the u_dot_v call is reported beside it.
+the stream it runs on; the u_dot_v call is reported beside it.  Both also
+report their fraction of the bandwidth a plain 1 GiB device copy reaches on
+the same box (the "stream" object: bytes read + written over time).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -226,13 +228,29 @@ def main():
     for (name, _, _), t in zip(ops, per_op):
         log(f"  {name:48s} {t:9.3f} ms")
 
-    # a plain 1 GiB device copy after the timed region: rocprofv3 counter runs
-    # scale FETCH_SIZE / WRITE_SIZE by what this copy of known size reads
+    # plain 1 GiB device copies after the timed region: rocprofv3 counter
+    # runs scale FETCH_SIZE / WRITE_SIZE by what a copy of known size reads,
+    # and their median time gives the bandwidth this machine reaches on a stream
+    # (STREAM's copy: bytes read + bytes written)
     cal_src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
     cal_dst = torch.empty_like(cal_src)
-    cal_dst.copy_(cal_src)
+    cal_bytes = cal_src.numel() * 4
+
+    def timed(fn):
+        ts = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) / 1e3)
+        return float(np.median(ts))
+
+    copy_gbs = 2 * cal_bytes / timed(lambda: cal_dst.copy_(cal_src)) / 1e9
     torch.cuda.synchronize()
     del cal_src, cal_dst
+    log(f"stream bandwidth on this box: copy {copy_gbs:.0f} GB/s (read + write)")
 
     i_spmm = [n for n, _, _ in ops].index("gspmm u_mul_e/sum")
     i_dot = [n for n, _, _ in ops].index("gsddmm u_dot_v")
@@ -283,6 +301,7 @@ def main():
             "kernel": "gspmm u_mul_e/sum, X (N,8,16) x attention (E,8,1): spmm_sum_kernel + hub-row combine",
             "bytes_alg": b_spmm,
             "ms": per_op[i_spmm],
+            "frac_of_stream_copy": ach / copy_gbs,
         },
         "roofline_sddmm": {
             "bound": "hbm",
@@ -293,7 +312,10 @@ def main():
             "kernel": "gsddmm u_dot_v (N,8,16).(N,8,16) -> (E,8,1): sddmm_kernel",
             "bytes_alg": b_dot,
             "ms": per_op[i_dot],
+            "frac_of_stream_copy": ach_dot / copy_gbs,
         },
+        "stream": {"copy_gbs": copy_gbs, "bytes": cal_bytes,
+                   "what": "median of 5 device copies of 1 GiB, bytes read + written over time"},
         "ops_ms": {name: round(float(t), 4) for (name, _, _), t in zip(ops, per_op)},
         "cpu_baseline": cpu,
     }
