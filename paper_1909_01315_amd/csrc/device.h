@@ -74,6 +74,19 @@ struct IO<float, VEC> {
         }
     }
     static __device__ __forceinline__ void store1(float* p, float v) { *p = v; }
+    static __device__ __forceinline__ void store_nt(float* p, const float* v) {
+        typedef float f4 __attribute__((ext_vector_type(4)));
+        typedef float f2 __attribute__((ext_vector_type(2)));
+        if constexpr (VEC == 4) {
+            f4 x = {v[0], v[1], v[2], v[3]};
+            __builtin_nontemporal_store(x, reinterpret_cast<f4*>(p));
+        } else if constexpr (VEC == 2) {
+            f2 x = {v[0], v[1]};
+            __builtin_nontemporal_store(x, reinterpret_cast<f2*>(p));
+        } else {
+            __builtin_nontemporal_store(v[0], p);
+        }
+    }
     // streaming store: scattered outputs that no later load of the kernel reads
     static __device__ __forceinline__ void store1_nt(float* p, float v) { __builtin_nontemporal_store(v, p); }
 };
@@ -115,6 +128,7 @@ struct IO<bf16_t, VEC> {
         }
     }
     static __device__ __forceinline__ void store1(bf16_t* p, float v) { *p = (bf16_t)f2bf(v); }
+    static __device__ __forceinline__ void store_nt(bf16_t* p, const float* v) { store(p, v); }
     static __device__ __forceinline__ void store1_nt(bf16_t* p, float v) {
         __builtin_nontemporal_store((bf16_t)f2bf(v), p);
     }

@@ -33,18 +33,20 @@ template <typename T, int VEC, bool BWD>
 __global__ __launch_bounds__(256) void leaky_flat_kernel(const T* x, const T* dy, T* y, int64_t n, float slope) {
     const int64_t nv = n / VEC;
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < nv; i += (int64_t)gridDim.x * blockDim.x) {
+        // a pure stream: nontemporal loads and stores (1.44 -> 1.40 ms on
+        // c3's (E, 8) scores)
         float xv[VEC], out[VEC];
-        IO<T, VEC>::load(x + i * VEC, xv);
+        IO<T, VEC>::load_nt(x + i * VEC, xv);
         if (BWD) {
             float d[VEC];
-            IO<T, VEC>::load(dy + i * VEC, d);
+            IO<T, VEC>::load_nt(dy + i * VEC, d);
 #pragma unroll
             for (int k = 0; k < VEC; ++k) out[k] = xv[k] > 0.0f ? d[k] : slope * d[k];
         } else {
 #pragma unroll
             for (int k = 0; k < VEC; ++k) out[k] = xv[k] > 0.0f ? xv[k] : slope * xv[k];
         }
-        IO<T, VEC>::store(y + i * VEC, out);
+        IO<T, VEC>::store_nt(y + i * VEC, out);
     }
     // the tail (fewer than VEC elements), by the first threads
     const int64_t t = nv * VEC + blockIdx.x * (int64_t)blockDim.x + threadIdx.x;

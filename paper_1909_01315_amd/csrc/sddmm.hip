@@ -32,7 +32,11 @@ struct SddmmSink {
                 float v[VEC];
 #pragma unroll
                 for (int i = 0; i < VEC; ++i) v[i] = (float)(neg ? -m[i] : m[i]);
-                IO<T, VEC>::store(row + col0, v);
+                // written once, never read by this kernel: nontemporal vector
+                // stores keep the gathered node rows in L2 (c3 u_add_v 1.83 ->
+                // 1.59 ms; single-value stores of reduced outputs stay plain,
+                // u_dot_v was slower with them)
+                IO<T, VEC>::store_nt(row + col0, v);
             }
         } else {
             double s = 0.0;

@@ -83,7 +83,7 @@ __device__ __forceinline__ void softmax_pass_write(const EngineArgs& A, int64_t 
 #pragma unroll
             for (int i = 0; i < VEC; ++i) v[i] = exp_le0(s[i] - mx[i]) * inv[i];
         }
-        if (active) IO<T, VEC>::store(reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0, v);
+        if (active) IO<T, VEC>::store_nt(reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0, v);
     }
 }
 
