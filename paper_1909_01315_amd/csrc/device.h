@@ -151,15 +151,21 @@ __device__ __forceinline__ void load_i32(const int32_t* p, int32_t* v) {
 }
 
 template <int VEC>
+// nontemporal: the arg arrays of max/min are written once per call
 __device__ __forceinline__ void store_i32(int32_t* p, const int32_t* v) {
+    typedef int i4 __attribute__((ext_vector_type(4)));
+    typedef int i2 __attribute__((ext_vector_type(2)));
     if constexpr (VEC >= 4 && VEC % 4 == 0) {
 #pragma unroll
-        for (int q = 0; q < VEC / 4; ++q)
-            reinterpret_cast<int4*>(p)[q] = make_int4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+        for (int q = 0; q < VEC / 4; ++q) {
+            i4 x = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
+            __builtin_nontemporal_store(x, reinterpret_cast<i4*>(p) + q);
+        }
     } else if constexpr (VEC == 2) {
-        *reinterpret_cast<int2*>(p) = make_int2(v[0], v[1]);
+        i2 x = {v[0], v[1]};
+        __builtin_nontemporal_store(x, reinterpret_cast<i2*>(p));
     } else {
-        *p = v[0];
+        __builtin_nontemporal_store(v[0], p);
     }
 }
 
