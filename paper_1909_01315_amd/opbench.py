@@ -24,6 +24,7 @@ first), the achievable stream bandwidth.  Gathered tables that fit the
 edge.feat/s = E x (message columns) / time.
 
 Usage: python -m paper_1909_01315_amd.opbench [--configs c2,c3,c4,c5] [--out FILE.md]
+       [--warm W] [--reps K] [--mark]
 Every graph and input is seeded and synthetic.  Needs a GPU and the built
 library.
 """
@@ -44,6 +45,7 @@ PEAK_GBS = 8000.0
 def _time(fn, warm: int = 3, reps: int = 20):
     for _ in range(warm):
         fn()
+    torch.cuda.synchronize()
     st = torch.cuda.current_stream()
     ts = []
     for _ in range(reps):
@@ -61,11 +63,24 @@ def _log(msg):
 
 
 class Rows:
-    def __init__(self):
+    """warm, reps: untimed and timed calls per operator.  mark: before and
+    after each operator, a one-element int32 fill on the device, so that a
+    hardware counter run (rocprofv3 --pmc, one call per operator) can tell
+    which dispatches belong to which operator."""
+
+    def __init__(self, warm: int = 3, reps: int = 20, mark: bool = False):
         self.rows = []
+        self.warm, self.reps = warm, reps
+        self.mark = torch.zeros(1, dtype=torch.int32, device="cuda") if mark else None
 
     def add(self, cfg, op, dtype, direction, b_alg, feat_cols, E, fn):
-        med, mn = _time(fn)
+        if self.mark is not None:
+            self.mark.fill_(len(self.rows) + 1)
+            torch.cuda.synchronize()
+        med, mn = _time(fn, self.warm, self.reps)
+        if self.mark is not None:
+            self.mark.fill_(-len(self.rows) - 1)
+            torch.cuda.synchronize()
         gbs = b_alg / med / 1e6
         self.rows.append(dict(config=cfg, op=op, dtype=dtype, dir=direction, b_alg=b_alg, ms=med, ms_min=mn,
                               gbs=gbs, frac=gbs / PEAK_GBS, ef=E * feat_cols / (med * 1e-3) if feat_cols else None))
@@ -258,12 +273,16 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--configs", default="c2,c3,c4,c5")
     ap.add_argument("--out", default=None)
+    ap.add_argument("--warm", type=int, default=3, help="untimed calls per operator")
+    ap.add_argument("--reps", type=int, default=20, help="timed calls per operator")
+    ap.add_argument("--mark", action="store_true",
+                    help="a one-element int32 fill before each operator (for counter runs)")
     args = ap.parse_args()
     gnnk.load()
     assert torch.cuda.is_available(), "the operator benchmark needs a GPU"
     copy_gbs = copy_bandwidth()
     _log(f"plain device copy: {copy_gbs:.0f} GB/s")
-    R = Rows()
+    R = Rows(args.warm, args.reps, args.mark)
     for name in args.configs.split(","):
         CONFIGS[name](R)
         torch.cuda.empty_cache()
