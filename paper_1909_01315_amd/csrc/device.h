@@ -74,17 +74,16 @@ struct IO<float, VEC> {
         }
     }
     static __device__ __forceinline__ void store1(float* p, float v) { *p = v; }
+    // nontemporal only for 16-byte vectors: narrower nontemporal stores are
+    // partial-line writes that L2 does not merge (a g-SDDMM with one value
+    // per edge ran twice as long with them); those stay plain
     static __device__ __forceinline__ void store_nt(float* p, const float* v) {
         typedef float f4 __attribute__((ext_vector_type(4)));
-        typedef float f2 __attribute__((ext_vector_type(2)));
         if constexpr (VEC == 4) {
             f4 x = {v[0], v[1], v[2], v[3]};
             __builtin_nontemporal_store(x, reinterpret_cast<f4*>(p));
-        } else if constexpr (VEC == 2) {
-            f2 x = {v[0], v[1]};
-            __builtin_nontemporal_store(x, reinterpret_cast<f2*>(p));
         } else {
-            __builtin_nontemporal_store(v[0], p);
+            store(p, v);
         }
     }
     // streaming store: scattered outputs that no later load of the kernel reads
@@ -128,7 +127,16 @@ struct IO<bf16_t, VEC> {
         }
     }
     static __device__ __forceinline__ void store1(bf16_t* p, float v) { *p = (bf16_t)f2bf(v); }
-    static __device__ __forceinline__ void store_nt(bf16_t* p, const float* v) { store(p, v); }
+    static __device__ __forceinline__ void store_nt(bf16_t* p, const float* v) {
+        typedef unsigned u4 __attribute__((ext_vector_type(4)));
+        if constexpr (VEC == 8) {
+            u4 x = {f2bf(v[0]) | (f2bf(v[1]) << 16), f2bf(v[2]) | (f2bf(v[3]) << 16), f2bf(v[4]) | (f2bf(v[5]) << 16),
+                    f2bf(v[6]) | (f2bf(v[7]) << 16)};
+            __builtin_nontemporal_store(x, reinterpret_cast<u4*>(p));
+        } else {
+            store(p, v);
+        }
+    }
     static __device__ __forceinline__ void store1_nt(bf16_t* p, float v) {
         __builtin_nontemporal_store((bf16_t)f2bf(v), p);
     }
@@ -150,22 +158,25 @@ __device__ __forceinline__ void load_i32(const int32_t* p, int32_t* v) {
     }
 }
 
-template <int VEC>
-// nontemporal: the arg arrays of max/min are written once per call
+// the arg arrays of max/min are written once per call: nontemporal 16-byte
+// vectors when NT (narrower ones stay plain, as in IO::store_nt)
+template <int VEC, bool NT = true>
 __device__ __forceinline__ void store_i32(int32_t* p, const int32_t* v) {
     typedef int i4 __attribute__((ext_vector_type(4)));
-    typedef int i2 __attribute__((ext_vector_type(2)));
-    if constexpr (VEC >= 4 && VEC % 4 == 0) {
+    if constexpr (NT && VEC >= 4 && VEC % 4 == 0) {
 #pragma unroll
         for (int q = 0; q < VEC / 4; ++q) {
             i4 x = {v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]};
             __builtin_nontemporal_store(x, reinterpret_cast<i4*>(p) + q);
         }
+    } else if constexpr (VEC >= 4 && VEC % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q)
+            reinterpret_cast<int4*>(p)[q] = make_int4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
     } else if constexpr (VEC == 2) {
-        i2 x = {v[0], v[1]};
-        __builtin_nontemporal_store(x, reinterpret_cast<i2*>(p));
+        *reinterpret_cast<int2*>(p) = make_int2(v[0], v[1]);
     } else {
-        __builtin_nontemporal_store(v[0], p);
+        *p = v[0];
     }
 }
 
@@ -262,7 +273,7 @@ __device__ __forceinline__ int32_t row_of(int32_t target, int32_t nb, int32_t ed
 
 template <typename T, int VEC, int TGT, int KIND, bool FAST>
 __device__ __forceinline__ void ld_opd(const OperandDev& o, int32_t nb, int32_t ed, int32_t self, int col0, int h,
-                                       float* v) {
+                                       float* v, bool random_edges = false) {
     const int32_t row = row_of(TGT == DYN ? o.target : TGT, nb, ed, self);
     if constexpr (FAST && TGT != DYN && TGT != T_EDGE && KIND != DYN) {
         const uint32_t rb = (uint32_t)o.stride * (uint32_t)sizeof(T);
@@ -279,11 +290,13 @@ __device__ __forceinline__ void ld_opd(const OperandDev& o, int32_t nb, int32_t 
     } else {
         const T* base = reinterpret_cast<const T*>(o.data) + (uint64_t)(uint32_t)row * (uint32_t)o.stride;
         const bool full = KIND == DYN ? (o.full != 0) : KIND == OK_FULL;
-        // edge operands are read once per call: nontemporal loads (on the
-        // reverse graph, where they arrive through the edge-id map in random
-        // order, c3's u_add_v backward ran 3.30 -> 3.09 ms and the dX pass of
-        // u_mul_e/sum 7.57 -> 7.20 ms; forward walks were unchanged)
-        const bool nt = TGT == DYN ? o.target == T_EDGE : TGT == T_EDGE;
+        // edge operands read through explicit edge ids (the reverse graph)
+        // arrive in random order, one line per record: nontemporal loads
+        // (c3's u_add_v backward 3.30 -> 3.09 ms, the dX pass of u_mul_e/sum
+        // 7.57 -> 7.20 ms).  In edge-id order a lane group reads each line
+        // several times in a row, so plain loads there (nontemporal ones
+        // made u_mul_e/sum on a degree-32 graph up to 24% slower)
+        const bool nt = random_edges && (TGT == DYN ? o.target == T_EDGE : TGT == T_EDGE);
         if (full) {
             if (nt) IO<T, VEC>::load_nt(base + col0, v);
             else IO<T, VEC>::load(base + col0, v);
@@ -345,20 +358,21 @@ __device__ __forceinline__ void fetch(const EngineArgs& A, int32_t nb, int32_t e
     } else if constexpr (EXT == EXT_BITS) {
 #pragma unroll
         for (int i = 0; i < VEC; ++i) r.a[i] = 0.0f;
-        if (r.kb) ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a);
+        if (r.kb) ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a, A.csr.eid != nullptr);
     } else {
-        ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a);
+        ld_opd<T, VEC, S::AT, S::AK, F>(A.a, nb, ed, self, col0, h, r.a, A.csr.eid != nullptr);
     }
     if constexpr (OPK >= 1) {
         if constexpr (S::PRE && S::BT == T_SELF) {
 #pragma unroll
             for (int i = 0; i < VEC; ++i) r.b[i] = pre.b[i];
         } else if constexpr (!S::CB) {
-            ld_opd<T, VEC, S::BT, S::BK, F>(A.b, nb, ed, self, col0, h, r.b);
+            ld_opd<T, VEC, S::BT, S::BK, F>(A.b, nb, ed, self, col0, h, r.b, A.csr.eid != nullptr);
         }
     }
     if constexpr (OPK == 2) {
-        if (A.op == M_NEGDIV2) ld_opd<T, VEC, DYN, DYN, false>(A.c, nb, ed, self, col0, h, r.c);
+        if (A.op == M_NEGDIV2)
+            ld_opd<T, VEC, DYN, DYN, false>(A.c, nb, ed, self, col0, h, r.c, A.csr.eid != nullptr);
     }
     const int32_t ar = row_of(S::AT == DYN ? A.a.target : S::AT, nb, ed, self);
     if constexpr (EXT == EXT_SCALE) r.dg = A.deg[ar];

@@ -16,7 +16,7 @@ namespace gnnk {
 // whole-row sum of a row wider than one pass (nchunk > 1: one lane group,
 // lane 0 writes every edge) keeps its running fp64 total per edge in xacc
 // between passes ch and writes the output in the last one.
-template <typename T, int VEC, int OPK, int EXT, int RM>
+template <typename T, int VEC, int OPK, int EXT, int RM, bool WAVE_ROW>
 struct SddmmSink {
     const EngineArgs& A;
     int lig, col0, h, ch;
@@ -34,9 +34,11 @@ struct SddmmSink {
                 for (int i = 0; i < VEC; ++i) v[i] = (float)(neg ? -m[i] : m[i]);
                 // written once, never read by this kernel: nontemporal vector
                 // stores keep the gathered node rows in L2 (c3 u_add_v 1.83 ->
-                // 1.59 ms; single-value stores of reduced outputs stay plain,
-                // u_dot_v was slower with them)
-                IO<T, VEC>::store_nt(row + col0, v);
+                // 1.59 ms) where the wavefront's lane groups write consecutive
+                // edges (whole lines per instruction); a lane group on a row of
+                // its own and single-value stores of reduced outputs stay plain
+                if constexpr (WAVE_ROW) IO<T, VEC>::store_nt(row + col0, v);
+                else IO<T, VEC>::store(row + col0, v);
             }
         } else {
             double s = 0.0;
@@ -78,7 +80,7 @@ __device__ __forceinline__ void sddmm_row(const EngineArgs& A, const Lanes& ln, 
         const int h = col0 / geo.F;
         Pre<VEC> pre;
         if (r >= 0) load_pre<T, VEC, OPK, S>(A, self, col0, h, pre);
-        SddmmSink<T, VEC, OPK, EXT, RM> sink{A, ln.lig, col0, h, ch, active};
+        SddmmSink<T, VEC, OPK, EXT, RM, WAVE_ROW> sink{A, ln.lig, col0, h, ch, active};
         if constexpr (WAVE_ROW) walk_row<T, VEC, OPK, EXT, S>(A, self, b, e, ln.g, G, col0, h, pre, sink);
         else walk_lane<T, VEC, OPK, EXT, S>(A, self, b, e, col0, h, pre, sink);
     }

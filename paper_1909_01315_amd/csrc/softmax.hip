@@ -14,12 +14,16 @@ template <typename T, int VEC>
 __device__ __forceinline__ void ld_edge(const OperandDev& o, int64_t ed, int col0, float* v) {
     IO<T, VEC>::load(reinterpret_cast<const T*>(o.data) + ed * o.stride + col0, v);
 }
-// the write pass reads each edge for the last time: nontemporal (c3 softmax
-// 2.22 -> 2.18 ms, its backward 3.55 -> 3.47 ms; the first pass keeps plain
-// loads, so that short rows are read again from L2)
+// the write pass reads each edge for the last time: nontemporal where a
+// wavefront's lane groups take consecutive edges of one row, so that an
+// instruction reads whole lines (c3 softmax 2.22 -> 2.18 ms, its backward
+// 3.55 -> 3.47 ms).  A lane group walking a row alone (stride 1) reads
+// each line several times in a row, and the first pass of every row keeps
+// plain loads, so that short rows are read again from L2.
 template <typename T, int VEC>
-__device__ __forceinline__ void ld_edge_last(const OperandDev& o, int64_t ed, int col0, float* v) {
-    IO<T, VEC>::load_nt(reinterpret_cast<const T*>(o.data) + ed * o.stride + col0, v);
+__device__ __forceinline__ void ld_edge_last(const OperandDev& o, int64_t ed, int col0, float* v, bool nt) {
+    if (nt) IO<T, VEC>::load_nt(reinterpret_cast<const T*>(o.data) + ed * o.stride + col0, v);
+    else IO<T, VEC>::load(reinterpret_cast<const T*>(o.data) + ed * o.stride + col0, v);
 }
 
 // running (max, sum of exp(s - max)) over the edges of a lane group
@@ -80,17 +84,21 @@ __device__ __forceinline__ void softmax_pass_write(const EngineArgs& A, int64_t 
     for (int64_t p = b + start; p < e; p += stride) {
         const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
         float s[VEC], v[VEC];
-        ld_edge_last<T, VEC>(A.a, ed, col0, s);
+        ld_edge_last<T, VEC>(A.a, ed, col0, s, stride > 1);
         if (backward) {
             float gg[VEC];
-            ld_edge_last<T, VEC>(A.b, ed, col0, gg);
+            ld_edge_last<T, VEC>(A.b, ed, col0, gg, stride > 1);
 #pragma unroll
             for (int i = 0; i < VEC; ++i) v[i] = (float)((double)s[i] * ((double)gg[i] - sum[i]));
         } else {
 #pragma unroll
             for (int i = 0; i < VEC; ++i) v[i] = exp_le0(s[i] - mx[i]) * inv[i];
         }
-        if (active) IO<T, VEC>::store_nt(reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0, v);
+        if (active) {
+            T* o = reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0;
+            if (stride > 1) IO<T, VEC>::store_nt(o, v);
+            else IO<T, VEC>::store(o, v);
+        }
     }
 }
 

@@ -225,12 +225,20 @@ __device__ __forceinline__ void write_cmp_row(const EngineArgs& A, int64_t row, 
     float v[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) v[i] = be[i] < 0 ? 0.0f : best[i];
-    // value and arg arrays are written once: nontemporal (c4 copy_u/max with
-    // arg edge 4.72 -> 4.48 ms, its three outputs being 2.9 GB)
-    IO<T, VEC>::store_nt(reinterpret_cast<T*>(A.out.data) + row * A.out.stride + col0, v);
+    // value and arg arrays are written once: nontemporal where a lane group
+    // writes whole lines of its row (8 lanes or more; c4 copy_u/max with arg
+    // edge 4.72 -> 4.48 ms, its three outputs being 2.9 GB), plain below that
     const int64_t D = (int64_t)A.geo.NV * VEC;
-    if (A.arg_edge) store_i32<VEC>(A.arg_edge + row * D + col0, be);
-    if (A.arg_nbr) store_i32<VEC>(A.arg_nbr + row * D + col0, bn);
+    T* out = reinterpret_cast<T*>(A.out.data) + row * A.out.stride + col0;
+    if (A.geo.L >= 8) {
+        IO<T, VEC>::store_nt(out, v);
+        if (A.arg_edge) store_i32<VEC>(A.arg_edge + row * D + col0, be);
+        if (A.arg_nbr) store_i32<VEC>(A.arg_nbr + row * D + col0, bn);
+    } else {
+        IO<T, VEC>::store(out, v);
+        if (A.arg_edge) store_i32<VEC, false>(A.arg_edge + row * D + col0, be);
+        if (A.arg_nbr) store_i32<VEC, false>(A.arg_nbr + row * D + col0, bn);
+    }
 }
 
 // Running max/min of one lane group.  The group sees its edges in ascending
