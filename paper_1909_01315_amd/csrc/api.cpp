@@ -142,6 +142,7 @@ CsrDev csr_of(const gnnk_graph* g, const Dir& d) {
     c.eid = d.eid;
     c.perm = d.perm;
     c.seg = d.seg;
+    c.seg_order = d.seg_order;
     c.hub_off = d.hub_off;
     c.row = d.row;
     c.ptr64 = g->ptr64;

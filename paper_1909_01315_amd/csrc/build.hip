@@ -364,6 +364,21 @@ hipError_t launch_edge_ends(const int32_t* idx, const int32_t* eid, const int32_
     return hipGetLastError();
 }
 
+// sort key of each hub segment: the halves of its first and last neighbour
+// id, summed (below the neighbour count, so it fits the key's bits)
+__global__ void seg_keys_kernel(const int4* seg, int64_t n_seg, const int32_t* idx, uint32_t* key) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n_seg; k += (int64_t)gridDim.x * blockDim.x) {
+        const int4 s = seg[k];
+        key[k] = ((uint32_t)idx[s.y] >> 1) + ((uint32_t)idx[s.z - 1] >> 1);
+    }
+}
+
+hipError_t launch_seg_keys(const int4* seg, int64_t n_seg, const int32_t* idx, uint32_t* key, hipStream_t s) {
+    if (n_seg <= 0) return hipSuccess;
+    hipLaunchKernelGGL(seg_keys_kernel, dim3(grid_1d(n_seg)), dim3(256), 0, s, seg, n_seg, idx, key);
+    return hipGetLastError();
+}
+
 hipError_t launch_hub_segments(const void* ptr, int ptr64, const int32_t* perm, const int32_t* hub_off, int64_t n_hub,
                                int64_t seg_edges, int4* seg, hipStream_t s) {
     if (n_hub <= 0) return hipSuccess;

@@ -130,8 +130,9 @@ __global__ __launch_bounds__(256) void gat_kernel(EngineArgs A, GatArgs G) {
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int4 s = A.csr.seg[w];
-            r = s.x; b = s.y; e = s.z; slot = w;
+            const int si = A.csr.seg_order[w];
+            const int4 s = A.csr.seg[si];
+            r = s.x; b = s.y; e = s.z; slot = si;
         } else {
             r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
             b = row_ptr(A.csr, r);
@@ -286,7 +287,7 @@ __global__ __launch_bounds__(256) void gat_attn_segments_kernel(EngineArgs A, Ga
     const GeomDev& geo = A.geo;
     const Lanes ln = lanes_of(geo);
     const int64_t D = (int64_t)geo.NV * VEC;
-    const int4 sg = A.csr.seg[w];
+    const int4 sg = A.csr.seg[A.csr.seg_order[w]];
     const double* ML = reinterpret_cast<const double*>(G.row_ml) + (int64_t)sg.w * 2 * D;
     for (int ch = 0; ch < geo.nchunk; ++ch) {
         const int j = ch * geo.L + ln.lig;
@@ -407,8 +408,9 @@ __global__ __launch_bounds__(256) void gat_bwd_dst_kernel(EngineArgs A, GatBwdAr
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int4 sg = A.csr.seg[w];
-            r = sg.x; b = sg.y; e = sg.z; slot = w;
+            const int si = A.csr.seg_order[w];
+            const int4 sg = A.csr.seg[si];
+            r = sg.x; b = sg.y; e = sg.z; slot = si;
         } else {
             r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
             b = row_ptr(A.csr, r);
@@ -583,8 +585,9 @@ __global__ __launch_bounds__(256) void gat_bwd_src_kernel(EngineArgs A, GatBwdAr
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int4 sg = A.csr.seg[w];
-            r = sg.x; b = sg.y; e = sg.z; slot = w;
+            const int si = A.csr.seg_order[w];
+            const int4 sg = A.csr.seg[si];
+            r = sg.x; b = sg.y; e = sg.z; slot = si;
         } else {
             r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
             b = row_ptr(A.csr, r);

@@ -95,7 +95,7 @@ constexpr int32_t FLAG_NOT_IDENT = 8; // edge ids differ from in-CSR positions
 struct Layout {
     size_t in_ptr = 0, in_idx = 0, in_eid = 0, out_ptr = 0, out_idx = 0, out_eid = 0;
     size_t in_deg = 0, out_deg = 0, in_perm = 0, out_perm = 0, in_row = 0, out_row = 0, out_pos = 0, flag = 0;
-    size_t in_hub = 0, out_hub = 0, in_seg = 0, out_seg = 0, total = 0;
+    size_t in_hub = 0, out_hub = 0, in_seg = 0, out_seg = 0, in_sego = 0, out_sego = 0, total = 0;
 };
 
 struct Bump {
@@ -129,6 +129,8 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t h
     L.out_hub = b.take((size_t)(hub_out + 1) * 4);
     L.in_seg = b.take((size_t)seg_in * 16);
     L.out_seg = b.take((size_t)seg_out * 16);
+    L.in_sego = b.take((size_t)seg_in * 4);
+    L.out_sego = b.take((size_t)seg_out * 4);
     L.total = b.off;
     return L;
 }
@@ -163,6 +165,7 @@ struct Builder {
     uint32_t* scratch = nullptr;
     hipStream_t s;
     hipError_t err = hipSuccess;
+    size_t scratch_words = 0;  // uint32 words of `scratch`
 
     void chk(hipError_t x) {
         if (err == hipSuccess) err = x;
@@ -183,6 +186,7 @@ struct Builder {
         const int64_t n = std::max(g->n_src, g->n_dst);
         const size_t words = std::max(radix_scratch_words(g->n_edges), 4 * (size_t)(n + 64) + radix_scratch_words(n));
         scratch = reinterpret_cast<uint32_t*>(graph_scratch(g, words * 4));
+        scratch_words = words;
         return scratch != nullptr;
     }
 
@@ -221,6 +225,36 @@ struct Builder {
         if (n > 0) chk(hipMemcpyAsync(keys_h.data(), sorted, (size_t)n * 4, hipMemcpyDeviceToHost, s));
     }
 
+    // The order in which wavefronts take the hub segments of a direction:
+    // by the neighbour ids a segment covers (its key, the halves of its
+    // first and last neighbour id summed), a stable sort, so equal keys keep
+    // table order.  Where rows list their neighbours in ascending order, the
+    // segments that run at the same time then gather from one slice of the
+    // neighbour table; elsewhere the order changes nothing.  Results do not
+    // depend on it (partials are combined in table order).
+    void order_segments(Dir& d, int64_t n_cols) {
+        const int64_t n = d.n_seg;
+        if (n <= 0) return;
+        const int64_t pad = (n + 63) / 64 * 64;
+        const size_t words = 4 * (size_t)pad + radix_scratch_words(n);
+        if (words > scratch_words) {
+            scratch = reinterpret_cast<uint32_t*>(graph_scratch(g, words * 4));
+            if (!scratch) {
+                if (err == hipSuccess) err = hipErrorOutOfMemory;
+                return;
+            }
+            scratch_words = words;
+        }
+        uint32_t* key = scratch;
+        uint32_t* sorted = key + pad;
+        uint32_t* tk = sorted + pad;
+        uint32_t* tv = tk + pad;
+        uint32_t* rs = tv + pad;
+        chk(launch_seg_keys(d.seg, n, d.idx, key, s));
+        chk(radix_sort_pairs(key, nullptr, n, key_bits(n_cols > 1 ? (uint64_t)(n_cols - 1) : 0), sorted,
+                             reinterpret_cast<uint32_t*>(d.seg_order), tk, tv, rs, s));
+    }
+
     // common tail: degree order, identity flag, hub tables
     gnnk_status finish(size_t ws_bytes, bool check_identity) {
         const int64_t E = g->n_edges;
@@ -256,10 +290,14 @@ struct Builder {
         out.hub_off = at<int32_t>(L.out_hub);
         in.seg = at<int4>(L.in_seg);
         out.seg = at<int4>(L.out_seg);
+        in.seg_order = at<int32_t>(L.in_sego);
+        out.seg_order = at<int32_t>(L.out_sego);
         chk(hipMemcpyAsync(in.hub_off, hin.data(), hin.size() * 4, hipMemcpyHostToDevice, s));
         chk(hipMemcpyAsync(out.hub_off, hout.data(), hout.size() * 4, hipMemcpyHostToDevice, s));
         chk(launch_hub_segments(in.ptr, g->ptr64, in.perm, in.hub_off, in.n_hub, g->seg_edges, in.seg, s));
         chk(launch_hub_segments(out.ptr, g->ptr64, out.perm, out.hub_off, out.n_hub, g->seg_edges, out.seg, s));
+        order_segments(in, g->n_src);
+        order_segments(out, g->n_dst);
         chk(hipMemsetAsync(g->flag, 0, 4, s));
         chk(hipStreamSynchronize(s));  // hin/hout are about to go away
         if (err != hipSuccess) return hip_fail(err, "graph build");

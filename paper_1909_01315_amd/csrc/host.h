@@ -23,6 +23,7 @@ struct Dir {
     int32_t* deg = nullptr;        // device degree per row
     int32_t* perm = nullptr;       // device rows by descending degree
     int4* seg = nullptr;           // device segments of hub rows
+    int32_t* seg_order = nullptr;  // device segment of each hub-segment wavefront
     int32_t* hub_off = nullptr;    // device first segment per hub row (n_hub + 1)
     int32_t* row = nullptr;        // device row of each position (COO form)
     int32_t* pos = nullptr;        // device position of each edge id in this CSR

@@ -66,6 +66,10 @@ struct CsrDev {
     const int32_t* eid;     // edge id of each position, nullptr = identity
     const int32_t* perm;    // rows by descending degree
     const int4* seg;        // {row, begin, end, hub index} per segment of a hub row
+    // segment taken by hub-segment wavefront w: segments in the order of the
+    // neighbour ids they cover, so that the segments of different rows that
+    // run at the same time gather from one slice of the neighbour table
+    const int32_t* seg_order;
     const int32_t* hub_off; // first segment of each hub row (hub rows = perm[0, n_hub)), n_hub + 1 entries
     const int32_t* row;     // row of each position (the COO form of the same CSR)
     int32_t ptr64;
@@ -231,6 +235,8 @@ hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, i
 hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int64_t n, hipStream_t s);
 
 // ----- device construction of the graph formats (build.hip) -----
+// key[k] = idx[seg[k].begin] / 2 + idx[seg[k].end - 1] / 2 for k < n_seg
+hipError_t launch_seg_keys(const int4* seg, int64_t n_seg, const int32_t* idx, uint32_t* key, hipStream_t s);
 // bits needed for keys in [0, max_key]
 int key_bits(uint64_t max_key);
 // uint32 words of scratch radix_sort_pairs needs for n pairs

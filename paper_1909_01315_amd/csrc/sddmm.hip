@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
     if (w < A.sch.w_big_end) {
         int64_t r, b, e;
         if (w < A.sch.n_seg) {
-            const int4 s = A.csr.seg[w];
+            const int4 s = A.csr.seg[A.csr.seg_order[w]];
             r = s.x; b = s.y; e = s.z;
         } else {
             r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];

@@ -115,8 +115,9 @@ __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
     int slot = -1;
     if (coop) {
         if (w < A.sch.n_seg) {
-            int4 s = A.csr.seg[w];
-            r = s.x; b = s.y; e = s.z; slot = w;
+            const int si = A.csr.seg_order[w];
+            const int4 s = A.csr.seg[si];
+            r = s.x; b = s.y; e = s.z; slot = si;
         } else {
             r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
             b = row_ptr(A.csr, r);
@@ -177,7 +178,7 @@ __global__ __launch_bounds__(256) void softmax_finish_kernel(EngineArgs A) {
     const Lanes ln = lanes_of(geo);
     const int g = ln.g, lig = ln.lig;
     const int64_t D = (int64_t)geo.NV * VEC;
-    const int4 sg = A.csr.seg[w];
+    const int4 sg = A.csr.seg[A.csr.seg_order[w]];
     const int s0 = A.csr.hub_off[sg.w], s1 = A.csr.hub_off[sg.w + 1];
     for (int ch = 0; ch < geo.nchunk; ++ch) {
         const int j = ch * geo.L + lig;

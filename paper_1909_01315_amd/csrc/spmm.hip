@@ -55,8 +55,9 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int4 s = A.csr.seg[w];
-            r = s.x; b = s.y; e = s.z; slot = w;
+            const int si = A.csr.seg_order[w];
+            const int4 s = A.csr.seg[si];
+            r = s.x; b = s.y; e = s.z; slot = si;
         } else {
             r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
             b = row_ptr(A.csr, r);
@@ -349,8 +350,9 @@ __global__ __launch_bounds__(256) void spmm_cmp_kernel(EngineArgs A) {
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int4 s = A.csr.seg[w];
-            r = s.x; b = s.y; e = s.z; slot = w;
+            const int si = A.csr.seg_order[w];
+            const int4 s = A.csr.seg[si];
+            r = s.x; b = s.y; e = s.z; slot = si;
         } else {
             r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
             b = row_ptr(A.csr, r);
