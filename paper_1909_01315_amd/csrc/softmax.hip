@@ -6,6 +6,8 @@
 // ds = a * (g - S).  Rows use the degree-sorted schedule; hub rows leave
 // per-segment (max, sum) or S partials and a second launch combines them in
 // segment order and writes the segment's edges.
+#include <type_traits>
+
 #include "device.h"
 
 namespace gnnk {
@@ -169,26 +171,29 @@ __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
     }
 }
 
-// hub rows: combine the segment partials of the row, then write this segment
-template <typename T, int VEC, bool BWD>
-__global__ __launch_bounds__(256) void softmax_finish_kernel(EngineArgs A) {
+// hub rows: combine the segment partials of each row once, in segment
+// order (one lane group per hub row), into the row's (max, sum) after the
+// segment partials
+template <int VEC, bool BWD>
+__global__ __launch_bounds__(256) void softmax_rows_kernel(EngineArgs A) {
     const int w = wave_id();
-    if (w >= A.sch.n_seg) return;
     const GeomDev& geo = A.geo;
     const Lanes ln = lanes_of(geo);
-    const int g = ln.g, lig = ln.lig;
+    if ((int64_t)w * geo.G >= A.sch.n_hub) return;  // wave-uniform
+    const int64_t k = (int64_t)w * geo.G + ln.g;
+    if (k >= A.sch.n_hub) return;
     const int64_t D = (int64_t)geo.NV * VEC;
-    const int4 sg = A.csr.seg[A.csr.seg_order[w]];
-    const int s0 = A.csr.hub_off[sg.w], s1 = A.csr.hub_off[sg.w + 1];
+    const int s0 = A.csr.hub_off[k], s1 = A.csr.hub_off[k + 1];
+    double* P = reinterpret_cast<double*>(A.partial);
+    double* R = P + ((int64_t)A.sch.n_seg + k) * 2 * D;
     for (int ch = 0; ch < geo.nchunk; ++ch) {
-        const int j = ch * geo.L + lig;
-        const bool active = j < geo.NV;
-        const int col0 = active ? j * VEC : 0;
+        const int j = ch * geo.L + ln.lig;
+        if (j >= geo.NV) continue;
+        const int col0 = j * VEC;
         float mx[VEC];
         double sum[VEC];
 #pragma unroll
         for (int i = 0; i < VEC; ++i) { mx[i] = -INFINITY; sum[i] = 0.0; }
-        const double* P = reinterpret_cast<const double*>(A.partial);
         if (!BWD) {
             for (int s = s0; s < s1; ++s)
 #pragma unroll
@@ -205,6 +210,36 @@ __global__ __launch_bounds__(256) void softmax_finish_kernel(EngineArgs A) {
                 sum[i] += part;
             }
         }
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            R[col0 + i] = (double)mx[i];
+            R[D + col0 + i] = sum[i];
+        }
+    }
+}
+
+// hub rows: write this segment with its row's combined (max, sum)
+template <typename T, int VEC, bool BWD>
+__global__ __launch_bounds__(256) void softmax_finish_kernel(EngineArgs A) {
+    const int w = wave_id();
+    if (w >= A.sch.n_seg) return;
+    const GeomDev& geo = A.geo;
+    const Lanes ln = lanes_of(geo);
+    const int g = ln.g, lig = ln.lig;
+    const int64_t D = (int64_t)geo.NV * VEC;
+    const int4 sg = A.csr.seg[A.csr.seg_order[w]];
+    const double* R = reinterpret_cast<const double*>(A.partial) + ((int64_t)A.sch.n_seg + sg.w) * 2 * D;
+    for (int ch = 0; ch < geo.nchunk; ++ch) {
+        const int j = ch * geo.L + lig;
+        const bool active = j < geo.NV;
+        const int col0 = active ? j * VEC : 0;
+        float mx[VEC];
+        double sum[VEC];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            mx[i] = (float)R[col0 + i];
+            sum[i] = R[D + col0 + i];
+        }
         softmax_pass_write<T, VEC>(A, sg.y, sg.z, g, geo.G, col0, active, mx, sum, BWD);
     }
 }
@@ -214,29 +249,30 @@ hipError_t launch_softmax(const EngineArgs& a, int dtype, int vec, bool backward
     if (a.sch.w_small_end <= 0) return hipSuccess;
     dim3 grid(blocks_for_waves(a.sch.w_small_end)), block(WAVE * WPB);
     dim3 fgrid(blocks_for_waves(a.sch.n_seg));
+    dim3 rgrid(blocks_for_waves((a.sch.n_hub + a.geo.G - 1) / a.geo.G));
+    // pass over all rows (hub segments leave partials), then for hub rows the
+    // per-row combine and the write pass of each segment
+    auto run = [&](auto tv, auto vv, auto bv) {
+        using T = decltype(tv);
+        constexpr int V = decltype(vv)::value;
+        constexpr bool B = decltype(bv)::value;
+        hipLaunchKernelGGL((softmax_kernel<T, V, B>), grid, block, 0, s, a);
+        if (a.sch.n_seg > 0) {
+            hipLaunchKernelGGL((softmax_rows_kernel<V, B>), rgrid, block, 0, s, a);
+            hipLaunchKernelGGL((softmax_finish_kernel<T, V, B>), fgrid, block, 0, s, a);
+        }
+    };
+    using BT = std::true_type;
+    using BF = std::false_type;
     if (dtype == 0) {
         GNNK_VEC_DISPATCH_F32(vec, {
-            if (backward) {
-                hipLaunchKernelGGL((softmax_kernel<float, V, true>), grid, block, 0, s, a);
-                if (a.sch.n_seg > 0)
-                    hipLaunchKernelGGL((softmax_finish_kernel<float, V, true>), fgrid, block, 0, s, a);
-            } else {
-                hipLaunchKernelGGL((softmax_kernel<float, V, false>), grid, block, 0, s, a);
-                if (a.sch.n_seg > 0)
-                    hipLaunchKernelGGL((softmax_finish_kernel<float, V, false>), fgrid, block, 0, s, a);
-            }
+            if (backward) run(float{}, std::integral_constant<int, V>{}, BT{});
+            else run(float{}, std::integral_constant<int, V>{}, BF{});
         })
     } else {
         GNNK_VEC_DISPATCH_BF16(vec, {
-            if (backward) {
-                hipLaunchKernelGGL((softmax_kernel<bf16_t, V, true>), grid, block, 0, s, a);
-                if (a.sch.n_seg > 0)
-                    hipLaunchKernelGGL((softmax_finish_kernel<bf16_t, V, true>), fgrid, block, 0, s, a);
-            } else {
-                hipLaunchKernelGGL((softmax_kernel<bf16_t, V, false>), grid, block, 0, s, a);
-                if (a.sch.n_seg > 0)
-                    hipLaunchKernelGGL((softmax_finish_kernel<bf16_t, V, false>), fgrid, block, 0, s, a);
-            }
+            if (backward) run(bf16_t{}, std::integral_constant<int, V>{}, BT{});
+            else run(bf16_t{}, std::integral_constant<int, V>{}, BF{});
         })
     }
     return hipGetLastError();
