@@ -217,6 +217,18 @@ constexpr int DPP_QUAD_2301 = 0x4E;  // quad_perm [2,3,0,1]
 constexpr int DPP_ROR12 = 0x12C;     // row_ror:12: lane i reads lane (i + 4) mod 16
 constexpr int DPP_ROR8 = 0x128;      // row_ror:8: lane i reads lane (i + 8) mod 16
 
+// run_sum with the run length known at compile time (no per-step branches)
+template <int RED>
+__device__ __forceinline__ double run_sum_c(double v) {
+    if constexpr (RED >= 2) v += dpp_d<DPP_QUAD_1032>(v);
+    if constexpr (RED >= 4) v += dpp_d<DPP_QUAD_2301>(v);
+    if constexpr (RED >= 8) v += dpp_d<DPP_ROR12>(v);
+    if constexpr (RED >= 16) v += dpp_d<DPP_ROR8>(v);
+    if constexpr (RED >= 32) v += shfl_xor_d(v, 16);
+    if constexpr (RED >= 64) v += shfl_xor_d(v, 32);
+    return v;
+}
+
 // Sum over aligned runs of `red` lanes (a power of two), correct in the first
 // lane of each run: DPP within 16-lane rows, swizzles beyond.
 __device__ __forceinline__ double run_sum(double v, int red) {

@@ -12,7 +12,8 @@ namespace gnnk {
 
 // Output of one edge: VEC columns (RM = 0), or the sum over runs of
 // out.red lanes (a head for dot, or the whole row): RM = 1 for power-of-two
-// runs (DPP within 16-lane rows), RM = -1 reads the mode at run time.  A
+// runs (DPP within 16-lane rows), RM > 1 for runs of exactly RM lanes known at
+// compile time (no per-step branches), RM = -1 reads the mode at run time.  A
 // whole-row sum of a row wider than one pass (nchunk > 1: one lane group,
 // lane 0 writes every edge) keeps its running fp64 total per edge in xacc
 // between passes ch and writes the output in the last one.
@@ -46,9 +47,11 @@ struct SddmmSink {
             for (int i = 0; i < VEC; ++i) s += m[i];
             const int red = A.out.red;
             s = active ? s : 0.0;
-            if constexpr (RM > 0) s = run_sum(s, red);
+            if constexpr (RM > 1) s = run_sum_c<RM>(s);
+            else if constexpr (RM == 1) s = run_sum(s, red);
             else s = (red & (red - 1)) == 0 ? run_sum(s, red) : seg_sum(s, lig, red);
-            const bool writer = RM > 0 ? ((lig & (red - 1)) == 0) : ((lig % red) == 0);
+            const bool writer = RM > 1 ? ((lig & (RM - 1)) == 0)
+                                       : (RM == 1 ? ((lig & (red - 1)) == 0) : ((lig % red) == 0));
             // (runtime-layout kernels only: the host picks them for such rows)
             if (RM < 0 && A.geo.nchunk > 1 && (ok & active & writer)) {
                 double* x = A.xacc + (uint32_t)ed;
@@ -124,25 +127,40 @@ using SpUV = Spec<T_NBR, OK_FULL, T_SELF, OK_FULL, C, false>;
 template <int C>
 using SpVU = Spec<T_SELF, OK_FULL, T_NBR, OK_FULL, C, false>;
 
+template <typename T, int V, int C, int R>
+void launch_sddmm_rm(const EngineArgs& a, int spec, dim3 grid, dim3 block, hipStream_t s) {
+    if (spec == SP_VU) hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, R, SpVU<C>>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, R, SpUV<C>>), grid, block, 0, s, a);
+}
+
+// red: lanes per reduced output (0: no reduction); a run of 2-64 lanes that
+// fits the lane group is a compile-time constant of the kernel
 template <typename T, int V, int C>
-void launch_sddmm_fast(const EngineArgs& a, int opk, int spec, int rm, dim3 grid, dim3 block, hipStream_t s) {
-    if (spec == SP_VU) {
-        if (rm) hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 1, SpVU<C>>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 0, SpVU<C>>), grid, block, 0, s, a);
-    } else if (opk == 1) {
-        if (rm) hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 1, SpUV<C>>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((sddmm_kernel<T, V, 1, EXT_NONE, 0, SpUV<C>>), grid, block, 0, s, a);
-    } else {
+void launch_sddmm_fast(const EngineArgs& a, int opk, int spec, int red, dim3 grid, dim3 block, hipStream_t s) {
+    if (spec != SP_VU && opk != 1) {
         hipLaunchKernelGGL((sddmm_kernel<T, V, 2, EXT_NONE, 0, SpUV<C>>), grid, block, 0, s, a);
+        return;
     }
+    constexpr int L = 64 / C;
+    switch (red) {
+        case 0: launch_sddmm_rm<T, V, C, 0>(a, spec, grid, block, s); return;
+        case 2: if constexpr (L >= 2) { launch_sddmm_rm<T, V, C, 2>(a, spec, grid, block, s); return; } break;
+        case 4: if constexpr (L >= 4) { launch_sddmm_rm<T, V, C, 4>(a, spec, grid, block, s); return; } break;
+        case 8: if constexpr (L >= 8) { launch_sddmm_rm<T, V, C, 8>(a, spec, grid, block, s); return; } break;
+        case 16: if constexpr (L >= 16) { launch_sddmm_rm<T, V, C, 16>(a, spec, grid, block, s); return; } break;
+        case 32: if constexpr (L >= 32) { launch_sddmm_rm<T, V, C, 32>(a, spec, grid, block, s); return; } break;
+        case 64: if constexpr (L >= 64) { launch_sddmm_rm<T, V, C, 64>(a, spec, grid, block, s); return; } break;
+        default: break;
+    }
+    launch_sddmm_rm<T, V, C, 1>(a, spec, grid, block, s);
 }
 
 template <typename T, int V>
 void launch_sddmm_t(const EngineArgs& a, int opk, int ext, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
     if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
         if (spec == SP_UV || spec == SP_VU) {
-            const int rm = a.out.reduce ? 1 : 0;
-            GNNK_GC_DISPATCH(gc, launch_sddmm_fast<T, V, C>(a, opk, spec, rm, grid, block, s))
+            const int red = a.out.reduce ? a.out.red : 0;
+            GNNK_GC_DISPATCH(gc, launch_sddmm_fast<T, V, C>(a, opk, spec, red, grid, block, s))
             return;
         }
     }

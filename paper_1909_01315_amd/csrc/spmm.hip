@@ -21,7 +21,9 @@ namespace gnnk {
 // DW: also write, per edge, the dot of a (dZ[v]) with the row's own x2
 // (X[u]) over runs of red2 lanes -- the edge-weight gradient of u_mul_e/sum,
 // computed in the reverse pass that gathers dZ[v] anyway
-template <typename T, int VEC, bool DW>
+// (DW: 0 none; 1 runs of A.red2 lanes read at run time; 2-64 runs of DW
+// lanes fixed at compile time, with no per-step branches)
+template <typename T, int VEC, int DW>
 struct EdgeDot {
     float x[VEC];
     __device__ __forceinline__ void load(const EngineArgs& A, int32_t self, int col0) {
@@ -33,15 +35,17 @@ struct EdgeDot {
             double dp = 0.0;
 #pragma unroll
             for (int i = 0; i < VEC; ++i) dp = fma((double)rw.a[i], (double)x[i], dp);
-            dp = run_sum(dp, A.red2);
-            if (ok & active & ((lig & (A.red2 - 1)) == 0))
+            const int red = DW > 1 ? DW : A.red2;
+            if constexpr (DW > 1) dp = run_sum_c<DW>(dp);
+            else dp = run_sum(dp, red);
+            if (ok & active & ((lig & (red - 1)) == 0))
                 IO<T, 1>::store1_nt(reinterpret_cast<T*>(A.out2) + (int64_t)ed * A.out2_stride +
                                         (A.per_head2 ? h : 0), (float)dp);
         }
     }
 };
 
-template <typename T, int VEC, int OPK, int EXT, class S, bool DW = false>
+template <typename T, int VEC, int OPK, int EXT, class S, int DW = 0>
 __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
     const int w = wave_id();
     if (w >= A.sch.w_total) return;
@@ -488,12 +492,28 @@ void launch_cmp_t(const EngineArgs& a, int opk, int spec, int gc, dim3 grid, dim
 template <typename T, int V>
 void launch_dw_t(const EngineArgs& a, int spec, int gc, dim3 grid, dim3 block, hipStream_t s) {
     if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
-        auto go = [&](auto cg) {
+        // the edge gradient's lane runs (a.red2) as a compile-time constant
+        // when they are 2-32 lanes long (the host fuses only runs that fit
+        // the lane group), else read at run time
+        auto launch = [&](auto cg, auto rg) {
             constexpr int C = decltype(cg)::value;
+            constexpr int R = decltype(rg)::value;
             if (spec == SP_UE_H)
-                hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUEH<C, false>, true>), grid, block, 0, s, a);
+                hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUEH<C, false>, R>), grid, block, 0, s, a);
             else
-                hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUER<C, false>, true>), grid, block, 0, s, a);
+                hipLaunchKernelGGL((spmm_sum_kernel<T, V, 1, EXT_NONE, SpUER<C, false>, R>), grid, block, 0, s, a);
+        };
+        auto go = [&](auto cg) {
+            constexpr int L = 64 / decltype(cg)::value;
+            switch (a.red2) {
+                case 2: if constexpr (L >= 2) { launch(cg, std::integral_constant<int, 2>{}); return; } break;
+                case 4: if constexpr (L >= 4) { launch(cg, std::integral_constant<int, 4>{}); return; } break;
+                case 8: if constexpr (L >= 8) { launch(cg, std::integral_constant<int, 8>{}); return; } break;
+                case 16: if constexpr (L >= 16) { launch(cg, std::integral_constant<int, 16>{}); return; } break;
+                case 32: if constexpr (L >= 32) { launch(cg, std::integral_constant<int, 32>{}); return; } break;
+                default: break;
+            }
+            launch(cg, std::integral_constant<int, 1>{});
         };
         if (gc == 1) go(std::integral_constant<int, 1>{});
         else if (gc == 2) go(std::integral_constant<int, 2>{});
