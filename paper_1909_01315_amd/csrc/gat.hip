@@ -325,6 +325,14 @@ __device__ __forceinline__ double head_sum(double v, int lig, int red) {
     return (red & (red - 1)) == 0 ? run_sum(v, red) : seg_sum(v, lig, red);
 }
 
+// head_sum with the lanes per head fixed at compile time (RED > 0: a power
+// of two, no per-step branches) or read at run time (RED = 0)
+template <int RED>
+__device__ __forceinline__ double head_sum_t(double v, int lig, int red) {
+    if constexpr (RED > 0) return run_sum_c<RED>(v);
+    else return head_sum(v, lig, red);
+}
+
 // the attention of one edge, recomputed as the forward computes it
 __device__ __forceinline__ float gat_attention(float el, float er, float slope, float m, float il, bool& pos) {
     const float s = el + er;
@@ -341,12 +349,12 @@ __device__ __forceinline__ void gat_finish_dst(const GatBwdArgs& B, int64_t v, i
 
 // pass A: one destination row (a hub segment, a row by the wavefront, or a
 // row by this lane group)
-template <typename T, int VEC, class S, bool WAVE_ROW>
+template <typename T, int VEC, class S, bool WAVE_ROW, int RED>
 __device__ __forceinline__ void gat_bwd_dst_row(const EngineArgs& A, const GatBwdArgs& B, const Lanes& ln, int Gn,
                                                 int64_t r, int64_t b, int64_t e, int slot) {
     const GeomDev& geo = A.geo;
     const int L = WAVE / Gn;
-    const int red = geo.F / VEC;
+    const int red = RED > 0 ? RED : geo.F / VEC;
     const bool active = ln.lig < geo.NV;
     const int col0 = active ? ln.lig * VEC : 0;
     const int h = col0 / geo.F;
@@ -368,7 +376,7 @@ __device__ __forceinline__ void gat_bwd_dst_row(const EngineArgs& A, const GatBw
         double dp = 0.0;
 #pragma unroll
         for (int i = 0; i < VEC; ++i) dp = fma((double)rw.a[i], dzd[i], dp);
-        const double da = head_sum(dp, ln.lig, red);
+        const double da = head_sum_t<RED>(dp, ln.lig, red);
         const double lk = pos ? 1.0 : (double)B.slope;
         const double ad = a * da;
         sS += ok ? ad : 0.0;
@@ -397,7 +405,7 @@ __device__ __forceinline__ void gat_bwd_dst_row(const EngineArgs& A, const GatBw
     }
 }
 
-template <typename T, int VEC, class S>
+template <typename T, int VEC, class S, int RED>
 __global__ __launch_bounds__(256) void gat_bwd_dst_kernel(EngineArgs A, GatBwdArgs B) {
     const int w = wave_id();
     if (w >= A.sch.w_total) return;
@@ -416,7 +424,7 @@ __global__ __launch_bounds__(256) void gat_bwd_dst_kernel(EngineArgs A, GatBwdAr
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        gat_bwd_dst_row<T, VEC, S, true>(A, B, ln, Gn, uniform64(r), uniform64(b), uniform64(e), slot);
+        gat_bwd_dst_row<T, VEC, S, true, RED>(A, B, ln, Gn, uniform64(r), uniform64(b), uniform64(e), slot);
     } else if (w < A.sch.w_small_end) {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * Gn + ln.g;
         int64_t r = -1, b = 0, e = 0;
@@ -425,7 +433,7 @@ __global__ __launch_bounds__(256) void gat_bwd_dst_kernel(EngineArgs A, GatBwdAr
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        gat_bwd_dst_row<T, VEC, S, false>(A, B, ln, Gn, r, b, e, -1);
+        gat_bwd_dst_row<T, VEC, S, false, RED>(A, B, ln, Gn, r, b, e, -1);
     } else if (B.d_er) {
         // rows without in-edges: d_er = 0 (no edge reads their record)
         const int64_t k0 = A.sch.n_nz + ((int64_t)(w - A.sch.w_small_end) * Gn + ln.g) * A.sch.fill_rows_per_group;
@@ -516,11 +524,11 @@ __device__ __forceinline__ void gat_write_src(const GatBwdArgs& B, int64_t u, in
 
 // pass B: one source row (a hub segment, a row by the wavefront, or a row by
 // this lane group)
-template <typename T, int VEC, bool WAVE_ROW>
+template <typename T, int VEC, bool WAVE_ROW, int RED>
 __device__ __forceinline__ void gat_bwd_src_row(const EngineArgs& A, const GatBwdArgs& B, const Lanes& ln,
                                                 int64_t r, int64_t b, int64_t e, int slot) {
     const GeomDev& geo = A.geo;
-    const int red = geo.F / VEC;
+    const int red = RED > 0 ? RED : geo.F / VEC;
     const bool active = ln.lig < geo.NV;
     const int col0 = active ? ln.lig * VEC : 0;
     const int h = col0 / geo.F;
@@ -542,7 +550,7 @@ __device__ __forceinline__ void gat_bwd_src_row(const EngineArgs& A, const GatBw
         double dp = 0.0;
 #pragma unroll
         for (int i = 0; i < VEC; ++i) dp = fma((double)z[i], xd[i], dp);
-        const double da = head_sum(dp, ln.lig, red);
+        const double da = head_sum_t<RED>(dp, ln.lig, red);
         const double lk = pos ? 1.0 : (double)B.slope;
         const double ak = ok ? a : 0.0;
 #pragma unroll
@@ -575,7 +583,7 @@ __device__ __forceinline__ void gat_bwd_src_row(const EngineArgs& A, const GatBw
     }
 }
 
-template <typename T, int VEC>
+template <typename T, int VEC, int RED>
 __global__ __launch_bounds__(256) void gat_bwd_src_kernel(EngineArgs A, GatBwdArgs B) {
     const int w = wave_id();
     if (w >= A.sch.w_total) return;
@@ -593,7 +601,7 @@ __global__ __launch_bounds__(256) void gat_bwd_src_kernel(EngineArgs A, GatBwdAr
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        gat_bwd_src_row<T, VEC, true>(A, B, ln, uniform64(r), uniform64(b), uniform64(e), slot);
+        gat_bwd_src_row<T, VEC, true, RED>(A, B, ln, uniform64(r), uniform64(b), uniform64(e), slot);
     } else if (w < A.sch.w_small_end) {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + ln.g;
         int64_t r = -1, b = 0, e = 0;
@@ -602,7 +610,7 @@ __global__ __launch_bounds__(256) void gat_bwd_src_kernel(EngineArgs A, GatBwdAr
             b = row_ptr(A.csr, r);
             e = row_ptr(A.csr, r + 1);
         }
-        gat_bwd_src_row<T, VEC, false>(A, B, ln, r, b, e, -1);
+        gat_bwd_src_row<T, VEC, false, RED>(A, B, ln, r, b, e, -1);
     } else {
         // sources without out-edges: zero gradients
         const int64_t k0 = A.sch.n_nz + ((int64_t)(w - A.sch.w_small_end) * geo.G + ln.g) * A.sch.fill_rows_per_group;
@@ -678,8 +686,8 @@ void gat_all(const EngineArgs& a, const GatArgs& g, int gc, hipStream_t s) {
     }
 }
 
-template <typename T, int V>
-void gat_bwd_all(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs& B, int gc, hipStream_t s) {
+template <typename T, int V, int RED>
+void gat_bwd_red(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs& B, int gc, hipStream_t s) {
     const dim3 block(WAVE * WPB);
     if (ain.sch.w_total > 0) {
         const dim3 grid(blocks_for_waves(ain.sch.w_total));
@@ -687,14 +695,14 @@ void gat_bwd_all(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs
         if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
             if (gc > 0) {
                 GNNK_GC_DISPATCH(gc, {
-                    hipLaunchKernelGGL((gat_bwd_dst_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, C, false>>),
+                    hipLaunchKernelGGL((gat_bwd_dst_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, C, false>, RED>),
                                        grid, block, 0, s, ain, B);
                 })
                 done = true;
             }
         }
         if (!done)
-            hipLaunchKernelGGL((gat_bwd_dst_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, 0, false>>), grid,
+            hipLaunchKernelGGL((gat_bwd_dst_kernel<T, V, Spec<T_NBR, OK_FULL, T_NBR, OK_HEAD, 0, false>, RED>), grid,
                                block, 0, s, ain, B);
         if (ain.sch.n_hub > 0) {
             const int64_t n = (int64_t)ain.sch.n_hub * B.H;
@@ -703,12 +711,25 @@ void gat_bwd_all(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs
         }
     }
     if (aout.sch.w_total > 0 && (B.d_feat || B.d_el)) {
-        hipLaunchKernelGGL((gat_bwd_src_kernel<T, V>), dim3(blocks_for_waves(aout.sch.w_total)), block, 0, s, aout,
-                           B);
+        hipLaunchKernelGGL((gat_bwd_src_kernel<T, V, RED>), dim3(blocks_for_waves(aout.sch.w_total)), block, 0, s,
+                           aout, B);
         if (aout.sch.n_hub > 0)
             hipLaunchKernelGGL((gat_bwd_src_combine_kernel<T, V>),
                                dim3(blocks_for_waves((aout.sch.n_hub + aout.geo.G - 1) / aout.geo.G)), block, 0, s,
                                aout, B);
+    }
+}
+
+// both passes with the lanes per head (F / V) as a compile-time constant
+// when it is 2-16, else read at run time
+template <typename T, int V>
+void gat_bwd_all(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs& B, int gc, hipStream_t s) {
+    switch (ain.geo.F / V) {
+        case 2: gat_bwd_red<T, V, 2>(ain, aout, B, gc, s); return;
+        case 4: gat_bwd_red<T, V, 4>(ain, aout, B, gc, s); return;
+        case 8: gat_bwd_red<T, V, 8>(ain, aout, B, gc, s); return;
+        case 16: gat_bwd_red<T, V, 16>(ain, aout, B, gc, s); return;
+        default: gat_bwd_red<T, V, 0>(ain, aout, B, gc, s); return;
     }
 }
 
