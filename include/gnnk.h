@@ -120,6 +120,13 @@ typedef struct {
  * on the device, on `stream`: stable radix sorts of (row, edge id) pairs, so
  * each row lists its edges in ascending edge id, row offsets by binary search
  * in the sorted rows, and rows ordered by descending degree (ties by row id).
+ * The segments of long rows are also ordered by the neighbour ids they cover
+ * (the halves of their first and last neighbour id, summed; a stable sort):
+ * calls take them in that order, so that where rows list their neighbours in
+ * ascending order (an edge list sorted by destination, then source) the
+ * segments processed at the same time gather from one slice of the neighbour
+ * table.  The order never changes a result: segment partials are combined in
+ * table order.
  * The call synchronises `stream` twice (after checking the input, and to read
  * back the sorted degrees) and may allocate the handle's scratch buffer. */
 
