@@ -34,7 +34,7 @@ from test_gpu_gat import oracle_gat, oracle_gat_backward
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 160
+N_CASES = 400
 OPS = ["copy_lhs", "copy_rhs", "add", "sub", "mul", "div"]
 TARGETS = ["u", "e", "v"]
 
