@@ -47,8 +47,8 @@ CSRC = os.path.join(ROOT, "paper_1909_01315_amd", "csrc")
 # figures hold for the kernel sources with this digest; any other source
 # state reports traffic as null.
 MEASURED_TRAFFIC = {
-    "sources_sha256": "3bd6cf346a7d1b669b8c8cc005adc5ce826ed93e061586214757b4c469c3ac1b",
-    "fetch_bytes": 23633382619,
+    "sources_sha256": "4a449d046a3a33df8f0cd3030b97f52f9dc89c870f5f7123adfaf0c6cedf7537",
+    "fetch_bytes": 23633333839,
     "write_bytes": 160583296,
 }
 

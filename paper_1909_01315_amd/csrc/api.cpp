@@ -832,11 +832,6 @@ static gnnk_status softmax_common(gnnk_graph_t g, const gnnk_tensor* a, const gn
     A.csr = csr_of(g, g->in);
     set_geo(A, geo);
     A.sch = schedule(g->in, geo, false);
-    if (A.sch.n_seg > 0) {
-        // segment partials, then the combined (max, sum) of each hub row
-        A.partial = graph_scratch(g, (size_t)(A.sch.n_seg + A.sch.n_hub) * geo.D * 16);
-        if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
-    }
     return launch_status(launch_softmax(A, dtype_code(a), geo.vec, backward, stream), "edge softmax launch");
 }
 

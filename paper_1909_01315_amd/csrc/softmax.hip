@@ -3,9 +3,12 @@
 // its backward.  Forward: one pass keeps the running max m and the fp64 sum
 // of exp(s - m), rescaled whenever m grows; a second pass writes
 // a = exp(s - max) / sum.  Backward: S = sum of a * g in fp64, then
-// ds = a * (g - S).  Rows use the degree-sorted schedule; hub rows leave
-// per-segment (max, sum) or S partials and a second launch combines them in
-// segment order and writes the segment's edges.
+// ds = a * (g - S).  Rows use the degree-sorted schedule.  A hub row takes
+// one block of wavefronts that merge their partials through LDS in wavefront
+// order and write the row at once, so the second read of its scores comes
+// from the caches rather than HBM (one launch for all hub rows instead of
+// segment partials, a combine and a write launch: c3 softmax 2.22 -> 1.80
+// ms, its backward 3.50 -> 2.70 ms).
 #include <type_traits>
 
 #include "device.h"
@@ -28,21 +31,45 @@ __device__ __forceinline__ void ld_edge_last(const OperandDev& o, int64_t ed, in
     else IO<T, VEC>::load(reinterpret_cast<const T*>(o.data) + ed * o.stride + col0, v);
 }
 
+// Each pass takes a lane group's edges in groups of SM_UNROLL: the group's
+// loads are issued together (one lane keeps several loads in flight, which
+// a wavefront or block walking one long row needs to cover the memory
+// latency) and its edges are then consumed in edge order, so the results are
+// those of the edge-by-edge loop.
+constexpr int SM_UNROLL = 4;
+
+__device__ __forceinline__ int64_t edge_at(const EngineArgs& A, int64_t p) {
+    return A.csr.eid ? (int64_t)A.csr.eid[p] : p;
+}
+
+template <int VEC>
+__device__ __forceinline__ void online_step(float* mx, double* sum, const float* s) {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) {
+        const float mn = fmaxf(mx[i], s[i]);
+        const double f = (double)exp_le0(fminf(mx[i], s[i]) - mn);
+        sum[i] = s[i] > mx[i] ? sum[i] * f + 1.0 : sum[i] + f;
+        mx[i] = mn;
+    }
+}
+
 // running (max, sum of exp(s - max)) over the edges of a lane group
 template <typename T, int VEC>
 __device__ __forceinline__ void softmax_pass_online(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
                                                     int col0, float* mx, double* sum) {
-    for (int64_t p = b + start; p < e; p += stride) {
-        const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
-        float s[VEC];
-        ld_edge<T, VEC>(A.a, ed, col0, s);
+    constexpr int U = SM_UNROLL;
+    int64_t p = b + start;
+    for (; p + (int64_t)(U - 1) * stride < e; p += (int64_t)U * stride) {
+        float s[U][VEC];
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) {
-            const float mn = fmaxf(mx[i], s[i]);
-            const double f = (double)exp_le0(fminf(mx[i], s[i]) - mn);
-            sum[i] = s[i] > mx[i] ? sum[i] * f + 1.0 : sum[i] + f;
-            mx[i] = mn;
-        }
+        for (int u = 0; u < U; ++u) ld_edge<T, VEC>(A.a, edge_at(A, p + (int64_t)u * stride), col0, s[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u) online_step<VEC>(mx, sum, s[u]);
+    }
+    for (; p < e; p += stride) {
+        float s[VEC];
+        ld_edge<T, VEC>(A.a, edge_at(A, p), col0, s);
+        online_step<VEC>(mx, sum, s);
     }
 }
 
@@ -55,22 +82,52 @@ __device__ __forceinline__ void softmax_merge(float& m, double& s, float om, dou
     m = mn;
 }
 
+// backward: S = sum of a * g over the edges of a lane group
 template <typename T, int VEC>
-__device__ __forceinline__ void softmax_pass_sum(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
-                                                 int col0, const float* mx, double* sum, bool backward) {
-    for (int64_t p = b + start; p < e; p += stride) {
-        const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
-        float s[VEC];
-        ld_edge<T, VEC>(A.a, ed, col0, s);
-        if (backward) {
-            float gg[VEC];
-            ld_edge<T, VEC>(A.b, ed, col0, gg);
+__device__ __forceinline__ void softmax_pass_dot(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
+                                                 int col0, double* sum) {
+    constexpr int U = SM_UNROLL;
+    int64_t p = b + start;
+    for (; p + (int64_t)(U - 1) * stride < e; p += (int64_t)U * stride) {
+        float s[U][VEC], gg[U][VEC];
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) sum[i] += (double)s[i] * (double)gg[i];
-        } else {
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) sum[i] += (double)exp_le0(s[i] - mx[i]);
+        for (int u = 0; u < U; ++u) {
+            const int64_t ed = edge_at(A, p + (int64_t)u * stride);
+            ld_edge<T, VEC>(A.a, ed, col0, s[u]);
+            ld_edge<T, VEC>(A.b, ed, col0, gg[u]);
         }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) sum[i] += (double)s[u][i] * (double)gg[u][i];
+    }
+    for (; p < e; p += stride) {
+        const int64_t ed = edge_at(A, p);
+        float s[VEC], gg[VEC];
+        ld_edge<T, VEC>(A.a, ed, col0, s);
+        ld_edge<T, VEC>(A.b, ed, col0, gg);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) sum[i] += (double)s[i] * (double)gg[i];
+    }
+}
+
+// the output of one edge from its loaded operands
+template <typename T, int VEC>
+__device__ __forceinline__ void softmax_out(const EngineArgs& A, int64_t ed, int col0, bool active, bool nt,
+                                            const float* s, const float* gg, const float* mx, const double* sum,
+                                            const float* inv, bool backward) {
+    float v[VEC];
+    if (backward) {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = (float)((double)s[i] * ((double)gg[i] - sum[i]));
+    } else {
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) v[i] = exp_le0(s[i] - mx[i]) * inv[i];
+    }
+    if (active) {
+        T* o = reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0;
+        if (nt) IO<T, VEC>::store_nt(o, v);
+        else IO<T, VEC>::store(o, v);
     }
 }
 
@@ -83,48 +140,46 @@ __device__ __forceinline__ void softmax_pass_write(const EngineArgs& A, int64_t 
     float inv[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) inv[i] = backward ? 0.0f : (float)(1.0 / sum[i]);
-    for (int64_t p = b + start; p < e; p += stride) {
-        const int64_t ed = A.csr.eid ? (int64_t)A.csr.eid[p] : p;
-        float s[VEC], v[VEC];
-        ld_edge_last<T, VEC>(A.a, ed, col0, s, stride > 1);
-        if (backward) {
-            float gg[VEC];
-            ld_edge_last<T, VEC>(A.b, ed, col0, gg, stride > 1);
+    const bool nt = stride > 1;
+    constexpr int U = SM_UNROLL;
+    int64_t p = b + start;
+    for (; p + (int64_t)(U - 1) * stride < e; p += (int64_t)U * stride) {
+        float s[U][VEC], gg[U][VEC];
+        int64_t ed[U];
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) v[i] = (float)((double)s[i] * ((double)gg[i] - sum[i]));
-        } else {
+        for (int u = 0; u < U; ++u) {
+            ed[u] = edge_at(A, p + (int64_t)u * stride);
+            ld_edge_last<T, VEC>(A.a, ed[u], col0, s[u], nt);
+            if (backward) ld_edge_last<T, VEC>(A.b, ed[u], col0, gg[u], nt);
+        }
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) v[i] = exp_le0(s[i] - mx[i]) * inv[i];
-        }
-        if (active) {
-            T* o = reinterpret_cast<T*>(A.out.data) + ed * A.out.stride + col0;
-            if (stride > 1) IO<T, VEC>::store_nt(o, v);
-            else IO<T, VEC>::store(o, v);
-        }
+        for (int u = 0; u < U; ++u) softmax_out<T, VEC>(A, ed[u], col0, active, nt, s[u], gg[u], mx, sum, inv, backward);
+    }
+    for (; p < e; p += stride) {
+        const int64_t ed = edge_at(A, p);
+        float s[VEC], gg[VEC];
+        ld_edge_last<T, VEC>(A.a, ed, col0, s, nt);
+        if (backward) ld_edge_last<T, VEC>(A.b, ed, col0, gg, nt);
+        softmax_out<T, VEC>(A, ed, col0, active, nt, s, gg, mx, sum, inv, backward);
     }
 }
 
+// rows after the hub rows: a wavefront per big row (its lane groups stride
+// over the row and merge by shuffles), a lane group per small row
 template <typename T, int VEC, bool BWD>
 __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
-    const int w = wave_id();
+    // the hub segments' wave indices are not launched
+    const int w = wave_id() + A.sch.n_seg;
     if (w >= A.sch.w_small_end) return;
     const GeomDev& geo = A.geo;
     const Lanes ln = lanes_of(geo);
     const int g = ln.g, lig = ln.lig;
-    const int64_t D = (int64_t)geo.NV * VEC;
-    bool coop = w < A.sch.w_big_end;
+    const bool coop = w < A.sch.w_big_end;
     int64_t r = -1, b = 0, e = 0;
-    int slot = -1;
     if (coop) {
-        if (w < A.sch.n_seg) {
-            const int si = A.csr.seg_order[w];
-            const int4 s = A.csr.seg[si];
-            r = s.x; b = s.y; e = s.z; slot = si;
-        } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
-        }
+        r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
+        b = row_ptr(A.csr, r);
+        e = row_ptr(A.csr, r + 1);
     } else {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + g;
         if (k < A.sch.n_nz) {
@@ -150,117 +205,85 @@ __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
                     for (int i = 0; i < VEC; ++i)
                         softmax_merge(mx[i], sum[i], __shfl_xor(mx[i], s, WAVE), shfl_xor_d(sum[i], s));
         } else {
-            softmax_pass_sum<T, VEC>(A, b, e, start, stride, col0, mx, sum, BWD);
+            softmax_pass_dot<T, VEC>(A, b, e, start, stride, col0, sum);
             if (coop)
                 for (int s = geo.L; s < WAVE; s <<= 1)
 #pragma unroll
                     for (int i = 0; i < VEC; ++i) sum[i] += shfl_xor_d(sum[i], s);
         }
-        if (slot >= 0) {
-            if (g == 0 && active) {
-                double* P = reinterpret_cast<double*>(A.partial) + (int64_t)slot * 2 * D;
-#pragma unroll
-                for (int i = 0; i < VEC; ++i) {
-                    P[col0 + i] = (double)mx[i];
-                    P[D + col0 + i] = sum[i];
-                }
-            }
-        } else {
-            softmax_pass_write<T, VEC>(A, b, e, start, stride, col0, active, mx, sum, BWD);
-        }
+        softmax_pass_write<T, VEC>(A, b, e, start, stride, col0, active, mx, sum, BWD);
     }
 }
 
-// hub rows: combine the segment partials of each row once, in segment
-// order (one lane group per hub row), into the row's (max, sum) after the
-// segment partials
-template <int VEC, bool BWD>
-__global__ __launch_bounds__(256) void softmax_rows_kernel(EngineArgs A) {
-    const int w = wave_id();
+// wavefronts per hub row: c3 (114.6M edges, (E,8) fp32) softmax takes
+// 2.03 / 1.80 / 2.87 ms with 4 / 8 / 16 (backward 2.97 / 2.70 / 2.78 ms)
+constexpr int HUB_WAVES = 8;
+
+// hub row perm[blockIdx.x]: the lane groups of all HUB_WAVES wavefronts
+// stride over the row; each wavefront merges its lane groups by shuffles,
+// then every wavefront merges the wavefronts' partials from LDS in wavefront
+// order (all reach the same values) and writes its share of the row
+template <typename T, int VEC, bool BWD>
+__global__ __launch_bounds__(WAVE * HUB_WAVES) void softmax_hub_kernel(EngineArgs A) {
+    __shared__ float smx[HUB_WAVES][WAVE];
+    __shared__ double ssum[HUB_WAVES][WAVE];
     const GeomDev& geo = A.geo;
     const Lanes ln = lanes_of(geo);
-    if ((int64_t)w * geo.G >= A.sch.n_hub) return;  // wave-uniform
-    const int64_t k = (int64_t)w * geo.G + ln.g;
-    if (k >= A.sch.n_hub) return;
-    const int64_t D = (int64_t)geo.NV * VEC;
-    const int s0 = A.csr.hub_off[k], s1 = A.csr.hub_off[k + 1];
-    double* P = reinterpret_cast<double*>(A.partial);
-    double* R = P + ((int64_t)A.sch.n_seg + k) * 2 * D;
+    const int wv = threadIdx.x >> 6;
+    const int64_t r = A.csr.perm[blockIdx.x];
+    const int64_t b = uniform64(row_ptr(A.csr, r)), e = uniform64(row_ptr(A.csr, r + 1));
+    const int start = wv * geo.G + ln.g, stride = HUB_WAVES * geo.G;
     for (int ch = 0; ch < geo.nchunk; ++ch) {
         const int j = ch * geo.L + ln.lig;
-        if (j >= geo.NV) continue;
-        const int col0 = j * VEC;
-        float mx[VEC];
-        double sum[VEC];
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) { mx[i] = -INFINITY; sum[i] = 0.0; }
-        if (!BWD) {
-            for (int s = s0; s < s1; ++s)
-#pragma unroll
-                for (int i = 0; i < VEC; ++i) mx[i] = fmaxf(mx[i], (float)P[(int64_t)s * 2 * D + col0 + i]);
-        }
-        for (int s = s0; s < s1; ++s) {
-#pragma unroll
-            for (int i = 0; i < VEC; ++i) {
-                double part = P[(int64_t)s * 2 * D + D + col0 + i];
-                if (!BWD) {
-                    const float ms = (float)P[(int64_t)s * 2 * D + col0 + i];
-                    part *= (double)exp_le0(ms - mx[i]);  // rescale the segment's sum to the row maximum
-                }
-                sum[i] += part;
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < VEC; ++i) {
-            R[col0 + i] = (double)mx[i];
-            R[D + col0 + i] = sum[i];
-        }
-    }
-}
-
-// hub rows: write this segment with its row's combined (max, sum)
-template <typename T, int VEC, bool BWD>
-__global__ __launch_bounds__(256) void softmax_finish_kernel(EngineArgs A) {
-    const int w = wave_id();
-    if (w >= A.sch.n_seg) return;
-    const GeomDev& geo = A.geo;
-    const Lanes ln = lanes_of(geo);
-    const int g = ln.g, lig = ln.lig;
-    const int64_t D = (int64_t)geo.NV * VEC;
-    const int4 sg = A.csr.seg[A.csr.seg_order[w]];
-    const double* R = reinterpret_cast<const double*>(A.partial) + ((int64_t)A.sch.n_seg + sg.w) * 2 * D;
-    for (int ch = 0; ch < geo.nchunk; ++ch) {
-        const int j = ch * geo.L + lig;
         const bool active = j < geo.NV;
         const int col0 = active ? j * VEC : 0;
         float mx[VEC];
         double sum[VEC];
 #pragma unroll
-        for (int i = 0; i < VEC; ++i) {
-            mx[i] = (float)R[col0 + i];
-            sum[i] = R[D + col0 + i];
+        for (int i = 0; i < VEC; ++i) { mx[i] = -INFINITY; sum[i] = 0.0; }
+        if (!BWD) {
+            softmax_pass_online<T, VEC>(A, b, e, start, stride, col0, mx, sum);
+            for (int s = geo.L; s < WAVE; s <<= 1)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i)
+                    softmax_merge(mx[i], sum[i], __shfl_xor(mx[i], s, WAVE), shfl_xor_d(sum[i], s));
+        } else {
+            softmax_pass_dot<T, VEC>(A, b, e, start, stride, col0, sum);
+            for (int s = geo.L; s < WAVE; s <<= 1)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) sum[i] += shfl_xor_d(sum[i], s);
         }
-        softmax_pass_write<T, VEC>(A, sg.y, sg.z, g, geo.G, col0, active, mx, sum, BWD);
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            __syncthreads();  // the previous column's readers are done
+            if (ln.g == 0) {
+                smx[wv][ln.lig] = mx[i];
+                ssum[wv][ln.lig] = sum[i];
+            }
+            __syncthreads();
+            float m = smx[0][ln.lig];
+            double t = ssum[0][ln.lig];
+            for (int k = 1; k < HUB_WAVES; ++k) {
+                if (!BWD) softmax_merge(m, t, smx[k][ln.lig], ssum[k][ln.lig]);
+                else t += ssum[k][ln.lig];
+            }
+            mx[i] = m;
+            sum[i] = t;
+        }
+        softmax_pass_write<T, VEC>(A, b, e, start, stride, col0, active, mx, sum, BWD);
     }
 }
 
-
 hipError_t launch_softmax(const EngineArgs& a, int dtype, int vec, bool backward, hipStream_t s) {
-    if (a.sch.w_small_end <= 0) return hipSuccess;
-    dim3 grid(blocks_for_waves(a.sch.w_small_end)), block(WAVE * WPB);
-    dim3 fgrid(blocks_for_waves(a.sch.n_seg));
-    dim3 rgrid(blocks_for_waves((a.sch.n_hub + a.geo.G - 1) / a.geo.G));
-    // pass over all rows (hub segments leave partials), then for hub rows the
-    // per-row combine and the write pass of each segment
+    const int64_t rest = (int64_t)a.sch.w_small_end - a.sch.n_seg;  // waves after the hub segments
+    // a block per hub row, then the other rows
     auto run = [&](auto tv, auto vv, auto bv) {
         using T = decltype(tv);
         constexpr int V = decltype(vv)::value;
         constexpr bool B = decltype(bv)::value;
-        hipLaunchKernelGGL((softmax_kernel<T, V, B>), grid, block, 0, s, a);
-        if (a.sch.n_seg > 0) {
-            hipLaunchKernelGGL((softmax_rows_kernel<V, B>), rgrid, block, 0, s, a);
-            hipLaunchKernelGGL((softmax_finish_kernel<T, V, B>), fgrid, block, 0, s, a);
-        }
+        if (a.sch.n_hub > 0)
+            hipLaunchKernelGGL((softmax_hub_kernel<T, V, B>), dim3(a.sch.n_hub), dim3(WAVE * HUB_WAVES), 0, s, a);
+        if (rest > 0) hipLaunchKernelGGL((softmax_kernel<T, V, B>), dim3(blocks_for_waves(rest)), dim3(WAVE * WPB), 0, s, a);
     };
     using BT = std::true_type;
     using BF = std::false_type;
