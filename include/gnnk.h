@@ -236,11 +236,13 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
  * scores): for each destination v and column c,
  *   out[e, c] = exp(score[e, c] - max) / sum over in-edges of v of exp(. - max).
  * score and out: num_edges rows, same shape.  Edges of a destination with one
- * in-edge get exactly 1. */
+ * in-edge get exactly 1.  Uses no scratch memory of the handle (a destination
+ * with many in-edges is reduced within one workgroup). */
 gnnk_status edge_softmax(gnnk_graph_t g, const gnnk_tensor* score, gnnk_tensor* out, hipStream_t stream);
 
 /* grad_score[e] = out[e] * (grad_out[e] - sum over in-edges e' of dst(e) of
- * out[e'] * grad_out[e']), where out is the softmax result. */
+ * out[e'] * grad_out[e']), where out is the softmax result.  No scratch
+ * memory, as for edge_softmax. */
 gnnk_status edge_softmax_backward(gnnk_graph_t g, const gnnk_tensor* out, const gnnk_tensor* grad_out,
                                   gnnk_tensor* grad_score, hipStream_t stream);
 
