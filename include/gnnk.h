@@ -81,7 +81,7 @@ typedef enum { GNNK_SUM = 0, GNNK_MEAN = 1, GNNK_MAX = 2, GNNK_MIN = 3 } gnnk_re
 typedef enum { GNNK_SRC = 0, GNNK_EDGE = 1, GNNK_DST = 2 } gnnk_target;
 
 /* A dense (rows, heads, feat) tensor, row-major, with a row stride in
- * elements (>= heads * feat, < 2^31).  Broadcasting (Appendix D's multi-head forms):
+ * elements (>= heads * feat, < 2^31).  Broadcasting (Appendix E's multi-head forms):
  * an operand may be (H, F), (H, 1) or (1, 1) against an (H, F) message. */
 typedef struct {
     void* data;
@@ -110,7 +110,7 @@ typedef struct {
 
 /* ------------------------------------------------------------------------ */
 /* Graph structure (Section 4.1: CSR for g-SpMM forward, the reverse graph's
- * CSR for backward, edge ids kept; Appendix A, definition of the reverse
+ * CSR for backward, edge ids kept; Appendix B, definition of the reverse
  * graph).  A handle holds the in-CSR (rows = destinations), the out-CSR of
  * the reverse graph (rows = sources, with the original edge ids), in- and
  * out-degrees, rows sorted by degree for scheduling, and the segment tables
@@ -201,12 +201,12 @@ gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_
  *   out[e] = op(lhs[t_l(e)], rhs[t_r(e)]) for every edge (u, e, v),
  * t(e) being u, e or v by the operand's target.  ADD/SUB/MUL/DIV are single
  * fp32 operations; DOT is the fp64-accumulated inner product over the feature
- * dimension, giving (E, H, 1) (the per-head attention score of Appendix D);
+ * dimension, giving (E, H, 1) (the per-head attention score of Appendix E);
  * COPY_LHS / COPY_RHS copy one operand.  out: num_edges rows. */
 gnnk_status gsddmm(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
                    const gnnk_tensor* rhs, gnnk_target rhs_target, gnnk_tensor* out, hipStream_t stream);
 
-/* Gradients of gspmm (Theorem 1; Appendix A, the lemma on dL/dW of g-SpMM and
+/* Gradients of gspmm (Theorem 1; Appendix B, the lemma on dL/dW of g-SpMM and
  * lemma complex_dspmm_dx).  With g'_e = grad_out[v] scaled by d rho/d m_e
  * (1 for SUM, 1/deg(v) for MEAN, for MAX/MIN 1 iff e is arg_rhs[v]):
  *   grad_lhs[u] = sum over out-edges (u, e, v) of g'_e * d phi/d lhs   (a
@@ -223,7 +223,7 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
                            const gnnk_tensor* grad_out, gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs,
                            hipStream_t stream);
 
-/* Gradients of gsddmm (Appendix A, the lemma on dL/dW of g-SDDMM and lemma
+/* Gradients of gsddmm (Appendix B, the lemma on dL/dW of g-SDDMM and lemma
  * rev): an operand on the source side collects over its node's out-edges
  * (reverse graph), on the destination side over its in-edges, on the edge side
  * from its own edge.  grad_out: num_edges rows of the output shape.
@@ -232,7 +232,7 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
                             const gnnk_tensor* rhs, gnnk_target rhs_target, const gnnk_tensor* grad_out,
                             gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs, hipStream_t stream);
 
-/* Edge softmax (the attention normalisation applied to Appendix D's edge
+/* Edge softmax (the attention normalisation applied to Appendix E's edge
  * scores): for each destination v and column c,
  *   out[e, c] = exp(score[e, c] - max) / sum over in-edges of v of exp(. - max).
  * score and out: num_edges rows, same shape.  Edges of a destination with one
@@ -252,7 +252,7 @@ gnnk_status edge_leaky_relu(const gnnk_tensor* x, gnnk_tensor* y, float slope, h
 gnnk_status edge_leaky_relu_backward(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* dx, float slope,
                                      hipStream_t stream);
 
-/* Fused graph attention: the multi-head attention layer of Appendix D (a
+/* Fused graph attention: the multi-head attention layer of Appendix E (a
  * g-SDDMM u_add_v producing per-head edge scores, leaky ReLU, softmax over
  * the in-edges of each destination, then a g-SpMM u_mul_e/sum) in one pass
  * over each destination's in-edges, without writing the scores:

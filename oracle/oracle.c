@@ -9,7 +9,7 @@
  *   - g-SpMM:   z_v = rho{ phi(x_u, w_e) : (u, e, v) in E }, a reduction over
  *               the in-edges of v (Section 3, definition of generalized SpMM);
  *   - gradients: the chain-rule sums in the proofs of the lemmas behind
- *               Theorem 1 (Appendix A): dX sums over the out-edges of u (the
+ *               Theorem 1 (Appendix B): dX sums over the out-edges of u (the
  *               reverse graph), dY over the in-edges of v, dW per edge.
  * Edges of a node are visited in ascending edge id.  Sums are taken in double
  * and rounded once to the output type (fp32: one IEEE rounding; bf16: to fp32,
@@ -156,7 +156,7 @@ int oracle_degrees(const or_graph* g, int64_t* in_deg, int64_t* out_deg) {
 
 /* In-CSR (rows = destinations, indices = sources) or, with reverse != 0, the
  * CSR of the reverse graph (rows = sources, indices = destinations); eids
- * keep the original edge ids (Appendix A, definition of the reverse graph). */
+ * keep the original edge ids (Appendix B, definition of the reverse graph). */
 int oracle_csr(const or_graph* g, int reverse, int64_t* indptr, int32_t* indices, int32_t* eids) {
     if (!graph_ok(g)) return -1;
     adj a;
@@ -302,7 +302,7 @@ int oracle_gsddmm(const or_graph* g, int op, const or_tensor* lhs, int lhs_targe
 }
 
 /* ------------------------------------------------------------------------ */
-/* g-SpMM backward (Appendix A: the lemma on dL/dW of g-SpMM and lemma      */
+/* g-SpMM backward (Appendix B: the lemma on dL/dW of g-SpMM and lemma      */
 /* complex_dspmm_dx).  With g'_{v,e} = dL/dz_v * d rho / d m_e:              */
 /*   dL/dx_u = sum over out-edges (u, e, v) of g'_{v,e} * d phi / d x_u      */
 /*   dL/dw_e = g'_{v,e} * d phi / d w_e                                      */
@@ -415,7 +415,7 @@ int oracle_gspmm_backward(const or_graph* g, int op, int reduce, const or_tensor
 }
 
 /* ------------------------------------------------------------------------ */
-/* g-SDDMM backward (Appendix A: the lemma on dL/dW of g-SDDMM and lemma     */
+/* g-SDDMM backward (Appendix B: the lemma on dL/dW of g-SDDMM and lemma     */
 /* rev).  An operand on the source side collects over the out-edges of its   */
 /* node, on the destination side over the in-edges, on the edge side from    */
 /* its own edge only.                                                        */

@@ -7,7 +7,7 @@
  * includes, links or calls it, and it includes nothing from the GPU library.
  *
  * Everything here is a plain single-threaded loop over the definitions of
- * Section 3 (g-SDDMM and g-SpMM) and Appendix A (Theorem 1 and its lemmas,
+ * Section 3 (g-SDDMM and g-SpMM) and Appendix B (Theorem 1 and its lemmas,
  * the reverse graph).  Floating point is accumulated in double and rounded
  * once to the output type.
  *

@@ -1,5 +1,5 @@
 // Graph formats built on the device (Section 4.1: the in-CSR for g-SpMM, the
-// reverse graph's CSR for the backward pass; Appendix A: the reverse graph
+// reverse graph's CSR for the backward pass; Appendix B: the reverse graph
 // keeps the edge ids).
 //
 // A CSR is a stable sort of the edge list by row key: sorting the pairs

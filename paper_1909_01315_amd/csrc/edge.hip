@@ -1,6 +1,6 @@
 // Edge-parallel (COO) walks: the load-balanced alternative to the row
 // engine (Table 1 of the paper: both are valid for commutative and
-// associative reducers; Appendix D compares them).  The positions of a CSR
+// associative reducers; Appendix E compares them).  The positions of a CSR
 // are cut into sub-chunks of sub_edges consecutive positions, one per lane
 // group, so every lane group handles the same number of edges whatever the
 // degree distribution.  The row of a position comes from the COO row array.

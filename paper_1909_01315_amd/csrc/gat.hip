@@ -1,5 +1,5 @@
 // Fused graph attention: the u_add_v -> leaky ReLU -> edge softmax ->
-// u_mul_e/sum chain (the multi-head attention layer of Appendix D, written
+// u_mul_e/sum chain (the multi-head attention layer of Appendix E, written
 // there as a g-SDDMM followed by a g-SpMM) in one pass over each
 // destination's in-edges:
 //

@@ -1,5 +1,5 @@
 // Graph handles of the gnnk library: the in-CSR, the reverse graph's CSR with
-// the original edge ids (Appendix A, definition of the reverse graph), the
+// the original edge ids (Appendix B, definition of the reverse graph), the
 // degree arrays, rows sorted by degree, and the segment tables of hub rows.
 //
 // Every structure is built on the device (build.hip: stable radix sorts, so

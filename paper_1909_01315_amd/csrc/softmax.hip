@@ -1,5 +1,5 @@
 // Edge softmax over the in-edges of each destination, per column (the
-// attention normalisation applied to the per-edge scores of Appendix D), and
+// attention normalisation applied to the per-edge scores of Appendix E), and
 // its backward.  Forward: one pass keeps the running max m and the fp64 sum
 // of exp(s - m), rescaled whenever m grows; a second pass writes
 // a = exp(s - max) / sum.  Backward: S = sum of a * g in fp64, then

@@ -11,7 +11,7 @@ the aggregation layers of the paper's experiments built from them:
   GraphConv     GCN, symmetric normalisation, u_mul_e/sum
   SAGEConv      GraphSAGE with mean aggregation, copy_u/mean
   GATConv       multi-head attention: u_add_v -> leaky ReLU -> edge softmax ->
-                u_mul_e/sum (the chain of Appendix D)
+                u_mul_e/sum (the chain of Appendix E)
   RelGraphConv  R-GCN aggregation: per-relation transformed source rows
                 gathered by (relation, source) on a bipartite encoding and
                 summed with 1/in-degree-per-relation weights
@@ -217,7 +217,7 @@ class SAGEConv(torch.nn.Module):
 class GATConv(torch.nn.Module):
     """Multi-head graph attention: per-head scores el[u] + er[v] (u_add_v),
     leaky ReLU, softmax over in-edges, and the attention-weighted sum of the
-    projected source features (u_mul_e/sum) -- the chain of Appendix D."""
+    projected source features (u_mul_e/sum) -- the chain of Appendix E."""
 
     def __init__(self, in_feats: int, out_feats: int, num_heads: int, negative_slope: float = 0.2,
                  fused: bool = False):
@@ -246,7 +246,7 @@ class GATConv(torch.nn.Module):
 
 
 class RelGraphConv(torch.nn.Module):
-    """R-GCN aggregation (the experiment appendix's formula): for each
+    """R-GCN aggregation (the formula of Appendix D, experiment configurations): for each
     relation r, sum over r-edges into v of W_r h_u / |N_r(v)|, plus a self
     term.  The per-relation products W_r h_u are computed densely for all
     (r, u) and gathered by the g-SpMM on the bipartite graph whose source id

@@ -1,7 +1,7 @@
 """Sensitivity of the two primitives to graph shape, feature width and
-parallelisation (the kernel study of Appendix D, on MI355X).
+parallelisation (the kernel study of Appendix E, on MI355X).
 
-Appendix D of the paper compares node-parallel and edge-parallel g-SpMM and
+Appendix E of the paper compares node-parallel and edge-parallel g-SpMM and
 g-SDDMM over CSR and COO while the per-head feature width F varies, on a
 constant-degree (k-NN-like) graph and on power-law graphs; its figure values
 are not printed in the text, so this is a characterisation, not a

@@ -182,7 +182,7 @@ def uniform_graph(seed: int, n_src: int, n_dst: int, n_edges: int, self_loops: b
 
 def knn_graph(seed: int, n: int, k: int, name: str = "knn") -> Graph:
     """Constant in-degree graph (a k-nearest-neighbour graph's shape): every
-    node receives k edges from uniform random sources (Appendix D's
+    node receives k edges from uniform random sources (Appendix E's
     sensitivity study contrasts such graphs with power-law ones)."""
     lib = _load()
     src = np.empty(n * k, dtype=np.int32)

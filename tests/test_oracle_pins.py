@@ -7,7 +7,7 @@ SDDMM W = A .* (X X^T)), the incidence-matrix form of the definitions
 brute force on tiny graphs, central finite differences of the fp64 oracle
 (Theorem 1's gradients), the reverse-graph identity of Theorem 1, invariants
 (degree counts, softmax normalisation and shift invariance), permutation
-invariance, the R-GCN aggregation formula of the experiment appendix, and
+invariance, the R-GCN aggregation formula of Appendix D (experiment configurations), and
 library routines (numpy/scipy/torch) for CSR construction, softmax and bf16
 rounding.
 """
@@ -505,7 +505,7 @@ def test_relabelling_permutes_outputs():
 
 
 # ---------------------------------------------------------------------------
-# P7: R-GCN aggregation (experiment appendix): sum_r D_r^-1 A_r X_r
+# P7: R-GCN aggregation (Appendix D, experiment configurations): sum_r D_r^-1 A_r X_r
 
 
 def test_rgcn_encoding_matches_dense_formula():
