@@ -53,8 +53,10 @@ struct Online {
     }
     // add one edge with score s and source row x
     __device__ __forceinline__ void add(float s, const float* x) {
+        // a score of -inf adds nothing; while the running max is still -inf
+        // too, -inf - (-inf) would give NaN
         const float mn = fmaxf(m, s);
-        const double f = (double)exp_le0(fminf(m, s) - mn);
+        const double f = mn == -INFINITY ? 0.0 : (double)exp_le0(fminf(m, s) - mn);
         const bool up = s > m;
         const double c_old = up ? f : 1.0;
         const double c_new = up ? 1.0 : f;

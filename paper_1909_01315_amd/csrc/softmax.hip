@@ -46,8 +46,10 @@ template <int VEC>
 __device__ __forceinline__ void online_step(float* mx, double* sum, const float* s) {
 #pragma unroll
     for (int i = 0; i < VEC; ++i) {
+        // a score of -inf (a masked edge) adds exp(-inf) = 0; while the
+        // running max is still -inf too, -inf - (-inf) would give NaN
         const float mn = fmaxf(mx[i], s[i]);
-        const double f = (double)exp_le0(fminf(mx[i], s[i]) - mn);
+        const double f = mn == -INFINITY ? 0.0 : (double)exp_le0(fminf(mx[i], s[i]) - mn);
         sum[i] = s[i] > mx[i] ? sum[i] * f + 1.0 : sum[i] + f;
         mx[i] = mn;
     }

@@ -40,17 +40,31 @@ def edges_of_rows(indptr, rows, cap=200000):
 
 
 def argmax_scatter_check(w, X, dm, ae_gpu, dXm_gpu, kind, name, seed=7):
-    """The masked reverse g-SpMM of max backward, checked on sampled sources.
-    The oracle's own arg edges are computed for every destination those
-    sources' out-edges reach (the only ones the backward reads)."""
+    """The masked reverse g-SpMM of max backward, checked on sampled sources
+    of every role of the reverse walk: the three largest out-degree sources
+    (hub segments, each reaching a large share of all destinations), sources
+    of out-degree 65..seg_edges (one wavefront per row) and sources of
+    out-degree 1..16 (a lane group per row).  The oracle's own arg edges are
+    computed for every destination those sources' out-edges reach (the only
+    ones the backward reads)."""
     rng = np.random.default_rng(seed)
-    cand = np.nonzero((w.outdeg > 0) & (w.outdeg <= 16))[0]
-    srcs = np.sort(rng.choice(cand, size=min(12, cand.size), replace=False)).astype(np.int64)
-    dsts = np.unique(w.sg.dst[np.isin(w.sg.src, srcs)]).astype(np.int64)
+    seg = w.g.info()["seg_edges"]
+    top = np.argsort(-w.outdeg, kind="stable")[:3]
+    assert np.all(w.outdeg[top] > seg)
+    big = np.nonzero((w.outdeg > 64) & (w.outdeg <= seg))[0]
+    small = np.nonzero((w.outdeg > 0) & (w.outdeg <= 16))[0]
+    srcs = np.unique(np.concatenate([top, rng.choice(big, size=min(4, big.size), replace=False),
+                                     rng.choice(small, size=min(12, small.size), replace=False)])).astype(np.int64)
+    picked = np.zeros(w.sg.n_src, dtype=bool)
+    picked[srcs] = True
+    dsts = np.unique(w.sg.dst[picked[w.sg.src]]).astype(np.int64)
+    log(f"{name}: {srcs.size} sources (out-degrees {sorted(w.outdeg[srcs].tolist())[-4:]} at the top) reach "
+        f"{dsts.size} destinations")
     _, _, ae_rows = orc.gspmm(w.o, "copy_lhs", "max", X, rows=dsts)
     assert_exact(host(ae_gpu)[dsts], ae_rows, f"{name} arg edges")
     ae_full = np.full((w.sg.n_dst,) + ae_rows.shape[1:], -1, np.int32)
     ae_full[dsts] = ae_rows
+    del ae_rows
     gl, _ = orc.gspmm_backward(w.o, "copy_lhs", "max", X, None, dm, arg_e=ae_full, sel=srcs)
     assert_close(host(dXm_gpu)[srcs], gl, kind=kind, name=name)
 
@@ -181,11 +195,30 @@ def test_c3_fused_gat(c3):
     assert_close(host(out)[c3.rows], ref, name="c3 fused attention output")
 
 
+def fused_grad_bound(o, a, da, lk, dst, src, n_dst, n_src, rows):
+    """2^-20 times the sum of the magnitudes of the terms each fused
+    attention gradient adds up, t_e = a_e (|da_e| + |S_v|) lk_e, summed over
+    the in-edges of each destination (d er) or the out-edges of each source
+    (d el), for the listed rows: the error bound of a sum of terms whose
+    attention factor the fused path recomputes in fp32 (the derivation is
+    with the tolerance of the random cases, tests/test_gpu_random_cases.py).
+    a, da, lk: (E, H) fp64."""
+    H = a.shape[1]
+    S = np.stack([np.bincount(dst, weights=a[:, h] * da[:, h], minlength=n_dst) for h in range(H)], 1)
+    out = np.zeros((rows.size, H))
+    for h in range(H):
+        t = a[:, h] * (np.abs(da[:, h]) + np.abs(S[dst, h])) * lk[:, h]
+        out[:, h] = np.bincount(src, weights=t, minlength=n_src)[rows]
+    return 2.0 ** -20 * out
+
+
 def test_c3_fused_gat_backward(c3):
-    """gat_aggregate_backward on c3 (hub rows in both directions): d feat on
-    sampled sources and d er on sampled destinations against the oracle's
-    chain in fp64; d el against the unfused GPU chain (each of its steps
-    checked at this size above) at the chain tolerance."""
+    """gat_aggregate_backward on c3 (hub rows in both directions) against the
+    oracle's chain of the four gradients in fp64: d feat on sampled sources
+    and d er on sampled destinations at the fp32 tolerance; d el on sampled
+    sources (the three largest out-degree sources among them, which reach
+    most destinations) at the fp32 tolerance or the bound of its terms,
+    whichever is wider (the attention the fused path recomputes is fp32)."""
     N, E = c3.sg.n_dst, c3.sg.n_edges
     fs = synth.feat_seed(3)
     X = synth.normal(fs, "X", (N, 8, 16))
@@ -195,35 +228,33 @@ def test_c3_fused_gat_backward(c3):
     Xd, eld, erd, dzd = dev(X), dev(el), dev(er), dev(dz)
     _, st = gnnk.gat_aggregate(c3.g, Xd, eld, erd, 0.2, want_stats=True)
     gf, gl, gr = gnnk.gat_aggregate_backward(c3.g, Xd, eld, erd, 0.2, st, dzd)
-    log("c3 fused attention backward: oracle chain in fp64 on sampled rows")
-    X64, el64, er64, dz64 = (a.astype(np.float64) for a in (X, el, er, dz))
+    gf, gl, gr = host(gf), host(gl), host(gr)
+    del Xd, eld, erd, dzd, st
+    log("c3 fused attention backward: oracle chain in fp64 on every edge")
+    X64, el64, er64, dz64 = (v.astype(np.float64) for v in (X, el, er, dz))
     s = orc.gsddmm(c3.o, "add", el64, "u", er64, "v")
     a = orc.edge_softmax(c3.o, orc.leaky_relu(s, 0.2))
     rf, _ = orc.gspmm_backward(c3.o, "mul", "sum", X64, a, dz64, want_rhs=False, sel=c3.srows)
-    assert_close(host(gf)[c3.srows], rf, name="c3 fused d feat")
-    er_rows = edges_of_rows(c3.indptr, c3.rows, cap=E)
-    full = np.zeros((E, 8, 1), np.float64)
-    full[er_rows] = orc.gsddmm(c3.o, "dot", X64, "u", dz64, "v", edges=er_rows)
-    ds2, eids = orc.edge_softmax_backward(c3.o, a, full, rows=c3.rows)
-    del a
-    full[:] = 0.0
-    full[eids] = orc.leaky_relu_backward(s[eids], ds2, 0.2)
+    assert_close(gf[c3.srows], rf, name="c3 fused d feat")
+    da = orc.gsddmm(c3.o, "dot", X64, "u", dz64, "v")
+    ds = orc.leaky_relu_backward(s, orc.edge_softmax_backward(c3.o, a, da), 0.2)
+    _, rr = orc.gsddmm_backward(c3.o, "add", el64, "u", er64, "v", ds, want_lhs=False, sel=c3.rows)
+    assert_close(gr[c3.rows], rr, name="c3 fused d er")
+    srcs = np.unique(np.concatenate([c3.srows, np.argsort(-c3.outdeg, kind="stable")[:3]])).astype(np.int64)
+    rl, _ = orc.gsddmm_backward(c3.o, "add", el64, "u", er64, "v", ds, want_rhs=False, sel=srcs)
+    del ds
+    lk = np.where(s[:, :, 0] > 0, 1.0, 0.2)
     del s
-    _, rr = orc.gsddmm_backward(c3.o, "add", el64, "u", er64, "v", full, want_lhs=False, sel=c3.rows)
-    del full
-    assert_close(host(gr)[c3.rows], rr, name="c3 fused d er")
-    # d el: the unfused chain on the GPU
-    sg_ = gnnk.gsddmm(c3.g, "add", eld, "u", erd, "v")
-    au = gnnk.edge_softmax(c3.g, gnnk.edge_leaky_relu(sg_, 0.2))
-    _, da = gnnk.gspmm_backward(c3.g, "mul", "sum", Xd, au, dzd, want_lhs=False)
-    ds = gnnk.edge_leaky_relu_backward(sg_, gnnk.edge_softmax_backward(c3.g, au, da), 0.2)
-    del au, da
-    ul, _ = gnnk.gsddmm_backward(c3.g, "add", eld, "u", erd, "v", ds, want_rhs=False)
-    del ds, sg_
-    ref = host(ul).astype(np.float64)
-    got = host(gl).astype(np.float64)
-    tol = 1e-4 * np.abs(ref) + 1e-5 * np.abs(ref).max()
-    assert np.all(np.abs(got - ref) <= tol), f"c3 fused d el: max err {np.abs(got - ref).max()}"
+    bound = fused_grad_bound(c3.o, a[:, :, 0], da[:, :, 0], lk, c3.sg.dst, c3.sg.src, N, N, srcs)
+    del a, da, lk
+    got = gl[srcs].astype(np.float64).reshape(rl.shape)
+    ref = rl.astype(np.float64)
+    tol = np.maximum(1e-6 + 1e-5 * np.abs(ref), bound[:, :, None])
+    bad = ~(np.abs(got - ref) <= tol)
+    assert not bad.any(), f"c3 fused d el: {int(bad.sum())} of {bad.size} out of tolerance, max err " \
+                          f"{np.abs(got - ref).max():.3g}"
+    log(f"c3 fused d el: {int((np.abs(got - ref) > 1e-6 + 1e-5 * np.abs(ref)).sum())} of {ref.size} values "
+        f"outside the plain fp32 tolerance, inside the term bound")
 
 
 def test_c3_sage_mean_and_max(c3):

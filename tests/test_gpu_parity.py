@@ -291,6 +291,69 @@ def test_edge_softmax_c1(c1, H):
     assert_close(ds, orc.edge_softmax_backward(c1.o, a, gout), name="softmax backward")
 
 
+def assert_close_nan(gpu, ref, name):
+    """NaN exactly where the oracle has NaN (a destination whose scores are
+    all -inf: 0 / 0), the fp32 tolerance elsewhere"""
+    g = host(gpu).reshape(np.shape(ref)) if isinstance(gpu, torch.Tensor) else gpu
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(g), nan), f"{name}: NaN positions differ"
+    assert_close(np.where(nan, 0.0, g).astype(np.float32), np.where(nan, 0.0, ref).astype(np.float32), name=name)
+
+
+@pytest.mark.parametrize("seg", [0, 64])
+@pytest.mark.parametrize("H", [1, 4])
+def test_edge_softmax_masked_scores(c2, seg, H):
+    """Scores of -inf (masked edges) get attention 0; a destination with
+    every score masked gets NaN (0 / 0) as the definition gives.  seg 64
+    sends the rows of more than 64 in-edges to the hub-row blocks."""
+    gnnk.set_option("seg_edges", seg)
+    p = Pair(c2.o.src, c2.o.dst, c2.o.n_src, c2.o.n_dst)
+    E = c2.o.n_edges
+    rng = np.random.default_rng(4400 + H)
+    s = feats(synth.feat_seed(2), f"ms{H}", (E, H, 1))
+    s[rng.random((E, H, 1)) < 0.4] = -np.inf
+    ind = np.bincount(c2.o.dst, minlength=c2.o.n_dst)
+    ptr = np.concatenate([[0], np.cumsum(ind)])
+    big = np.argsort(-ind, kind="stable")[:3]
+    for v in big[:2]:                    # whole rows masked, one a hub row
+        s[ptr[v]:ptr[v + 1]] = -np.inf
+    v = big[2]                           # a hub row with one finite score in its middle
+    s[ptr[v]:ptr[v + 1]] = -np.inf
+    s[(ptr[v] + ptr[v + 1]) // 2] = 0.5
+    ref = orc.edge_softmax(c2.o, s)
+    assert np.isnan(ref).any() and (ref == 0.0).any()
+    assert_close_nan(gnnk.edge_softmax(p.g, dev(s)), ref, name="masked softmax")
+    assert_close(gnnk.edge_softmax(p.g, dev(s))[ptr[v]:ptr[v + 1]], ref[ptr[v]:ptr[v + 1]], name="one finite score")
+    # the backward of the masked attention (zeros, and no NaN rows)
+    a = np.where(np.isnan(ref), 0.0, ref).astype(np.float32)
+    gout = feats(synth.grad_seed(2), f"mg{H}", (E, H, 1))
+    assert_close(gnnk.edge_softmax_backward(p.g, dev(a), dev(gout)), orc.edge_softmax_backward(c2.o, a, gout),
+                 name="masked softmax backward")
+
+
+@pytest.mark.parametrize("seg", [0, 64])
+def test_gat_aggregate_masked_sources(c2, seg):
+    """Fused attention with el = -inf for some (source, head) pairs: every
+    out-edge of such a source scores -inf in that head (attention 0); a
+    destination whose in-edges are all masked in a head gets NaN there, as
+    the oracle's chain gives."""
+    gnnk.set_option("seg_edges", seg)
+    p = Pair(c2.o.src, c2.o.dst, c2.o.n_src, c2.o.n_dst)
+    N, H, F = c2.o.n_src, 4, 8
+    fs = synth.feat_seed(2)
+    feat = feats(fs, "mfeat", (N, H, F))
+    el = feats(fs, "mel", (N, H, 1))
+    er = feats(fs, "mer", (c2.o.n_dst, H, 1))
+    el[np.random.default_rng(4500).random((N, H, 1)) < 0.5] = -np.inf
+    sc = orc.leaky_relu(orc.gsddmm(c2.o, "add", el, "u", er, "v"), 0.2)
+    a = orc.edge_softmax(c2.o, sc)
+    ref = orc.gspmm(c2.o, "mul", "sum", feat, a)
+    assert np.isnan(ref).any()
+    out, attn = gnnk.gat_aggregate(p.g, dev(feat), dev(el), dev(er), 0.2, want_attn=True)
+    assert_close_nan(attn, a, name="masked fused attention")
+    assert_close_nan(out, ref, name="masked fused output")
+
+
 def test_leaky_relu_bit_exact(c1):
     x = feats(S1, "lx", (c1.o.n_edges, 4, 1))
     x[:7] = 0.0

@@ -2,10 +2,10 @@
 in-edges, destinations whose degree sits just below, at and above the
 segment sizes (64, 256, 2048), empty destinations, rows wider than one
 pass of 64 lanes, edges in destination order and shuffled (edge ids through
-the map), fp32 and bf16, against the oracle.  The forward check is relative
-(a row of 40,000 edges has values near 2.5e-5, below the absolute part of
-the usual tolerance); the backward bound comes from the magnitudes of the
-terms of S = sum of a * g."""
+the map), fp32 and bf16, against the oracle at the tolerances of
+tests/_gpu.py.  A row of 40,000 edges has values near 2.5e-5, below the
+absolute part of the fp32 tolerance, so the forward is also held to 1e-5
+relative to each value alone."""
 import functools
 
 import numpy as np
@@ -71,20 +71,15 @@ def test_softmax_hub_rows(shuffled, seg, H, F, bf16):
         assert_close(a_gpu, a, kind="bf16", name="softmax bf16")
         assert_close(ds_gpu, ref_ds, kind="bf16", name="softmax backward bf16")
         return
-    # forward: relative to each value
+    assert_close(a_gpu, a, name="softmax")
+    assert_close(ds_gpu, ref_ds, name="softmax backward")
+    # forward, relative to each value alone: the exponential is within a few
+    # units of 2^-24 times (1 + |s - max|) of exp (|s - max| < 10 here)
     ga, ra = as_f64(host(a_gpu)).reshape(a.shape), as_f64(a)
     err = np.abs(ga - ra)
-    assert np.all(err <= 2e-5 * np.abs(ra)), f"softmax: max rel err {np.max(err / np.maximum(np.abs(ra), 1e-300)):.3g}"
+    assert np.all(err <= 1e-5 * np.abs(ra)), f"softmax: max rel err {np.max(err / np.maximum(np.abs(ra), 1e-300)):.3g}"
     # every non-empty row sums to 1
     sums = np.zeros((N, H, F))
     np.add.at(sums, dst, ga)
     rows = np.unique(dst)
     assert np.allclose(sums[rows], 1.0, rtol=0, atol=1e-4)
-    # backward: ds = a (g - S), S = sum over the row of a * g
-    a64, g64 = as_f64(a), as_f64(g)
-    t_abs = np.zeros((N, H, F))
-    np.add.at(t_abs, dst, np.abs(a64 * g64))
-    bound = 2e-5 * a64 * (np.abs(g64) + t_abs[dst]) + 1e-30
-    gd = as_f64(host(ds_gpu)).reshape(ref_ds.shape)
-    err = np.abs(gd - as_f64(ref_ds))
-    assert np.all(err <= bound), f"softmax backward: max err / bound {np.max(err / bound):.3g}"
