@@ -21,9 +21,12 @@
  *    the caller; the library never frees them.  A NULL tensor pointer means
  *    "absent" where the argument is documented nullable.
  *  - Work is enqueued on `stream` and runs asynchronously; calls return before
- *    the kernels finish.  Only graph_create_* and graph_validate synchronise,
- *    and a call that has to grow the handle's scratch buffer (its first call
- *    of a larger kind; warm up once before capturing a HIP graph).
+ *    the kernels finish.  Only graph_create_* and graph_validate synchronise.
+ *    No call allocates device memory (Section 4.2: the framework allocates):
+ *    the graph's derived arrays live in a workspace the caller provides, and
+ *    the scratch memory some compute calls need is lent by the caller per
+ *    stream (graph_attach_scratch).  A sequence of compute calls can
+ *    therefore be captured into a HIP graph as it is.
  *  - Outputs are fully overwritten, never accumulated into.  Inputs may alias
  *    each other; outputs must not alias inputs or each other.
  *  - Edge tensors are indexed by edge id.  Node tensors by node id.
@@ -35,8 +38,8 @@
  *    gradient of an operand broadcast over features) wider than one pass of a
  *    wavefront (64 lanes of 4 fp32 or 8 bf16 values) adds its passes in fp64
  *    in order, and per-head sums of such rows run as slices of heads.
- *  - Calls that use the same graph handle must be ordered (one stream, or
- *    synchronised): the handle owns the scratch space of hub-row partials.
+ *  - A handle is immutable after creation: calls on several streams may use
+ *    it at once, each stream with its own lent scratch buffer.
  */
 #ifndef GNNK_H
 #define GNNK_H
@@ -128,7 +131,8 @@ typedef struct {
  * table.  The order never changes a result: segment partials are combined in
  * table order.
  * The call synchronises `stream` twice (after checking the input, and to read
- * back the sorted degrees) and may allocate the handle's scratch buffer. */
+ * back the sorted degrees); it allocates no device memory (its temporaries
+ * are part of the workspace). */
 
 /* Upper bound of the workspace for a graph of this size; ptr_t is the width
  * of the CSR row offsets the handle builds (either width for any size).
@@ -177,8 +181,51 @@ gnnk_status graph_csr_export(gnnk_graph_t g, int reverse, void* indptr, int32_t*
  * Returns GNNK_ERANGE if any index is out of range. */
 gnnk_status graph_validate(gnnk_graph_t g, hipStream_t stream);
 
-/* Free the handle and any scratch it allocated (not the workspace). */
+/* Free the handle (a host object; the workspace and every lent scratch
+ * buffer stay the caller's, to be released once the kernels queued on them
+ * have finished). */
 gnnk_status graph_destroy(gnnk_graph_t g);
+
+/* ------------------------------------------------------------------------ */
+/* Scratch memory of compute calls.  Some calls need device memory beyond
+ * their inputs and outputs: fp64 partial results of the segments of hub
+ * rows (g-SpMM sum/mean/max/min and their gradients, the fused attention),
+ * the winner masks of the max/min backward, the per-(destination, head)
+ * records of the fused attention backward, per-edge fp64 running sums of
+ * reductions wider than one pass of a wavefront, and the partial rows of the
+ * edge-parallel schedules.  The caller lends it, per stream: a call that
+ * needs scratch uses the buffer attached to the handle for the stream it is
+ * issued on, front to back; with none, or one too small, it returns
+ * GNNK_ENOMEM before launching anything, and gnnk_scratch_needed() tells the
+ * bytes it asked for.  Calls on one stream run in stream order and share its
+ * buffer; calls on different streams use different buffers.  The contents
+ * of a buffer need not be initialised and are not preserved between
+ * calls. */
+
+enum {
+    GNNK_SCRATCH_ARGMAX = 1,     /* include the max/min backward (winner masks: E * ceil(cols / 32) * 4 bytes) */
+    GNNK_SCRATCH_WIDE_SUMS = 2   /* include sums over more than 64 lanes of a row (E * 8 bytes) */
+};
+
+/* Bytes of scratch that any call on this handle with messages of at most
+ * max_cols columns (heads * feat) needs, under the options set now; flags
+ * add the two kinds above. */
+gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags, size_t* bytes);
+
+/* Lend buf (device memory, 256-byte aligned, `bytes` bytes) to the handle for
+ * the calls issued on `stream`, replacing any earlier buffer of that stream;
+ * buf == NULL or bytes == 0 takes the stream's buffer back.  Host-side only:
+ * no GPU work.  The caller keeps the buffer alive, unchanged by other work,
+ * until the calls queued on `stream` with it have finished (releasing it to
+ * an allocator ordered on that stream is enough).  At most 16 streams per
+ * handle (GNNK_EINVAL beyond). */
+gnnk_status graph_attach_scratch(gnnk_graph_t g, hipStream_t stream, void* buf, size_t bytes);
+
+/* Bytes of scratch the last call on this thread that returned GNNK_ENOMEM for
+ * lack of scratch asked for (0 after any other outcome).  A call that needs
+ * several parts asks for them in turn, so a call retried with that many
+ * bytes may ask for more. */
+gnnk_status gnnk_scratch_needed(size_t* bytes);
 
 /* ------------------------------------------------------------------------ */
 /* g-SpMM (Section 3, definition of generalized SpMM):
@@ -191,6 +238,8 @@ gnnk_status graph_destroy(gnnk_graph_t g);
  * MAX/MIN: messages are formed in fp32 and compared exactly; the smallest edge
  * id wins a tie.  arg_lhs (source id) and arg_rhs (edge id) are nullable dense
  * (num_dst, H, F) int32 arrays, -1 for empty destinations.
+ * Scratch: fp64 partials of hub-row segments, segments x H * F x 8 bytes
+ * (12 for MAX/MIN).
  * Errors: GNNK_EINVAL on a bad op/reduce, shapes or dtypes; GNNK_EUNSUPPORTED
  * for arg arrays with SUM/MEAN. */
 gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
@@ -236,8 +285,8 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
  * scores): for each destination v and column c,
  *   out[e, c] = exp(score[e, c] - max) / sum over in-edges of v of exp(. - max).
  * score and out: num_edges rows, same shape.  Edges of a destination with one
- * in-edge get exactly 1.  Uses no scratch memory of the handle (a destination
- * with many in-edges is reduced within one workgroup). */
+ * in-edge get exactly 1.  Uses no scratch memory (a destination with many
+ * in-edges is reduced within one workgroup). */
 gnnk_status edge_softmax(gnnk_graph_t g, const gnnk_tensor* score, gnnk_tensor* out, hipStream_t stream);
 
 /* grad_score[e] = out[e] * (grad_out[e] - sum over in-edges e' of dst(e) of
@@ -286,9 +335,8 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
  * A head must fit one pass of a wavefront, F / vec <= 64 (vec: 4 fp32 or 8
  * bf16 values per lane as F and the row strides allow; GNNK_EUNSUPPORTED
  * otherwise); rows of several heads wider than a pass run as slices of
- * heads.  Uses the handle's
- * scratch: 16 bytes per (destination, head) plus per-segment partials of
- * hub rows.  Errors: GNNK_EINVAL on shapes or dtypes. */
+ * heads.  Scratch: 16 bytes per (destination, head) plus per-segment
+ * partials of hub rows.  Errors: GNNK_EINVAL on shapes or dtypes. */
 gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
                                    const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
                                    const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,

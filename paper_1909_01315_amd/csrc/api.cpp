@@ -308,7 +308,7 @@ void set_edge_chunks(EngineArgs& A, int64_t E, const Geo& geo) {
 // for a u_mul_e/sum backward and asks for the edge gradient in this pass;
 // *fused_dw tells whether it was written (else the caller runs its g-SDDMM)
 gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& geo, int dtype, int opk,
-                         hipStream_t s, bool* fused_dw = nullptr) {
+                         hipStream_t s, Scratch& sc, bool* fused_dw = nullptr) {
     A.csr = csr_of(g, d);
     set_geo(A, geo);
     A.sch = schedule(d, geo, true);
@@ -325,8 +325,8 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
         set_edge_chunks(A, g->n_edges, geo);
         const size_t need = walk == 3 ? (size_t)d.n_rows * geo.D * 8 : (size_t)2 * A.n_sub * geo.D * 8;
         if (need > 0) {
-            A.partial = graph_scratch(g, need);
-            if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
+            A.partial = sc.take(need);
+            if (!A.partial) return scratch_fail(sc);
         }
         gnnk_status st = launch_status(launch_spmm_edge(A, g->n_edges, d.n_rows, dtype, geo.vec, opk, pk.spec, pk.gc,
                                                         walk == 3 ? 1 : 0, s),
@@ -345,8 +345,8 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
         return launch_status(launch_spmm(F, dtype, geo.vec, false, opk, SP_DYN, 0, s), "empty-row fill launch");
     }
     if (A.sch.n_seg > 0) {
-        A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 8);
-        if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
+        A.partial = sc.take((size_t)A.sch.n_seg * geo.D * 8);
+        if (!A.partial) return scratch_fail(sc);
     }
     gnnk_status st = (fused_dw && *fused_dw)
                          ? launch_status(launch_spmm_dw(A, dtype, geo.vec, pk.spec, pk.gc, s),
@@ -358,7 +358,7 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
     return st;
 }
 
-gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, int opk, hipStream_t s) {
+gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, int opk, hipStream_t s, Scratch& sc) {
     A.csr = csr_of(g, g->in);
     set_geo(A, geo);
     A.sch = schedule(g->in, geo, false);
@@ -366,8 +366,8 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
     const bool multi = A.out.reduce && geo.nchunk > 1;
     if (multi) {
         // running per-edge sums between the passes of a row wider than the wavefront
-        A.xacc = reinterpret_cast<double*>(graph_scratch(g, (size_t)g->n_edges * 8));
-        if (!A.xacc) return fail(GNNK_ENOMEM, "scratch allocation failed");
+        A.xacc = reinterpret_cast<double*>(sc.take((size_t)g->n_edges * 8));
+        if (!A.xacc) return scratch_fail(sc);
     }
     if (pick_walk(g->in, multi)) {
         set_edge_chunks(A, g->n_edges, geo);
@@ -413,16 +413,12 @@ int heads_per_slice(int Hm, int Fm, std::initializer_list<const gnnk_tensor*> al
 }
 
 }  // namespace
-}  // namespace gnnk
 
-using namespace gnnk;
-
-extern "C" {
-
-gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
-                  const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
-                  hipStream_t stream) {
-    clear_error();
+// gspmm with its scratch from `sc` (the buffer lent for the stream); checks
+// every argument before it takes scratch or launches anything
+gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                       const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
+                       hipStream_t stream, Scratch& sc) {
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
     if (op < GNNK_COPY_LHS || op > GNNK_DIV) return fail(GNNK_EINVAL, "gspmm op must be COPY_LHS..DIV");
     if (reduce < GNNK_SUM || reduce > GNNK_MIN) return fail(GNNK_EINVAL, "bad reduce");
@@ -467,21 +463,68 @@ gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_
     A.out.red = 1;
     A.out.reduce = 0;
     A.flags = (reduce == GNNK_MEAN ? F_OWN_MEAN : 0) | (reduce == GNNK_MIN ? F_IS_MIN : 0);
-    if (!cmp) return run_spmm_sum(g, g->in, A, geo, dtype_code(out), opk, stream);
+    if (!cmp) return run_spmm_sum(g, g->in, A, geo, dtype_code(out), opk, stream, sc);
     A.arg_nbr = arg_lhs;
     A.arg_edge = arg_rhs;
     A.csr = csr_of(g, g->in);
     set_geo(A, geo);
     A.sch = schedule(g->in, geo, true);
     if (A.sch.n_seg > 0) {
-        A.partial = graph_scratch(g, (size_t)A.sch.n_seg * geo.D * 12);
-        if (!A.partial) return fail(GNNK_ENOMEM, "scratch allocation failed");
+        A.partial = sc.take((size_t)A.sch.n_seg * geo.D * 12);
+        if (!A.partial) return scratch_fail(sc);
     }
     const Pick pk = pick_spmm(g, g->in, A, geo, dtype_code(out), opk, true);
     st = launch_status(launch_spmm(A, dtype_code(out), geo.vec, true, opk, pk.spec, pk.gc, stream), "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
         st = launch_status(launch_spmm_combine(A, dtype_code(out), geo.vec, true, stream), "g-SpMM combine launch");
     return st;
+}
+
+}  // namespace gnnk
+
+using namespace gnnk;
+
+extern "C" {
+
+gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                  const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
+                  hipStream_t stream) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    Scratch sc = scratch_of(g, stream);
+    return gspmm_impl(g, op, reduce, lhs, rhs, out, arg_lhs, arg_rhs, stream, sc);
+}
+
+gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags, size_t* bytes) {
+    clear_error();
+    if (!g || !bytes) return fail(GNNK_EINVAL, "NULL argument");
+    if (max_cols < 1 || max_cols > ((int64_t)1 << 31)) return fail(GNNK_EINVAL, "max_cols must be in [1, 2^31]");
+    if (flags & ~(GNNK_SCRATCH_ARGMAX | GNNK_SCRATCH_WIDE_SUMS)) return fail(GNNK_EINVAL, "unknown flags");
+    auto al = [](size_t n) { return (n + 255) / 256 * 256; };
+    const size_t C = (size_t)max_cols, E = (size_t)g->n_edges;
+    const size_t si = (size_t)g->in.n_seg, so = (size_t)g->out.n_seg;
+    // sums and their gradients: fp64 partials of hub segments (either CSR)
+    size_t need = al(std::max(si, so) * C * 8);
+    // max / min: value, edge and neighbour per segment and column
+    need = std::max(need, al(si * C * 12));
+    // fused attention: partial states of segments, and the row state of hub
+    // rows when the attention is written
+    need = std::max(need, al(si * 3 * C * 8 + (size_t)g->in.n_hub * 2 * C * 8));
+    // its backward: a record per destination and head (heads <= columns),
+    // then the larger of the two passes' segment partials
+    need = std::max(need, al(al((size_t)g->n_dst * C * 16) + std::max(si * 3 * C * 8, so * 2 * C * 8) + 8));
+    if (flags & GNNK_SCRATCH_ARGMAX)  // winner masks, then the reverse pass's partials
+        need = std::max(need, al(E * ((C + 31) / 32) * 4) + al(so * C * 8));
+    if (flags & GNNK_SCRATCH_WIDE_SUMS)  // running fp64 sum per edge between passes
+        need = std::max(need, al(E * 8));
+    if (options().schedule >= 2) {
+        // edge-parallel walks: two partial rows per sub-chunk of at least 64
+        // positions, or one per row with atomics
+        const size_t n_sub = (E + 63) / 64;
+        need = std::max(need, al(std::max(2 * n_sub, (size_t)std::max(g->n_src, g->n_dst)) * C * 8));
+    }
+    *bytes = need;
+    return GNNK_OK;
 }
 
 gnnk_status gsddmm(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
@@ -545,7 +588,8 @@ gnnk_status gsddmm(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_t
         opk = (op == GNNK_MUL || op == GNNK_DOT) ? 1 : 2;
         A.op = op == GNNK_ADD ? M_ADD : (op == GNNK_SUB ? M_SUB : (op == GNNK_DIV ? M_DIV : M_MUL));
     }
-    return run_sddmm(g, A, geo, dtype_code(out), opk, stream);
+    Scratch sc = scratch_of(g, stream);
+    return run_sddmm(g, A, geo, dtype_code(out), opk, stream, sc);
 }
 
 // arg_ld: elements per row of arg_rhs (-1: H * F of the call; a head slice
@@ -597,6 +641,7 @@ static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce redu
     const int dt = dtype_code(grad_out);
     const int32_t scale_flags = (reduce == GNNK_MEAN ? F_SCALE_A_DEG : 0) | (cmp ? F_MASK_A : 0);
     bool dw_done = false;
+    const Scratch lent = scratch_of(g, stream);
 
     if (grad_lhs && g->n_src > 0) {
         // Lemma complex_dspmm_dx: a g-SpMM on the reverse graph, message dZ[v] * d phi / d x
@@ -620,14 +665,15 @@ static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce redu
         A.deg = g->in.deg;
         A.mask_arg = arg_rhs;
         A.mask_ld = ld;
+        Scratch sc = lent;
         if (cmp && g->n_edges > 0) {
             // the argmax scatter as a masked g-SpMM on the reverse graph: the
             // winning columns of each edge are marked once in a bit mask laid
             // out in reverse-CSR order, so the walk reads 4 bytes per 32
             // columns per edge instead of the arg array of its destination
             const int32_t words = (int32_t)((geo.D + 31) / 32);
-            uint32_t* bits = reinterpret_cast<uint32_t*>(graph_scratch(g, (size_t)g->n_edges * words * 4, 1));
-            if (!bits) return fail(GNNK_ENOMEM, "scratch allocation failed");
+            uint32_t* bits = reinterpret_cast<uint32_t*>(sc.take((size_t)g->n_edges * words * 4));
+            if (!bits) return scratch_fail(sc);
             st = launch_status(launch_winner_bits(arg_rhs, g->n_dst, (int32_t)geo.D, ld, g->out.pos, bits,
                                                   g->n_edges, words, stream),
                                "winner mask launch");
@@ -649,7 +695,7 @@ static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce redu
             A.per_head2 = rhs->heads > 1 ? 1 : 0;
             A.red2 = A.per_head2 ? Fm / geo.vec : (int32_t)geo.NV;
         }
-        st = run_spmm_sum(g, g->out, A, geo, dt, opk, stream, want_dw ? &dw_done : nullptr);
+        st = run_spmm_sum(g, g->out, A, geo, dt, opk, stream, sc, want_dw ? &dw_done : nullptr);
         if (st != GNNK_OK) return st;
     }
     if (grad_rhs && g->n_edges > 0 && !dw_done) {
@@ -680,7 +726,9 @@ static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce redu
         A.deg = g->in.deg;
         A.mask_arg = arg_rhs;
         A.mask_ld = ld;
-        st = run_sddmm(g, A, geo, dt, opk, stream);
+        // the passes run in stream order: this one reuses the scratch from its start
+        Scratch sc = lent;
+        st = run_sddmm(g, A, geo, dt, opk, stream, sc);
         if (st != GNNK_OK) return st;
     }
     return GNNK_OK;
@@ -799,8 +847,9 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
         st = out_desc(gx, ms.back().kind, geo, A.out);
         if (st != GNNK_OK) return st;
         A.flags = flags;
-        if (tx == GNNK_EDGE) st = run_sddmm(g, A, geo, dt, opk, stream);
-        else st = run_spmm_sum(g, tx == GNNK_SRC ? g->out : g->in, A, geo, dt, opk, stream);
+        Scratch sc = scratch_of(g, stream);
+        if (tx == GNNK_EDGE) st = run_sddmm(g, A, geo, dt, opk, stream, sc);
+        else st = run_spmm_sum(g, tx == GNNK_SRC ? g->out : g->in, A, geo, dt, opk, stream, sc);
         if (st != GNNK_OK) return st;
     }
     return GNNK_OK;
@@ -887,8 +936,9 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
     const size_t part = (size_t)A.sch.n_seg * 3 * geo.D * 8, ml = attn ? (size_t)A.sch.n_hub * 2 * geo.D * 8 : 0;
     void* row_ml = nullptr;
     if (part + ml > 0) {
-        char* p = reinterpret_cast<char*>(graph_scratch(g, part + ml));
-        if (!p) return fail(GNNK_ENOMEM, "scratch allocation failed");
+        Scratch sc = scratch_of(g, stream);
+        char* p = reinterpret_cast<char*>(sc.take(part + ml));
+        if (!p) return scratch_fail(sc);
         A.partial = p;
         row_ml = ml ? p + part : nullptr;
     }
@@ -961,8 +1011,9 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
     const size_t rec = (size_t)g->n_dst * H * 16, pa = (size_t)ain.sch.n_seg * 3 * H * 8,
                  pb = (size_t)aout.sch.n_seg * (geo.D + H) * 8;
     const size_t rec_al = (rec + 255) / 256 * 256;
-    char* p = reinterpret_cast<char*>(graph_scratch(g, rec_al + std::max(pa, pb) + 8));
-    if (!p) return fail(GNNK_ENOMEM, "scratch allocation failed");
+    Scratch sc = scratch_of(g, stream);
+    char* p = reinterpret_cast<char*>(sc.take(rec_al + std::max(pa, pb) + 8));
+    if (!p) return scratch_fail(sc);
     GatBwdArgs B{};
     B.er = er->data;
     B.er_stride = er->row_stride;

@@ -19,15 +19,15 @@ namespace gnnk {
 // ---------------------------------------------------------------------------
 // errors and options
 
-static thread_local std::string g_err;
+static thread_local char g_err[512];
+// bytes of scratch the last call on this thread that ran short asked for
+static thread_local size_t g_need = 0;
 
 gnnk_status fail(gnnk_status st, const char* fmt, ...) {
-    char buf[512];
     va_list ap;
     va_start(ap, fmt);
-    vsnprintf(buf, sizeof(buf), fmt, ap);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
     va_end(ap);
-    g_err = buf;
     return st;
 }
 
@@ -35,7 +35,10 @@ gnnk_status hip_fail(hipError_t e, const char* what) {
     return fail(GNNK_EHIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
 }
 
-void clear_error() { g_err.clear(); }
+void clear_error() {
+    g_err[0] = 0;
+    g_need = 0;
+}
 
 Options& options() {
     static Options o;
@@ -57,24 +60,32 @@ int64_t Dir::count_above(int64_t t) const {
     return (int64_t)(it - sorted_deg.begin());
 }
 
-void* graph_scratch(gnnk_graph* g, size_t bytes, int slot) {
-    std::lock_guard<std::mutex> lk(g->scratch_mu);
-    void*& buf = slot ? g->scratch2 : g->scratch;
-    size_t& have = slot ? g->scratch2_bytes : g->scratch_bytes;
-    if (bytes <= have) return buf;
-    if (buf) {
-        (void)hipDeviceSynchronize();  // in-flight kernels may still read the old buffer
-        (void)hipFree(buf);
-        buf = nullptr;
-        have = 0;
-    }
-    size_t want = bytes + bytes / 4;
-    if (hipMalloc(&buf, want) != hipSuccess) {
-        buf = nullptr;
+void* Scratch::take(size_t n) {
+    const size_t at = used;
+    used += (n + 255) / 256 * 256;
+    if (used > bytes) {
+        g_need = used;
         return nullptr;
     }
-    have = want;
-    return buf;
+    return base + at;
+}
+
+Scratch scratch_of(gnnk_graph* g, hipStream_t s) {
+    Scratch sc;
+    std::lock_guard<std::mutex> lk(g->lent_mu);
+    for (int k = 0; k < g->n_lent; ++k)
+        if (g->lent[k].stream == s) {
+            sc.base = g->lent[k].buf;
+            sc.bytes = g->lent[k].bytes;
+        }
+    return sc;
+}
+
+gnnk_status scratch_fail(const Scratch& sc) {
+    return fail(GNNK_ENOMEM,
+                "the call needs at least %zu bytes of scratch on its stream and has %zu: lend a larger buffer with "
+                "graph_attach_scratch (graph_scratch_bytes gives a bound, gnnk_scratch_needed this call's need)",
+                g_need, sc.bytes);
 }
 
 // ---------------------------------------------------------------------------
@@ -95,6 +106,7 @@ constexpr int32_t FLAG_NOT_IDENT = 8; // edge ids differ from in-CSR positions
 struct Layout {
     size_t in_ptr = 0, in_idx = 0, in_eid = 0, out_ptr = 0, out_idx = 0, out_eid = 0;
     size_t in_deg = 0, out_deg = 0, in_perm = 0, out_perm = 0, in_row = 0, out_row = 0, out_pos = 0, flag = 0;
+    size_t tmp = 0, tmp_words = 0;  // the build's temporaries (radix-sort counts, degree and segment sort keys)
     size_t in_hub = 0, out_hub = 0, in_seg = 0, out_seg = 0, in_sego = 0, out_sego = 0, total = 0;
 };
 
@@ -107,8 +119,23 @@ struct Bump {
     }
 };
 
-Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t hub_in, int64_t hub_out, int64_t seg_in,
-                   int64_t seg_out) {
+// segments a graph can have at most: hub rows have more than S edges, so at
+// most E / S of them, and at most E / S + (hub rows) <= 2 E / S + 2 segments
+int64_t max_segments(int64_t E, int64_t S) { return 2 * E / S + 2; }
+
+// uint32 words of build temporaries: the radix sort of the edges, or four
+// row-sized arrays plus the sort of the degree keys, or the same for the
+// segment keys
+size_t build_tmp_words(int64_t n_src, int64_t n_dst, int64_t E, int64_t S) {
+    const int64_t n = std::max(n_src, n_dst);
+    const int64_t m = max_segments(E, S);
+    auto pad = [](int64_t x) { return (size_t)((x + 63) / 64 * 64); };
+    return std::max({radix_scratch_words(E), 4 * pad(n + 64) + radix_scratch_words(n),
+                     4 * pad(m) + radix_scratch_words(m)});
+}
+
+Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t S, int64_t hub_in, int64_t hub_out,
+                   int64_t seg_in, int64_t seg_out) {
     Layout L;
     Bump b;
     L.in_ptr = b.take((size_t)(n_dst + 1) * ps);
@@ -125,6 +152,8 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t h
     L.out_row = b.take((size_t)E * 4);
     L.out_pos = b.take((size_t)E * 4);
     L.flag = b.take(ALIGN);
+    L.tmp_words = build_tmp_words(n_src, n_dst, E, S);
+    L.tmp = b.take(L.tmp_words * 4);
     L.in_hub = b.take((size_t)(hub_in + 1) * 4);
     L.out_hub = b.take((size_t)(hub_out + 1) * 4);
     L.in_seg = b.take((size_t)seg_in * 16);
@@ -181,13 +210,10 @@ struct Builder {
         return h;
     }
 
-    // radix scratch, plus four row-sized buffers for the degree order
-    bool get_scratch() {
-        const int64_t n = std::max(g->n_src, g->n_dst);
-        const size_t words = std::max(radix_scratch_words(g->n_edges), 4 * (size_t)(n + 64) + radix_scratch_words(n));
-        scratch = reinterpret_cast<uint32_t*>(graph_scratch(g, words * 4));
-        scratch_words = words;
-        return scratch != nullptr;
+    // the build's temporaries, a region of the workspace
+    void get_scratch() {
+        scratch = at<uint32_t>(L.tmp);
+        scratch_words = L.tmp_words;
     }
 
     // the reverse graph's CSR from the source and destination of every edge id
@@ -236,14 +262,11 @@ struct Builder {
         const int64_t n = d.n_seg;
         if (n <= 0) return;
         const int64_t pad = (n + 63) / 64 * 64;
-        const size_t words = 4 * (size_t)pad + radix_scratch_words(n);
-        if (words > scratch_words) {
-            scratch = reinterpret_cast<uint32_t*>(graph_scratch(g, words * 4));
-            if (!scratch) {
-                if (err == hipSuccess) err = hipErrorOutOfMemory;
-                return;
-            }
-            scratch_words = words;
+        // the temporaries are sized for the largest segment count a graph of
+        // this size can have
+        if (4 * (size_t)pad + radix_scratch_words(n) > scratch_words) {
+            if (err == hipSuccess) err = hipErrorInvalidValue;
+            return;
         }
         uint32_t* key = scratch;
         uint32_t* sorted = key + pad;
@@ -279,10 +302,12 @@ struct Builder {
         for (size_t k = 0; k < kin.size(); ++k) in.sorted_deg[k] = (int32_t)((uint32_t)E - kin[k]);
         out.sorted_deg.resize(kout.size());
         for (size_t k = 0; k < kout.size(); ++k) out.sorted_deg[k] = (int32_t)((uint32_t)E - kout[k]);
-        std::vector<int32_t> hin, hout;
+        std::vector<int32_t>& hin = in.hub_host;
+        std::vector<int32_t>& hout = out.hub_host;
         schedule_host(in, g->seg_edges, hin);
         schedule_host(out, g->seg_edges, hout);
-        L = make_layout(g->n_src, g->n_dst, E, g->ptr64 ? 8 : 4, in.n_hub, out.n_hub, in.n_seg, out.n_seg);
+        L = make_layout(g->n_src, g->n_dst, E, g->ptr64 ? 8 : 4, g->seg_edges, in.n_hub, out.n_hub, in.n_seg,
+                        out.n_seg);
         if (ws_bytes < L.total)
             return fail(GNNK_ENOMEM, "workspace of %zu bytes is smaller than the %zu bytes this graph needs",
                         ws_bytes, L.total);
@@ -299,24 +324,18 @@ struct Builder {
         order_segments(in, g->n_src);
         order_segments(out, g->n_dst);
         chk(hipMemsetAsync(g->flag, 0, 4, s));
-        chk(hipStreamSynchronize(s));  // hin/hout are about to go away
+        // the host copies of the hub offsets stay with the handle, so the
+        // copies above may still be in flight when the call returns
         if (err != hipSuccess) return hip_fail(err, "graph build");
         g->ws_used = L.total;
         return GNNK_OK;
     }
 };
 
-void free_graph(gnnk_graph* g) {
-    if (g->scratch2) {
-        (void)hipDeviceSynchronize();
-        (void)hipFree(g->scratch2);
-    }
-    if (g->scratch) {
-        (void)hipDeviceSynchronize();
-        (void)hipFree(g->scratch);
-    }
-    delete g;
-}
+// The handle owns no device memory (its arrays live in the caller's
+// workspace, its scratch is lent by the caller), so destroying it is a host
+// operation; kernels still in flight keep reading the caller's buffers.
+void free_graph(gnnk_graph* g) { delete g; }
 
 gnnk_graph* new_graph(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_itype ptr_t) {
     gnnk_graph* g = new gnnk_graph();
@@ -331,7 +350,7 @@ gnnk_graph* new_graph(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_
 // workspace checks shared by both constructors; fills b.W, b.L, g->flag
 gnnk_status begin_build(Builder& b, void* ws, size_t ws_bytes) {
     gnnk_graph* g = b.g;
-    b.L = make_layout(g->n_src, g->n_dst, g->n_edges, g->ptr64 ? 8 : 4, 0, 0, 0, 0);
+    b.L = make_layout(g->n_src, g->n_dst, g->n_edges, g->ptr64 ? 8 : 4, g->seg_edges, 0, 0, 0, 0);
     if (!ws || ws_bytes < b.L.total)
         return fail(GNNK_ENOMEM, "workspace of %zu bytes is smaller than the %zu bytes this graph needs", ws_bytes,
                     b.L.total);
@@ -352,7 +371,7 @@ gnnk_status create_coo(Builder& b, const int32_t* src, const int32_t* dst, void*
     const int32_t h = b.read_flag();
     if (b.err != hipSuccess) return hip_fail(b.err, "checking the edge list");
     if (h & FLAG_INDEX) return fail(GNNK_EINVAL, "an edge has an endpoint out of range");
-    if (!b.get_scratch()) return fail(GNNK_ENOMEM, "scratch allocation for the graph build failed");
+    b.get_scratch();
     const Layout& L = b.L;
     Dir& in = g->in;
     in.ptr = b.W + L.in_ptr;
@@ -389,7 +408,7 @@ gnnk_status create_csr(Builder& b, const void* indptr, const int32_t* indices, c
         return fail(GNNK_EINVAL, "indptr must start at 0, end at num_edges and never decrease");
     if (h & FLAG_INDEX) return fail(GNNK_EINVAL, "an index is out of range");
     if (h & FLAG_PERM) return fail(GNNK_EINVAL, "eids is not a permutation of 0..num_edges-1");
-    if (!b.get_scratch()) return fail(GNNK_ENOMEM, "scratch allocation for the graph build failed");
+    b.get_scratch();
     const bool identity = !eids || !(h & FLAG_NOT_IDENT);
     g->identity_eids = identity;
     Dir& in = g->in;
@@ -425,8 +444,8 @@ gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_
     // hub rows have more than S edges: at most E / S of them, and at most
     // E / S + (hub rows) <= 2 E / S segments
     int64_t S = seg_edges_for(num_edges);
-    int64_t hub = num_edges / S + 1, seg = 2 * num_edges / S + 2;
-    Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, hub, hub, seg, seg);
+    int64_t hub = num_edges / S + 1, seg = max_segments(num_edges, S);
+    Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, S, hub, hub, seg, seg);
     *bytes = L.total;
     return GNNK_OK;
 }
@@ -549,6 +568,34 @@ gnnk_status graph_destroy(gnnk_graph_t g) {
     return GNNK_OK;
 }
 
+gnnk_status graph_attach_scratch(gnnk_graph_t g, hipStream_t stream, void* buf, size_t bytes) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    if (bytes > 0 && !buf) return fail(GNNK_EINVAL, "buf is NULL");
+    if ((uintptr_t)buf % ALIGN) return fail(GNNK_EINVAL, "scratch must be 256-byte aligned");
+    std::lock_guard<std::mutex> lk(g->lent_mu);
+    int k = 0;
+    while (k < g->n_lent && g->lent[k].stream != stream) ++k;
+    if (!buf || bytes == 0) {
+        if (k < g->n_lent) g->lent[k] = g->lent[--g->n_lent];
+        return GNNK_OK;
+    }
+    if (k == g->n_lent) {
+        if (g->n_lent == gnnk_graph::MAX_STREAMS)
+            return fail(GNNK_EINVAL, "a handle takes scratch for at most %d streams", gnnk_graph::MAX_STREAMS);
+        ++g->n_lent;
+    }
+    g->lent[k] = {stream, reinterpret_cast<char*>(buf), bytes};
+    return GNNK_OK;
+}
+
+gnnk_status gnnk_scratch_needed(size_t* bytes) {
+    // not clear_error(): this reports on the previous call
+    if (!bytes) return GNNK_EINVAL;
+    *bytes = g_need;
+    return GNNK_OK;
+}
+
 gnnk_status gnnk_set_option(const char* key, int64_t value) {
     clear_error();
     if (!key) return fail(GNNK_EINVAL, "NULL key");
@@ -579,6 +626,6 @@ gnnk_status gnnk_set_option(const char* key, int64_t value) {
     return GNNK_OK;
 }
 
-const char* gnnk_last_error(void) { return g_err.c_str(); }
+const char* gnnk_last_error(void) { return g_err; }
 
 }  // extern "C"

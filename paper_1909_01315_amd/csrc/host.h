@@ -29,6 +29,7 @@ struct Dir {
     int32_t* pos = nullptr;        // device position of each edge id in this CSR
     int64_t n_seg = 0, n_hub = 0, n_nz = 0, max_deg = 0;
     std::vector<int32_t> sorted_deg;  // host, descending (bin boundaries by binary search)
+    std::vector<int32_t> hub_host;    // host copy of hub_off (the source of its upload)
     int64_t count_above(int64_t t) const;  // rows with degree > t
 };
 
@@ -42,13 +43,16 @@ struct gnnk_graph {
     gnnk::Dir in, out;
     int32_t* flag = nullptr;  // device word for graph_validate
     size_t ws_used = 0;
-    // scratch for hub-row partials, owned by the handle and grown on demand
-    void* scratch = nullptr;
-    size_t scratch_bytes = 0;
-    // second scratch (winner masks of max/min backward)
-    void* scratch2 = nullptr;
-    size_t scratch2_bytes = 0;
-    std::mutex scratch_mu;
+    // scratch buffers the caller lent to the handle, one per stream
+    static constexpr int MAX_STREAMS = 16;
+    struct Lent {
+        hipStream_t stream;
+        char* buf;
+        size_t bytes;
+    };
+    Lent lent[MAX_STREAMS];
+    int n_lent = 0;
+    std::mutex lent_mu;
 };
 
 namespace gnnk {
@@ -72,8 +76,26 @@ gnnk_status fail(gnnk_status st, const char* fmt, ...);
 gnnk_status hip_fail(hipError_t e, const char* what);
 void clear_error();
 
-// scratch of at least `bytes` bytes owned by g (nullptr on failure); slot 0
-// holds partials, slot 1 winner masks
-void* graph_scratch(gnnk_graph* g, size_t bytes, int slot = 0);
+// Device scratch of one compute call: the buffer lent to the handle for the
+// call's stream, handed out front to back in 256-byte steps.  take() returns
+// nullptr when the buffer is too small, after recording how many bytes the
+// call asked for up to that point (gnnk_scratch_needed).
+struct Scratch {
+    char* base = nullptr;
+    size_t bytes = 0;
+    size_t used = 0;
+    void* take(size_t n);
+};
+
+// the buffer lent to g for stream s (empty when none)
+Scratch scratch_of(gnnk_graph* g, hipStream_t s);
+
+// status and message of a call that did not get the scratch it needs
+gnnk_status scratch_fail(const Scratch& sc);
+
+// gspmm with its scratch from sc (api.cpp)
+gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                       const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
+                       hipStream_t stream, Scratch& sc);
 
 }  // namespace gnnk

@@ -85,6 +85,9 @@ SYMBOLS = {
     "gat_aggregate_backward": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
                                ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                ctypes.c_void_p],
+    "graph_scratch_bytes": [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p],
+    "graph_attach_scratch": [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t],
+    "gnnk_scratch_needed": [ctypes.c_void_p],
     "gnnk_set_option": [ctypes.c_char_p, ctypes.c_int64],
     "gnnk_last_error": [],
 }
@@ -116,6 +119,27 @@ def _stream(stream=None) -> int:
     if stream is None:
         stream = torch.cuda.current_stream()
     return stream.cuda_stream
+
+
+SCRATCH_ARGMAX, SCRATCH_WIDE_SUMS = 1, 2
+
+
+def _run(g, call, stream=None):
+    """Run call() (a C entry point on g); when it ran short of scratch, lend g
+    a buffer of the size it asked for on the call's stream and run it again
+    (outputs are overwritten, never accumulated, so a repeated call gives the
+    same result).  A call that needs several parts asks for them in turn."""
+    st = call()
+    for _ in range(4):
+        if st != ENOMEM:
+            break
+        need = ctypes.c_size_t(0)
+        load().gnnk_scratch_needed(ctypes.byref(need))
+        if need.value == 0:  # short of something else (a workspace)
+            break
+        g.lend_scratch(need.value, stream)
+        st = call()
+    _check(st)
 
 
 def _as3(t: torch.Tensor) -> torch.Tensor:
@@ -168,7 +192,32 @@ class Graph:
     def __init__(self, handle, keep, num_src, num_dst, num_edges):
         self._h = handle
         self._keep = keep  # tensors the handle points into
+        self._lent = {}    # stream handle -> scratch buffer lent for that stream
         self.num_src, self.num_dst, self.num_edges = num_src, num_dst, num_edges
+
+    @property
+    def device(self):
+        return self._keep[0].device
+
+    def scratch_bytes(self, max_cols: int, argmax: bool = False, wide_sums: bool = False) -> int:
+        """Bytes of scratch any call with messages of at most max_cols columns needs."""
+        n = ctypes.c_size_t(0)
+        flags = (SCRATCH_ARGMAX if argmax else 0) | (SCRATCH_WIDE_SUMS if wide_sums else 0)
+        _check(load().graph_scratch_bytes(self.handle, int(max_cols), flags, ctypes.byref(n)))
+        return n.value
+
+    def lend_scratch(self, nbytes: int, stream=None):
+        """Lend the handle a scratch buffer of at least nbytes for the calls on
+        `stream` (default: the current stream), allocated on that stream; the
+        buffer it replaces goes back to torch's allocator, which reuses it only
+        for work ordered after the calls already queued on that stream."""
+        s = stream if stream is not None else torch.cuda.current_stream()
+        old = self._lent.get(s.cuda_stream)
+        size = max(int(nbytes), int(old.numel() * 5 // 4) if old is not None else 0, 256)
+        with torch.cuda.stream(s):
+            buf = torch.empty(size, dtype=torch.uint8, device=self.device)
+        _check(load().graph_attach_scratch(self.handle, s.cuda_stream, buf.data_ptr(), size))
+        self._lent[s.cuda_stream] = buf
 
     @staticmethod
     def _workspace(num_src, num_dst, num_edges, ptr_t, device):
@@ -246,6 +295,7 @@ class Graph:
             _check(load().graph_destroy(self._h))
             self._h = None
             self._keep = None
+            self._lent = None
 
     def __del__(self):
         try:
@@ -291,8 +341,8 @@ def gspmm(g: Graph, op: str, reduce: str, lhs=None, rhs=None, out=None, want_arg
         if arg_r is None:
             arg_r = torch.empty((g.num_dst, h, f), dtype=torch.int32, device=dev)
     dl, dr, do = _desc(lhs), _desc(rhs), _desc(out)
-    _check(load().gspmm(g.handle, OPS[op], REDUCES[reduce], _ref(dl), _ref(dr), _ref(do), _ptr(arg_l), _ptr(arg_r),
-                        _stream(stream)))
+    _run(g, lambda: load().gspmm(g.handle, OPS[op], REDUCES[reduce], _ref(dl), _ref(dr), _ref(do), _ptr(arg_l),
+                                 _ptr(arg_r), _stream(stream)), stream)
     return (out, arg_l, arg_r) if want_args else out
 
 
@@ -308,8 +358,8 @@ def gsddmm(g: Graph, op: str, lhs, lhs_target: str, rhs, rhs_target: str, out=No
     if out is None:
         out = torch.empty((g.num_edges, h, f), dtype=dt, device=dev)
     dl, dr, do = _desc(lhs), _desc(rhs), _desc(out)
-    _check(load().gsddmm(g.handle, OPS[op], _ref(dl), TARGETS[lhs_target], _ref(dr), TARGETS[rhs_target], _ref(do),
-                         _stream(stream)))
+    _run(g, lambda: load().gsddmm(g.handle, OPS[op], _ref(dl), TARGETS[lhs_target], _ref(dr), TARGETS[rhs_target],
+                                  _ref(do), _stream(stream)), stream)
     return out
 
 
@@ -328,8 +378,8 @@ def gspmm_backward(g: Graph, op: str, reduce: str, lhs, rhs, grad_out, arg_rhs=N
     if not want_rhs:
         grad_rhs = None
     d = [_desc(x) for x in (lhs, rhs, grad_out, grad_lhs, grad_rhs)]
-    _check(load().gspmm_backward(g.handle, OPS[op], REDUCES[reduce], _ref(d[0]), _ref(d[1]), None, _ptr(arg_rhs),
-                                 _ref(d[2]), _ref(d[3]), _ref(d[4]), _stream(stream)))
+    _run(g, lambda: load().gspmm_backward(g.handle, OPS[op], REDUCES[reduce], _ref(d[0]), _ref(d[1]), None,
+                                          _ptr(arg_rhs), _ref(d[2]), _ref(d[3]), _ref(d[4]), _stream(stream)), stream)
     return grad_lhs, grad_rhs
 
 
@@ -347,8 +397,9 @@ def gsddmm_backward(g: Graph, op: str, lhs, lhs_target: str, rhs, rhs_target: st
     if not want_rhs:
         grad_rhs = None
     d = [_desc(x) for x in (lhs, rhs, grad_out, grad_lhs, grad_rhs)]
-    _check(load().gsddmm_backward(g.handle, OPS[op], _ref(d[0]), TARGETS[lhs_target], _ref(d[1]),
-                                  TARGETS[rhs_target], _ref(d[2]), _ref(d[3]), _ref(d[4]), _stream(stream)))
+    _run(g, lambda: load().gsddmm_backward(g.handle, OPS[op], _ref(d[0]), TARGETS[lhs_target], _ref(d[1]),
+                                           TARGETS[rhs_target], _ref(d[2]), _ref(d[3]), _ref(d[4]), _stream(stream)),
+         stream)
     return grad_lhs, grad_rhs
 
 
@@ -357,7 +408,7 @@ def edge_softmax(g: Graph, score, out=None, stream=None):
     if out is None:
         out = torch.empty(score.shape, dtype=score.dtype, device=score.device)
     d1, d2 = _desc(score), _desc(out)
-    _check(load().edge_softmax(g.handle, _ref(d1), _ref(d2), _stream(stream)))
+    _run(g, lambda: load().edge_softmax(g.handle, _ref(d1), _ref(d2), _stream(stream)), stream)
     return out
 
 
@@ -366,7 +417,7 @@ def edge_softmax_backward(g: Graph, out, grad_out, grad_score=None, stream=None)
     if grad_score is None:
         grad_score = torch.empty(out.shape, dtype=grad_out.dtype, device=grad_out.device)
     d1, d2, d3 = _desc(out), _desc(grad_out), _desc(grad_score)
-    _check(load().edge_softmax_backward(g.handle, _ref(d1), _ref(d2), _ref(d3), _stream(stream)))
+    _run(g, lambda: load().edge_softmax_backward(g.handle, _ref(d1), _ref(d2), _ref(d3), _stream(stream)), stream)
     return grad_score
 
 
@@ -383,8 +434,8 @@ def gat_aggregate(g: Graph, feat, el, er, slope: float = 0.2, out=None, attn=Non
     if want_stats and stats is None:
         stats = torch.empty((g.num_dst, feat.shape[1], 2), dtype=torch.float32, device=feat.device)
     d = [_desc(x) for x in (feat, el, er, out, attn, stats)]
-    _check(load().gat_aggregate(g.handle, _ref(d[0]), _ref(d[1]), _ref(d[2]), ctypes.c_float(slope), _ref(d[3]),
-                                _ref(d[4]), _ref(d[5]), _stream(stream)))
+    _run(g, lambda: load().gat_aggregate(g.handle, _ref(d[0]), _ref(d[1]), _ref(d[2]), ctypes.c_float(slope),
+                                         _ref(d[3]), _ref(d[4]), _ref(d[5]), _stream(stream)), stream)
     res = (out,) + ((attn,) if attn is not None else ()) + ((stats,) if stats is not None else ())
     return res if len(res) > 1 else out
 
@@ -397,9 +448,9 @@ def gat_aggregate_backward(g: Graph, feat, el, er, slope: float, stats, grad_out
     gl = torch.empty(el.shape, dtype=feat.dtype, device=feat.device) if want_el else None
     gr = torch.empty(er.shape, dtype=feat.dtype, device=feat.device) if want_er else None
     d = [_desc(x) for x in (feat, el, er, stats, grad_out, gf, gl, gr)]
-    _check(load().gat_aggregate_backward(g.handle, _ref(d[0]), _ref(d[1]), _ref(d[2]), ctypes.c_float(slope),
-                                         _ref(d[3]), _ref(d[4]), _ref(d[5]), _ref(d[6]), _ref(d[7]),
-                                         _stream(stream)))
+    _run(g, lambda: load().gat_aggregate_backward(g.handle, _ref(d[0]), _ref(d[1]), _ref(d[2]),
+                                                  ctypes.c_float(slope), _ref(d[3]), _ref(d[4]), _ref(d[5]),
+                                                  _ref(d[6]), _ref(d[7]), _stream(stream)), stream)
     return gf, gl, gr
 
 

@@ -54,6 +54,11 @@ def test_host_side_errors(lib):
     assert lib.gnnk_set_option(b"seg_edges", 1) == gnnk.EINVAL
     assert lib.gnnk_set_option(b"seg_edges", 0) == gnnk.OK  # per graph (the default)
     assert lib.edge_leaky_relu(None, None, ctypes.c_float(0.2), None) == gnnk.EINVAL
+    n = ctypes.c_size_t(7)
+    assert lib.graph_scratch_bytes(None, 64, 0, ctypes.byref(n)) == gnnk.EINVAL
+    assert lib.graph_attach_scratch(None, None, None, 0) == gnnk.EINVAL
+    assert lib.gnnk_scratch_needed(None) == gnnk.EINVAL
+    assert lib.gnnk_scratch_needed(ctypes.byref(n)) == gnnk.OK and n.value == 0
 
 
 def test_workspace_bound_grows_with_size(lib):

@@ -3,8 +3,9 @@ SAGE-mean aggregation captured once into a torch.cuda.CUDAGraph (HIP graph on
 ROCm) and replayed several times, with eager work and synchronisations
 between replays; every replay must equal the eager result bit for bit (the
 kernels are deterministic, and no call inside issues hipMemsetAsync, whose
-graph nodes have misbehaved on replays).  Scratch buffers are sized by an
-eager warm-up call before capture."""
+graph nodes have misbehaved on replays).  The binding lends each stream its
+scratch buffer on first need: the warm-up on the capture stream does it
+before capture, so the captured calls allocate nothing."""
 import numpy as np
 import pytest
 import torch
@@ -47,8 +48,10 @@ def test_gat_and_sage_replay_equals_eager():
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
+    lent = dict(g._lent)
+    with torch.cuda.graph(graph, stream=side):
         outs = step()
+    assert {k: v.data_ptr() for k, v in g._lent.items()} == {k: v.data_ptr() for k, v in lent.items()}
     for rep in range(4):
         for t in outs:
             t.fill_(float("nan"))
@@ -82,7 +85,7 @@ def test_small_graph_step_time_graph_vs_eager():
         step()
     torch.cuda.current_stream().wait_stream(side)
     graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
+    with torch.cuda.graph(graph, stream=side):
         step()
 
     def timed(fn, n=20):
