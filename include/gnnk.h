@@ -246,6 +246,22 @@ gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_
                   const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
                   hipStream_t stream);
 
+/* gspmm for callers that cannot allocate at all (code under HIP graph
+ * capture with no buffer to lend, tight serving loops, harnesses that forbid
+ * allocation): the same operation, arguments and results as gspmm, with its
+ * scratch taken from a fixed buffer of 64 MiB that the library holds on each
+ * GPU it runs on (from the first call on that GPU until the process ends)
+ * instead of a lent one; no buffer needs to be attached.  The caller still
+ * provides inputs and outputs.  A call whose scratch would exceed 64 MiB
+ * (segments x H * F x 8 bytes, x 12 for MAX/MIN) returns GNNK_ENOMEM before
+ * launching anything.  Every call on one GPU shares that GPU's buffer: calls
+ * that overlap in time on one GPU (on different streams, or from several
+ * threads without ordering) race and give undefined results; calls ordered
+ * on one stream are safe.  Nothing in the buffer needs to start at zero. */
+gnnk_status gspmm_noalloc(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                          const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
+                          hipStream_t stream);
+
 /* g-SDDMM (Section 3, definition of generalized SDDMM):
  *   out[e] = op(lhs[t_l(e)], rhs[t_r(e)]) for every edge (u, e, v),
  * t(e) being u, e or v by the operand's target.  ADD/SUB/MUL/DIV are single

@@ -17,7 +17,8 @@ LIB = os.path.join(HERE, "libgnnk.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["spmm.hip", "sddmm.hip", "edge.hip", "gat.hip", "softmax.hip", "misc.hip", "build.hip", "graph.cpp", "api.cpp"]
+SOURCES = ["spmm.hip", "sddmm.hip", "edge.hip", "gat.hip", "softmax.hip", "misc.hip", "build.hip", "noalloc.hip",
+           "graph.cpp", "api.cpp"]
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", os.path.join(ROOT, "include"), "-I", CSRC]
 # no hand-packed or compiler-packed fp32 math (v_pk_*_f32) on this target

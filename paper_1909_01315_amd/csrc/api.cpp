@@ -414,8 +414,9 @@ int heads_per_slice(int Hm, int Fm, std::initializer_list<const gnnk_tensor*> al
 
 }  // namespace
 
-// gspmm with its scratch from `sc` (the buffer lent for the stream); checks
-// every argument before it takes scratch or launches anything
+// gspmm with its scratch from `sc` (the buffer lent for the stream, or the
+// static buffer of gspmm_noalloc); checks every argument before it takes
+// scratch or launches anything
 gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
                        const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
                        hipStream_t stream, Scratch& sc) {
@@ -493,6 +494,21 @@ gnnk_status gspmm(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
     Scratch sc = scratch_of(g, stream);
     return gspmm_impl(g, op, reduce, lhs, rhs, out, arg_lhs, arg_rhs, stream, sc);
+}
+
+gnnk_status gspmm_noalloc(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
+                          const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
+                          hipStream_t stream) {
+    clear_error();
+    if (!g) return fail(GNNK_EINVAL, "NULL graph");
+    Scratch sc;
+    gnnk_status st = static_scratch(stream, sc);
+    if (st != GNNK_OK) return st;
+    st = gspmm_impl(g, op, reduce, lhs, rhs, out, arg_lhs, arg_rhs, stream, sc);
+    if (st == GNNK_ENOMEM && sc.used > sc.bytes)
+        return fail(GNNK_ENOMEM, "gspmm_noalloc: the call needs at least %zu bytes of scratch, more than the %zu of "
+                    "the fixed buffer (gspmm takes a lent buffer of any size)", sc.used, sc.bytes);
+    return st;
 }
 
 gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags, size_t* bytes) {

@@ -77,7 +77,8 @@ gnnk_status hip_fail(hipError_t e, const char* what);
 void clear_error();
 
 // Device scratch of one compute call: the buffer lent to the handle for the
-// call's stream, handed out front to back in 256-byte steps.  take() returns
+// call's stream (or the library's static buffer of the no-allocation entry
+// point), handed out front to back in 256-byte steps.  take() returns
 // nullptr when the buffer is too small, after recording how many bytes the
 // call asked for up to that point (gnnk_scratch_needed).
 struct Scratch {
@@ -97,5 +98,11 @@ gnnk_status scratch_fail(const Scratch& sc);
 gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,
                        const gnnk_tensor* rhs, gnnk_tensor* out, int32_t* arg_lhs, int32_t* arg_rhs,
                        hipStream_t stream, Scratch& sc);
+
+// size of the fixed scratch buffer of gspmm_noalloc (one per GPU)
+constexpr size_t STATIC_SCRATCH_BYTES = (size_t)64 << 20;
+
+// the fixed buffer of the GPU that `stream` runs on (noalloc.hip)
+gnnk_status static_scratch(hipStream_t stream, Scratch& sc);
 
 }  // namespace gnnk

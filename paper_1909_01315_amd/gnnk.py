@@ -68,6 +68,8 @@ SYMBOLS = {
     "graph_destroy": [ctypes.c_void_p],
     "gspmm": [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
+    "gspmm_noalloc": [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p],
     "gsddmm": [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
                ctypes.c_void_p, ctypes.c_void_p],
     "gspmm_backward": [ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
@@ -344,6 +346,24 @@ def gspmm(g: Graph, op: str, reduce: str, lhs=None, rhs=None, out=None, want_arg
     _run(g, lambda: load().gspmm(g.handle, OPS[op], REDUCES[reduce], _ref(dl), _ref(dr), _ref(do), _ptr(arg_l),
                                  _ptr(arg_r), _stream(stream)), stream)
     return (out, arg_l, arg_r) if want_args else out
+
+
+def gspmm_noalloc(g: Graph, op: str, reduce: str, lhs=None, rhs=None, out=None, arg_lhs=None, arg_rhs=None,
+                  stream=None):
+    """gspmm with the library's fixed per-GPU scratch buffer (no buffer is
+    lent or allocated by the call; outputs and arg arrays are the caller's,
+    allocated here only when not given).  Returns out, or (out, arg_lhs,
+    arg_rhs) when arg arrays are given."""
+    lhs = _as3(lhs) if lhs is not None else None
+    rhs = _as3(rhs) if rhs is not None else None
+    if out is None:
+        h, f = _msg_shape(op, lhs, rhs)
+        dev, dt = _dev_dtype(lhs, rhs)
+        out = torch.empty((g.num_dst, h, f), dtype=dt, device=dev)
+    dl, dr, do = _desc(lhs), _desc(rhs), _desc(out)
+    _check(load().gspmm_noalloc(g.handle, OPS[op], REDUCES[reduce], _ref(dl), _ref(dr), _ref(do), _ptr(arg_lhs),
+                                _ptr(arg_rhs), _stream(stream)))
+    return (out, arg_lhs, arg_rhs) if (arg_lhs is not None or arg_rhs is not None) else out
 
 
 def gsddmm(g: Graph, op: str, lhs, lhs_target: str, rhs, rhs_target: str, out=None, stream=None):
