@@ -348,11 +348,13 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
  * once.  feat, el, er, slope and stats as passed to (and written by)
  * gat_aggregate; grad_out (num_dst, H, F); the three gradients are nullable
  * and take their operand's shape; all tensors but stats share one dtype.
- * A head must fit one pass of a wavefront, F / vec <= 64 (vec: 4 fp32 or 8
- * bf16 values per lane as F and the row strides allow; GNNK_EUNSUPPORTED
- * otherwise); rows of several heads wider than a pass run as slices of
- * heads.  Scratch: 16 bytes per (destination, head) plus per-segment
- * partials of hub rows.  Errors: GNNK_EINVAL on shapes or dtypes. */
+ * Rows of several heads wider than one pass of a wavefront (64 lanes of vec
+ * values, vec being 4 fp32 or 8 bf16 as F and the row strides allow) run as
+ * slices of heads; a single head wider than a pass runs in column chunks of
+ * one pass, S, P and d_el being sums of per-chunk parts carried in fp64
+ * between the chunks.  Scratch: 16 bytes per (destination, head), per-segment
+ * partials of hub rows, and for a head in column chunks 16 bytes per
+ * destination and 8 per source.  Errors: GNNK_EINVAL on shapes or dtypes. */
 gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
                                    const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
                                    const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,

@@ -527,8 +527,10 @@ gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags,
     // rows when the attention is written
     need = std::max(need, al(si * 3 * C * 8 + (size_t)g->in.n_hub * 2 * C * 8));
     // its backward: a record per destination and head (heads <= columns),
-    // then the larger of the two passes' segment partials
-    need = std::max(need, al(al((size_t)g->n_dst * C * 16) + std::max(si * 3 * C * 8, so * 2 * C * 8) + 8));
+    // the accumulators of a head run in column chunks, then the larger of
+    // the two passes' segment partials
+    need = std::max(need, al((size_t)g->n_dst * C * 16) + al((size_t)g->n_dst * 16) + al((size_t)g->n_src * 8) +
+                              al(std::max(si * 3 * C * 8, so * 2 * C * 8) + 8));
     if (flags & GNNK_SCRATCH_ARGMAX)  // winner masks, then the reverse pass's partials
         need = std::max(need, al(E * ((C + 31) / 32) * 4) + al(so * C * 8));
     if (flags & GNNK_SCRATCH_WIDE_SUMS)  // running fp64 sum per edge between passes
@@ -968,6 +970,77 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
                          "fused attention launch");
 }
 
+// One run of the fused attention backward's kernels over one head slice
+// whose heads fit a pass of the wavefront (or one column chunk of a wider
+// head: chunk 1-3, with the accumulators acc_dst / acc_src; chunk 0 for
+// whole heads).  passes: 1 pass A, 2 pass B, 3 both.  rec: the records of
+// pass A read by pass B; the segment partials are carved from sc.
+static gnnk_status gat_bwd_run(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el, const gnnk_tensor* er,
+                               float slope, const gnnk_tensor* stats, const gnnk_tensor* grad_out,
+                               gnnk_tensor* grad_feat, gnnk_tensor* grad_el, gnnk_tensor* grad_er, hipStream_t stream,
+                               Scratch& sc, float4* rec, int chunk, int passes, double* acc_dst, double* acc_src) {
+    const int H = feat->heads, F = feat->feat;
+    std::vector<Member> ms{{feat, K_FULL}, {el, K_FULL}, {grad_out, K_FULL}};
+    Geo geo;
+    gnnk_status st = choose_geo(H, F, ms, {}, geo, true);
+    if (st != GNNK_OK) return st;
+    if (geo.nchunk != 1) return fail(GNNK_EUNSUPPORTED, "fused attention backward: a slice wider than one pass");
+    const int dt = dtype_code(grad_out);
+    EngineArgs ain{}, aout{};
+    ain.a = operand(feat, K_FULL, T_NBR);
+    ain.b = operand(el, ms[1].kind, T_NBR);
+    ain.op = M_MUL;
+    ain.csr = csr_of(g, g->in);
+    set_geo(ain, geo);
+    ain.sch = schedule(g->in, geo, true);
+    aout.csr = csr_of(g, g->out);
+    set_geo(aout, geo);
+    aout.sch = schedule(g->out, geo, true);
+    const size_t pa = (size_t)ain.sch.n_seg * 3 * H * 8, pb = (size_t)aout.sch.n_seg * (geo.D + H) * 8;
+    double* part = reinterpret_cast<double*>(sc.take(std::max(pa, pb) + 8));
+    if (!part) return scratch_fail(sc);
+    GatBwdArgs B{};
+    B.er = er->data;
+    B.er_stride = er->row_stride;
+    B.stats = reinterpret_cast<const float*>(stats->data);
+    B.stats_stride = stats->row_stride;
+    B.dz = grad_out->data;
+    B.dz_stride = grad_out->row_stride;
+    B.d_er = grad_er ? grad_er->data : nullptr;
+    B.d_er_stride = grad_er ? grad_er->row_stride : 0;
+    B.d_el = grad_el ? grad_el->data : nullptr;
+    B.d_el_stride = grad_el ? grad_el->row_stride : 0;
+    B.d_feat = grad_feat ? grad_feat->data : nullptr;
+    B.d_feat_stride = grad_feat ? grad_feat->row_stride : 0;
+    B.el = el->data;
+    B.el_stride = el->row_stride;
+    B.feat = feat->data;
+    B.feat_stride = feat->row_stride;
+    B.rec = rec;
+    B.part = part;
+    B.slope = slope;
+    B.H = H;
+    B.chunk = chunk;
+    B.passes = passes;
+    B.acc_dst = acc_dst;
+    B.acc_src = acc_src;
+    const int es = dt == 1 ? 2 : 4;
+    const bool fast = !options().no_fast && fast_geo(geo, dt) && fits32(ain.a, g->n_src, es) &&
+                      fits32(ain.b, g->n_src, es);
+    return launch_status(launch_gat_backward(ain, aout, B, dt, geo.vec, fast ? geo.G : 0, stream),
+                         "fused attention backward launch");
+}
+
+// columns [c0, c0 + cw) of a one-head (rows, 1, F) tensor (a view: same rows
+// and row stride)
+static gnnk_tensor col_slice(const gnnk_tensor* t, int c0, int cw) {
+    gnnk_tensor s = *t;
+    const size_t es = t->dtype == GNNK_BF16 ? 2 : 4;
+    if (s.data) s.data = static_cast<char*>(t->data) + (size_t)c0 * es;
+    s.feat = cw;
+    return s;
+}
+
 gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
                                    const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
                                    const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,
@@ -995,67 +1068,62 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
     Geo geo;
     gnnk_status st = choose_geo(H, F, ms, {}, geo, true);
     if (st != GNNK_OK) return st;
-    // a head's dot products are reduced across the lanes of one pass: rows
-    // wider than a pass run as slices of heads (heads are independent)
-    if (geo.nchunk != 1) {
-        if (F / geo.vec > 64) return fail(GNNK_EUNSUPPORTED, "fused attention backward needs F / vec <= 64");
-        const int hs = 64 / (F / geo.vec);
-        for (int h0 = 0; h0 < H; h0 += hs) {
-            const int hc = std::min(hs, H - h0);
-            gnnk_tensor f = head_slice(feat, H, h0, hc), l = head_slice(el, H, h0, hc), r = head_slice(er, H, h0, hc);
-            gnnk_tensor sts = head_slice(stats, H, h0, hc), go = head_slice(grad_out, H, h0, hc);
-            gnnk_tensor gf = grad_feat ? head_slice(grad_feat, H, h0, hc) : gnnk_tensor{};
-            gnnk_tensor gl = grad_el ? head_slice(grad_el, H, h0, hc) : gnnk_tensor{};
-            gnnk_tensor gr = grad_er ? head_slice(grad_er, H, h0, hc) : gnnk_tensor{};
-            st = gat_aggregate_backward(g, &f, &l, &r, slope, &sts, &go, grad_feat ? &gf : nullptr,
-                                        grad_el ? &gl : nullptr, grad_er ? &gr : nullptr, stream);
-            if (st != GNNK_OK) return st;
-        }
-        return GNNK_OK;
-    }
-    const int dt = dtype_code(grad_out);
-    EngineArgs ain{}, aout{};
-    ain.a = operand(feat, K_FULL, T_NBR);
-    ain.b = operand(el, ms[1].kind, T_NBR);
-    ain.op = M_MUL;
-    ain.csr = csr_of(g, g->in);
-    set_geo(ain, geo);
-    ain.sch = schedule(g->in, geo, true);
-    aout.csr = csr_of(g, g->out);
-    set_geo(aout, geo);
-    aout.sch = schedule(g->out, geo, true);
-    const size_t rec = (size_t)g->n_dst * H * 16, pa = (size_t)ain.sch.n_seg * 3 * H * 8,
-                 pb = (size_t)aout.sch.n_seg * (geo.D + H) * 8;
-    const size_t rec_al = (rec + 255) / 256 * 256;
     Scratch sc = scratch_of(g, stream);
-    char* p = reinterpret_cast<char*>(sc.take(rec_al + std::max(pa, pb) + 8));
-    if (!p) return scratch_fail(sc);
-    GatBwdArgs B{};
-    B.er = er->data;
-    B.er_stride = er->row_stride;
-    B.stats = reinterpret_cast<const float*>(stats->data);
-    B.stats_stride = stats->row_stride;
-    B.dz = grad_out->data;
-    B.dz_stride = grad_out->row_stride;
-    B.d_er = grad_er ? grad_er->data : nullptr;
-    B.d_er_stride = grad_er ? grad_er->row_stride : 0;
-    B.d_el = grad_el ? grad_el->data : nullptr;
-    B.d_el_stride = grad_el ? grad_el->row_stride : 0;
-    B.d_feat = grad_feat ? grad_feat->data : nullptr;
-    B.d_feat_stride = grad_feat ? grad_feat->row_stride : 0;
-    B.el = el->data;
-    B.el_stride = el->row_stride;
-    B.feat = feat->data;
-    B.feat_stride = feat->row_stride;
-    B.rec = reinterpret_cast<float4*>(p);
-    B.part = reinterpret_cast<double*>(p + rec_al);
-    B.slope = slope;
-    B.H = H;
-    const int es = dt == 1 ? 2 : 4;
-    const bool fast = !options().no_fast && fast_geo(geo, dt) && fits32(ain.a, g->n_src, es) &&
-                      fits32(ain.b, g->n_src, es);
-    return launch_status(launch_gat_backward(ain, aout, B, dt, geo.vec, fast ? geo.G : 0, stream),
-                         "fused attention backward launch");
+    if (geo.nchunk == 1) {
+        float4* rec = reinterpret_cast<float4*>(sc.take((size_t)g->n_dst * H * 16));
+        if (!rec) return scratch_fail(sc);
+        return gat_bwd_run(g, feat, el, er, slope, stats, grad_out, grad_feat, grad_el, grad_er, stream, sc, rec, 0, 3,
+                           nullptr, nullptr);
+    }
+    // a head's dot products are reduced across the lanes of one pass: rows
+    // wider than a pass run as slices of heads (heads are independent), and
+    // a head wider than a pass in column chunks of one pass each
+    const int lanes = F / geo.vec;
+    const int hs = lanes <= 64 ? 64 / lanes : 1;
+    const int cw = lanes <= 64 ? F : 64 * geo.vec;
+    const int nc = (F + cw - 1) / cw;
+    float4* rec = reinterpret_cast<float4*>(sc.take((size_t)g->n_dst * hs * 16));
+    double* acc_dst = nullptr;
+    double* acc_src = nullptr;
+    if (rec && nc > 1) {
+        acc_dst = reinterpret_cast<double*>(sc.take((size_t)g->n_dst * 2 * 8));
+        acc_src = reinterpret_cast<double*>(sc.take((size_t)g->n_src * 8));
+    }
+    if (!rec || (nc > 1 && (!acc_dst || !acc_src))) return scratch_fail(sc);
+    const size_t base = sc.used;
+    for (int h0 = 0; h0 < H; h0 += hs) {
+        const int hc = std::min(hs, H - h0);
+        gnnk_tensor f = head_slice(feat, H, h0, hc), l = head_slice(el, H, h0, hc), r = head_slice(er, H, h0, hc);
+        gnnk_tensor sts = head_slice(stats, H, h0, hc), go = head_slice(grad_out, H, h0, hc);
+        gnnk_tensor gf = grad_feat ? head_slice(grad_feat, H, h0, hc) : gnnk_tensor{};
+        gnnk_tensor gl = grad_el ? head_slice(grad_el, H, h0, hc) : gnnk_tensor{};
+        gnnk_tensor gr = grad_er ? head_slice(grad_er, H, h0, hc) : gnnk_tensor{};
+        gnnk_tensor* pgf = grad_feat ? &gf : nullptr;
+        gnnk_tensor* pgl = grad_el ? &gl : nullptr;
+        gnnk_tensor* pgr = grad_er ? &gr : nullptr;
+        if (nc == 1) {
+            sc.used = base;  // the slices run in stream order and reuse the partials
+            st = gat_bwd_run(g, &f, &l, &r, slope, &sts, &go, pgf, pgl, pgr, stream, sc, rec, 0, 3, nullptr,
+                             nullptr);
+            if (st != GNNK_OK) return st;
+            continue;
+        }
+        // one head in column chunks: every chunk of pass A, then every chunk
+        // of pass B (which reads the records the last chunk of pass A wrote)
+        for (int pass = 1; pass <= 2; ++pass) {
+            for (int k = 0; k < nc; ++k) {
+                const int c0 = k * cw, w = std::min(cw, F - c0);
+                gnnk_tensor fc = col_slice(&f, c0, w), zc = col_slice(&go, c0, w);
+                gnnk_tensor gfc = grad_feat ? col_slice(&gf, c0, w) : gnnk_tensor{};
+                const int chunk = k == 0 ? 1 : (k == nc - 1 ? 3 : 2);
+                sc.used = base;
+                st = gat_bwd_run(g, &fc, &l, &r, slope, &sts, &zc, grad_feat ? &gfc : nullptr, pgl, pgr, stream, sc,
+                                 rec, chunk, pass, acc_dst, acc_src);
+                if (st != GNNK_OK) return st;
+            }
+        }
+    }
+    return GNNK_OK;
 }
 
 static gnnk_status leaky_common(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* y, float slope,

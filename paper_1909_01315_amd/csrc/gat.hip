@@ -345,6 +345,20 @@ __device__ __forceinline__ float gat_attention(float el, float er, float slope, 
 template <typename T>
 __device__ __forceinline__ void gat_finish_dst(const GatBwdArgs& B, int64_t v, int h, float er_h, float m, float il,
                                                double S, double P, double Q) {
+    if (B.chunk) {
+        // S and P of this column chunk: stored by the first, added by the
+        // others in chunk order; Q does not depend on the columns
+        double* ac = B.acc_dst + (v * B.H + h) * 2;
+        if (B.chunk > 1) {
+            S += ac[0];
+            P += ac[1];
+        }
+        if (B.chunk < 3) {
+            ac[0] = S;
+            ac[1] = P;
+            return;
+        }
+    }
     if (B.d_er) IO<T, 1>::store1(reinterpret_cast<T*>(B.d_er) + v * B.d_er_stride + h, (float)(P - S * Q));
     B.rec[v * B.H + h] = make_float4(er_h, m, il, (float)S);
 }
@@ -521,7 +535,18 @@ __device__ __forceinline__ void gat_write_src(const GatBwdArgs& B, int64_t u, in
         for (int i = 0; i < VEC; ++i) v[i] = (float)df[i];
         IO<T, VEC>::store(reinterpret_cast<T*>(B.d_feat) + u * B.d_feat_stride + col0, v);
     }
-    if (B.d_el && head_lane) IO<T, 1>::store1(reinterpret_cast<T*>(B.d_el) + u * B.d_el_stride + h, (float)dl);
+    if (B.d_el && head_lane) {
+        if (B.chunk) {
+            // this column chunk's share of d_el, added in chunk order
+            double* ac = B.acc_src + u * B.H + h;
+            if (B.chunk > 1) dl += *ac;
+            if (B.chunk < 3) {
+                *ac = dl;
+                return;
+            }
+        }
+        IO<T, 1>::store1(reinterpret_cast<T*>(B.d_el) + u * B.d_el_stride + h, (float)dl);
+    }
 }
 
 // pass B: one source row (a hub segment, a row by the wavefront, or a row by
@@ -546,6 +571,9 @@ __device__ __forceinline__ void gat_bwd_src_row(const EngineArgs& A, const GatBw
     }
     const float el_h = IO<T, 1>::load1(reinterpret_cast<const T*>(B.el) + self * B.el_stride + h);
     double dl = 0.0;
+    // d_el = sum of a (da - S) lk: a head in column chunks adds the a S lk
+    // part with its first chunk only (da is summed chunk by chunk)
+    const bool with_s = B.chunk <= 1;
     auto sink = [&](const float* z, const float4& rc, bool ok) {
         bool pos;
         const double a = gat_attention(el_h, rc.x, B.slope, rc.y, rc.z, pos);
@@ -557,7 +585,7 @@ __device__ __forceinline__ void gat_bwd_src_row(const EngineArgs& A, const GatBw
         const double ak = ok ? a : 0.0;
 #pragma unroll
         for (int i = 0; i < VEC; ++i) df[i] = fma(ak, (double)z[i], df[i]);
-        dl += ak * (da - (double)rc.w) * lk;
+        dl += ak * (da - (with_s ? (double)rc.w : 0.0)) * lk;
     };
     if constexpr (WAVE_ROW) {
         const int L = geo.L;
@@ -691,7 +719,7 @@ void gat_all(const EngineArgs& a, const GatArgs& g, int gc, hipStream_t s) {
 template <typename T, int V, int RED>
 void gat_bwd_red(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs& B, int gc, hipStream_t s) {
     const dim3 block(WAVE * WPB);
-    if (ain.sch.w_total > 0) {
+    if ((B.passes & 1) && ain.sch.w_total > 0) {
         const dim3 grid(blocks_for_waves(ain.sch.w_total));
         bool done = false;
         if constexpr ((sizeof(T) == 4 && V == 4) || (sizeof(T) == 2 && (V == 4 || V == 8))) {
@@ -712,7 +740,7 @@ void gat_bwd_red(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs
                                ain, B);
         }
     }
-    if (aout.sch.w_total > 0 && (B.d_feat || B.d_el)) {
+    if ((B.passes & 2) && aout.sch.w_total > 0 && (B.d_feat || B.d_el)) {
         hipLaunchKernelGGL((gat_bwd_src_kernel<T, V, RED>), dim3(blocks_for_waves(aout.sch.w_total)), block, 0, s,
                            aout, B);
         if (aout.sch.n_hub > 0)

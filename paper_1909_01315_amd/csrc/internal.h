@@ -212,6 +212,15 @@ struct GatBwdArgs {
     double* part;            // hub segments: pass A 3 x H, pass B D + H doubles per segment
     float slope;
     int32_t H;
+    // A head wider than one pass of the wavefront runs in column chunks: the
+    // sums S and P of pass A and d_el of pass B are linear in the per-chunk
+    // dot products, so each chunk adds its share into fp64 accumulators and
+    // the last chunk finishes.  chunk: 0 a whole head; 1 the first chunk
+    // (stores), 2 a middle one (adds), 3 the last (adds and writes).
+    int32_t chunk;
+    int32_t passes;          // 1: pass A only, 2: pass B only, 3: both
+    double* acc_dst;         // (N_dst, H) x {S, P} of the chunks so far
+    double* acc_src;         // (N_src, H): d_el of the chunks so far
 };
 hipError_t launch_gat_backward(const EngineArgs& ain, const EngineArgs& aout, const GatBwdArgs& b, int dtype, int vec,
                                int gc, hipStream_t s);

@@ -228,10 +228,8 @@ def test_gat_backward_empty_rows_partial_grads_and_bf16():
 
 def test_gat_backward_wide_rows(c1):
     """Rows of H * F / 4 > 64 lanes: the fused backward runs as slices of
-    heads and the unfused attention gradient (a per-head reduction over F)
-    as slices too, both against the oracle; a single head wider than one
-    pass (F / 4 > 64) is declined by the fused backward with
-    GNNK_EUNSUPPORTED."""
+    heads, and the unfused attention gradient (a per-head reduction over F)
+    as slices too, both against the oracle."""
     N = c1.o.n_src
     feat = synth.normal(S, "wf", (N, 4, 100))
     el = synth.normal(S, "wl", (N, 4, 1))
@@ -248,10 +246,37 @@ def test_gat_backward_wide_rows(c1):
     ox, oa = orc.gspmm_backward(c1.o, "mul", "sum", feat, a, dz)
     assert_close(dx, ox, name="unfused d feat")
     assert_close(da, oa, name="unfused d attention")
-    f1 = synth.normal(S, "wf1", (N, 1, 300))
-    e1 = synth.normal(S, "wl1", (N, 1, 1))
-    r1 = synth.normal(S, "wr1", (c1.o.n_dst, 1, 1))
-    _, st1 = gnnk.gat_aggregate(c1.g, dev(f1), dev(e1), dev(r1), 0.2, want_stats=True)
-    with pytest.raises(gnnk.GnnkError) as e:
-        gnnk.gat_aggregate_backward(c1.g, dev(f1), dev(e1), dev(r1), 0.2, st1, dev(f1[: c1.o.n_dst]))
-    assert e.value.status == gnnk.EUNSUPPORTED
+
+
+@pytest.mark.parametrize("H,F,bf16", [(1, 300, False), (2, 260, False), (1, 1030, False), (1, 600, True)])
+@pytest.mark.parametrize("seg", [0, 64])
+def test_gat_backward_head_wider_than_a_pass(H, F, bf16, seg):
+    """A single head wider than one pass of the wavefront (F / vec > 64)
+    runs in column chunks of one pass each (fp64 accumulators of S, P and
+    d_el carried across the chunks), on c2 with and without hub segments;
+    against the oracle's fp64 chain at the fused-gradient bound (the
+    attention is recomputed in fp32).  1030 columns: 5 chunks, the last
+    narrower than the others."""
+    gnnk.set_option("seg_edges", seg)
+    p = Pair.of(synth.graph_c2())
+    if seg:
+        info = p.g.info()
+        assert info["hub_dst_rows"] > 0 and info["hub_src_rows"] > 0
+    N = p.o.n_src
+    feat = synth.normal(S, f"ww{H}{F}", (N, H, F))
+    el = synth.normal(S, f"wwl{H}", (N, H, 1))
+    er = synth.normal(S, f"wwr{H}", (p.o.n_dst, H, 1))
+    dz = synth.normal(synth.grad_seed(21), f"wwz{H}{F}", (p.o.n_dst, H, F))
+    if bf16:
+        feat, el, er, dz = (synth.to_bf16_bits(x) for x in (feat, el, er, dz))
+    _, st = gnnk.gat_aggregate(p.g, dev(feat), dev(el), dev(er), 0.2, want_stats=True)
+    gf, gl, gr = gnnk.gat_aggregate_backward(p.g, dev(feat), dev(el), dev(er), 0.2, st, dev(dz))
+    w = orc.bf16_to_f32 if bf16 else (lambda x: x)
+    f64 = [np.asarray(w(x), np.float64) for x in (feat, el, er, dz)]
+    rf, rl, rr = oracle_gat_backward(p.o, *f64[:3], 0.2, f64[3])
+    from test_gpu_random_cases import check_bound, gat_grad_bounds
+    bf, bl, br = gat_grad_bounds(p.o, *f64[:3], f64[3], 0.2)
+    rel = 1e-2 if bf16 else 1e-5
+    check_bound(gf, rf, bf, "wide head d feat", rel=rel)
+    check_bound(gl, rl, bl, "wide head d el", rel=rel)
+    check_bound(gr, rr, br, "wide head d er", rel=rel)
