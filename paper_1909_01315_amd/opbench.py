@@ -23,7 +23,7 @@ first), the achievable stream bandwidth.  Gathered tables that fit the
 256 MB Infinity Cache can exceed both; B_alg still counts them.
 edge.feat/s = E x (message columns) / time.
 
-Usage: python -m paper_1909_01315_amd.opbench [--configs c2,c3,c4,c5] [--out FILE.md]
+Usage: python -m paper_1909_01315_amd.opbench [--configs c2,c3,c3r,c4,c5] [--out FILE.md]
        [--warm W] [--reps K] [--mark]
 Every graph and input is seeded and synthetic.  Needs a GPU and the built
 library.
@@ -189,6 +189,36 @@ def c3(R: Rows):
     g.destroy()
 
 
+def c3r(R: Rows):
+    """The gated c3 operators on the same graph with each destination's
+    in-edges in random source order (synth.shuffle_within_rows): what the
+    row order contributes (the generated graphs list sources in ascending
+    order, which the segment order turns into L2 locality)."""
+    sg = synth.shuffle_within_rows(synth.graph_c3(), synth.SEED_BASE + 300)
+    g = _graph(sg)
+    N, E = sg.n_dst, sg.n_edges
+    H, F, D = 8, 16, 128
+    off = (N + 1) * 4
+    cu = dict(device="cuda")
+    X = torch.randn((N, H, F), **cu)
+    X1 = X.view(N, 1, D)
+    dZ = torch.randn((N, H, F), **cu)
+    a = torch.rand((E, H, 1), **cu)
+    Z, Z1, dX = torch.empty((N, H, F), **cu), torch.empty((N, 1, D), **cu), torch.empty((N, H, F), **cu)
+    M8 = torch.empty((E, H, 1), **cu)
+    tag = "c3 rows shuffled"
+    R.add(tag, "u_mul_e/sum H=8 F=16, attention (E,8)", "f32", "fwd",
+          E * (512 + 32 + 4) + N * 512 + off, D, E, lambda: gnnk.gspmm(g, "mul", "sum", X, a, out=Z))
+    R.add(tag, "u_dot_v H=8 F=16 -> (E,8)", "f32", "fwd",
+          E * (512 + 4 + 32) + N * 512 + off, D, E, lambda: gnnk.gsddmm(g, "dot", X, "u", X, "v", out=M8))
+    R.add(tag, "copy_u/mean D=128", "f32", "fwd",
+          E * (512 + 4) + N * 512 + off, D, E, lambda: gnnk.gspmm(g, "copy_lhs", "mean", X1, out=Z1))
+    R.add(tag, "u_mul_e/sum H=8: d feat and d attention in one reverse pass", "f32", "bwd",
+          E * (512 + 32 + 4 + 4 + 32) + N * (512 + 512) + off, D, E,
+          lambda: gnnk.gspmm_backward(g, "mul", "sum", X, a, dZ, grad_lhs=dX, grad_rhs=M8))
+    g.destroy()
+
+
 def c4(R: Rows):
     sg = synth.graph_c4()
     g = _graph(sg, ptr64=True)
@@ -245,7 +275,7 @@ def c5(R: Rows):
     g.destroy()
 
 
-CONFIGS = {"c2": c2, "c3": c3, "c4": c4, "c5": c5}
+CONFIGS = {"c2": c2, "c3": c3, "c3r": c3r, "c4": c4, "c5": c5}
 
 
 def copy_bandwidth() -> float:

@@ -225,6 +225,17 @@ C3_N, C3_E = 232965, 114600000
 C4_N, C4_E = 2449029, 61859140
 
 
+def shuffle_within_rows(g: Graph, seed: int, name: str = "row order") -> Graph:
+    """The same edges with each destination's in-edges in a seeded random
+    order instead of ascending source: edges sorted by (destination, random
+    key), edge ids renumbered to the new positions.  Rows then list their
+    sources in no particular order, as an edge list in arrival order does."""
+    key = permutation(seed, name, g.n_edges).astype(np.int64)
+    order = np.argsort((g.dst.astype(np.int64) << 32) | key, kind="stable")
+    return Graph(g.name + " (rows shuffled)", g.n_src, g.n_dst, np.ascontiguousarray(g.src[order]),
+                 np.ascontiguousarray(g.dst[order]), dict(g.extra))
+
+
 def graph_c3() -> Graph:
     return rmat_graph(SEED_BASE + 3, 18, C3_N, C3_E, name="c3")
 

@@ -113,3 +113,19 @@ def test_bf16_inputs_round_to_nearest_even():
     x = np.array([1.0, 1.00390625, 1.005859375, -2.5], dtype=np.float32)  # 1 + 2^-8 is a tie
     b = synth.to_bf16_bits(x)
     assert list(b) == [0x3F80, 0x3F80, 0x3F81, 0xC020]
+
+
+def test_shuffle_within_rows_keeps_each_rows_edges():
+    g = synth.uniform_graph(5, 300, 120, 5000)
+    r = synth.shuffle_within_rows(g, 17)
+    r2 = synth.shuffle_within_rows(g, 17)
+    assert np.array_equal(r.src, r2.src) and np.array_equal(r.dst, r2.dst)  # seeded
+    assert np.array_equal(r.dst, g.dst)  # still grouped by destination, rows in place
+    assert not np.array_equal(r.src, g.src)
+    ptr = np.concatenate([[0], np.cumsum(np.bincount(g.dst, minlength=g.n_dst))])
+    unsorted = 0
+    for v in range(g.n_dst):
+        a, b = r.src[ptr[v]:ptr[v + 1]], g.src[ptr[v]:ptr[v + 1]]
+        assert np.array_equal(np.sort(a), b)
+        unsorted += int(not np.array_equal(a, b))
+    assert unsorted > g.n_dst // 2
