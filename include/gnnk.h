@@ -105,10 +105,11 @@ typedef struct {
     int32_t identity_eids;  /* 1 when edge id == in-CSR position */
     int64_t max_in_degree, max_out_degree;
     int64_t empty_dst_rows, empty_src_rows;
-    int64_t seg_edges;      /* edges per segment of a hub row */
-    int64_t hub_dst_rows, hub_src_rows;   /* rows longer than seg_edges */
+    int64_t seg_edges;      /* edges per segment of a hub row of the in-CSR */
+    int64_t hub_dst_rows, hub_src_rows;   /* rows longer than their CSR's segment size */
     int64_t segments_in, segments_out;    /* segments of those rows */
     size_t workspace_bytes;
+    int64_t seg_edges_out;  /* edges per segment of a hub row of the reverse graph's CSR */
 } gnnk_graph_info;
 
 /* ------------------------------------------------------------------------ */
@@ -365,9 +366,11 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
  * associative reducers).  Process-wide; "seg_edges" applies to graphs created
  * afterwards, the others to calls issued afterwards.  Keys:
  *   "seg_edges"   edges per hub-row segment: 0 (default) chooses per graph
- *                 the next power of two of num_edges / 2048 within [64, 2048]
- *                 (small graphs split their long rows across more
- *                 wavefronts); otherwise a fixed value in [32, 2^30]
+ *                 the next power of two of num_edges / 8192 within [64, 512]
+ *                 for the in-CSR and of num_edges / 2048 within [64, 2048]
+ *                 for the reverse graph's CSR (small graphs split their long
+ *                 rows across more wavefronts); otherwise a fixed value in
+ *                 [32, 2^30] for both
  *   "no_split"    1: never split a row across waves (hub rows run whole)
  *   "small_deg"   rows of at most this many edges take one lane group each
  *                 and share a wavefront (-1 = auto: 32, or the lane groups

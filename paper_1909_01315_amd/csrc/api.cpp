@@ -149,12 +149,14 @@ CsrDev csr_of(const gnnk_graph* g, const Dir& d) {
     return c;
 }
 
-SchedDev schedule(const Dir& d, const Geo& geo, bool fill_empty) {
+// hub_above >= 0: the hub rows are the rows longer than hub_above, taken
+// whole (a kernel that gives each one a workgroup, with no segments)
+SchedDev schedule(const Dir& d, const Geo& geo, bool fill_empty, int64_t hub_above = -1) {
     SchedDev s{};
     const Options& o = options();
     const bool split = o.no_split == 0;
-    const int64_t n_hub = split ? d.n_hub : 0;
-    const int64_t n_seg = split ? d.n_seg : 0;
+    const int64_t n_hub = hub_above >= 0 ? (split ? d.count_above(hub_above) : 0) : (split ? d.n_hub : 0);
+    const int64_t n_seg = hub_above >= 0 ? 0 : (split ? d.n_seg : 0);
     // rows of at most T edges take one lane group each; automatic: 32 (at
     // least the lane groups of a wavefront), none when a wavefront is one group
     int64_t T = o.small_deg >= 0 ? o.small_deg : (geo.G > 1 ? std::max<int64_t>(geo.G, 32) : 0);
@@ -898,7 +900,10 @@ static gnnk_status softmax_common(gnnk_graph_t g, const gnnk_tensor* a, const gn
     A.out.reduce = 0;
     A.csr = csr_of(g, g->in);
     set_geo(A, geo);
-    A.sch = schedule(g->in, geo, false);
+    // a workgroup of its own for every row of more than 2048 in-edges (or
+    // the graph's segment size, when larger); shorter rows by one wavefront
+    // or lane group, whatever the segment size
+    A.sch = schedule(g->in, geo, false, std::max<int64_t>(g->seg_edges, 2048));
     return launch_status(launch_softmax(A, dtype_code(a), geo.vec, backward, stream), "edge softmax launch");
 }
 

@@ -45,10 +45,15 @@ Options& options() {
     return o;
 }
 
-int64_t seg_edges_for(int64_t E) {
+int64_t seg_edges_for(int64_t E, bool reverse) {
     if (options().seg_edges > 0) return options().seg_edges;
+    // in-CSR segments of 512 edges: on the 114.6M-edge graph the gathers of
+    // the in-CSR passes take 0.15-0.37 ms less each than with 2048 (more of
+    // every hub row runs in narrow, source-ordered pieces); the reverse
+    // passes gain nothing from it (copy_e sums and the argmax scatter lose)
+    const int64_t cap = reverse ? 2048 : 512, div = reverse ? 2048 : 8192;
     int64_t S = 64;
-    while (S < 2048 && S * 2048 < E) S <<= 1;
+    while (S < cap && S * div < E) S <<= 1;
     return S;
 }
 
@@ -305,9 +310,9 @@ struct Builder {
         std::vector<int32_t>& hin = in.hub_host;
         std::vector<int32_t>& hout = out.hub_host;
         schedule_host(in, g->seg_edges, hin);
-        schedule_host(out, g->seg_edges, hout);
-        L = make_layout(g->n_src, g->n_dst, E, g->ptr64 ? 8 : 4, g->seg_edges, in.n_hub, out.n_hub, in.n_seg,
-                        out.n_seg);
+        schedule_host(out, g->seg_edges_out, hout);
+        L = make_layout(g->n_src, g->n_dst, E, g->ptr64 ? 8 : 4, std::min(g->seg_edges, g->seg_edges_out), in.n_hub,
+                        out.n_hub, in.n_seg, out.n_seg);
         if (ws_bytes < L.total)
             return fail(GNNK_ENOMEM, "workspace of %zu bytes is smaller than the %zu bytes this graph needs",
                         ws_bytes, L.total);
@@ -320,7 +325,7 @@ struct Builder {
         chk(hipMemcpyAsync(in.hub_off, hin.data(), hin.size() * 4, hipMemcpyHostToDevice, s));
         chk(hipMemcpyAsync(out.hub_off, hout.data(), hout.size() * 4, hipMemcpyHostToDevice, s));
         chk(launch_hub_segments(in.ptr, g->ptr64, in.perm, in.hub_off, in.n_hub, g->seg_edges, in.seg, s));
-        chk(launch_hub_segments(out.ptr, g->ptr64, out.perm, out.hub_off, out.n_hub, g->seg_edges, out.seg, s));
+        chk(launch_hub_segments(out.ptr, g->ptr64, out.perm, out.hub_off, out.n_hub, g->seg_edges_out, out.seg, s));
         order_segments(in, g->n_src);
         order_segments(out, g->n_dst);
         chk(hipMemsetAsync(g->flag, 0, 4, s));
@@ -343,14 +348,16 @@ gnnk_graph* new_graph(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_
     g->n_dst = num_dst;
     g->n_edges = num_edges;
     g->ptr64 = ptr_t == GNNK_I64;
-    g->seg_edges = seg_edges_for(num_edges);
+    g->seg_edges = seg_edges_for(num_edges, false);
+    g->seg_edges_out = seg_edges_for(num_edges, true);
     return g;
 }
 
 // workspace checks shared by both constructors; fills b.W, b.L, g->flag
 gnnk_status begin_build(Builder& b, void* ws, size_t ws_bytes) {
     gnnk_graph* g = b.g;
-    b.L = make_layout(g->n_src, g->n_dst, g->n_edges, g->ptr64 ? 8 : 4, g->seg_edges, 0, 0, 0, 0);
+    b.L = make_layout(g->n_src, g->n_dst, g->n_edges, g->ptr64 ? 8 : 4, std::min(g->seg_edges, g->seg_edges_out), 0,
+                      0, 0, 0);
     if (!ws || ws_bytes < b.L.total)
         return fail(GNNK_ENOMEM, "workspace of %zu bytes is smaller than the %zu bytes this graph needs", ws_bytes,
                     b.L.total);
@@ -443,9 +450,9 @@ gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_
     if (ptr_t != GNNK_I32 && ptr_t != GNNK_I64) return fail(GNNK_EINVAL, "bad ptr type");
     // hub rows have more than S edges: at most E / S of them, and at most
     // E / S + (hub rows) <= 2 E / S segments
-    int64_t S = seg_edges_for(num_edges);
-    int64_t hub = num_edges / S + 1, seg = max_segments(num_edges, S);
-    Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, S, hub, hub, seg, seg);
+    const int64_t Si = seg_edges_for(num_edges, false), So = seg_edges_for(num_edges, true);
+    Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, std::min(Si, So), num_edges / Si + 1,
+                           num_edges / So + 1, max_segments(num_edges, Si), max_segments(num_edges, So));
     *bytes = L.total;
     return GNNK_OK;
 }
@@ -501,6 +508,7 @@ gnnk_status graph_info(gnnk_graph_t g, gnnk_graph_info* info) {
     info->empty_dst_rows = g->n_dst - g->in.n_nz;
     info->empty_src_rows = g->n_src - g->out.n_nz;
     info->seg_edges = g->seg_edges;
+    info->seg_edges_out = g->seg_edges_out;
     info->hub_dst_rows = g->in.n_hub;
     info->hub_src_rows = g->out.n_hub;
     info->segments_in = g->in.n_seg;

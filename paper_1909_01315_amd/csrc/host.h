@@ -39,7 +39,8 @@ struct gnnk_graph {
     int64_t n_src = 0, n_dst = 0, n_edges = 0;
     int ptr64 = 0;
     int identity_eids = 1;
-    int64_t seg_edges = 2048;
+    int64_t seg_edges = 512;       // edges per segment of a hub row of the in-CSR
+    int64_t seg_edges_out = 2048;  // the same for the reverse graph's CSR
     gnnk::Dir in, out;
     int32_t* flag = nullptr;  // device word for graph_validate
     size_t ws_used = 0;
@@ -68,9 +69,10 @@ struct Options {
 Options& options();
 
 // edges per hub-row segment for a graph of E edges: the option when set, else
-// the next power of two of E / 2048 within [64, 2048] -- small graphs split
-// their long rows so that enough wavefronts share the work
-int64_t seg_edges_for(int64_t E);
+// for the in-CSR the next power of two of E / 8192 within [64, 512], for the
+// reverse graph's CSR the next power of two of E / 2048 within [64, 2048] --
+// small graphs split their long rows so that enough wavefronts share the work
+int64_t seg_edges_for(int64_t E, bool reverse);
 
 gnnk_status fail(gnnk_status st, const char* fmt, ...);
 gnnk_status hip_fail(hipError_t e, const char* what);

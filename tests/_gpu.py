@@ -99,15 +99,16 @@ def check_formats(p, seg_edges=None):
     assert_exact(p.g.in_degrees(), ind.astype(np.int32), "in-degrees")
     assert_exact(p.g.out_degrees(), outd.astype(np.int32), "out-degrees")
     info = p.g.info()
-    if seg_edges is None:
-        seg_edges = info["seg_edges"]
+    seg_in = seg_edges if seg_edges is not None else info["seg_edges"]
+    seg_out = seg_edges if seg_edges is not None else info["seg_edges_out"]
     assert info["max_in_degree"] == (ind.max() if ind.size else 0)
     assert info["max_out_degree"] == (outd.max() if outd.size else 0)
     assert info["empty_dst_rows"] == int((ind == 0).sum())
     assert info["empty_src_rows"] == int((outd == 0).sum())
-    for deg, hub, seg in ((ind, "hub_dst_rows", "segments_in"), (outd, "hub_src_rows", "segments_out")):
-        big = deg[deg > seg_edges].astype(np.int64)
+    for deg, hub, seg, S in ((ind, "hub_dst_rows", "segments_in", seg_in),
+                             (outd, "hub_src_rows", "segments_out", seg_out)):
+        big = deg[deg > S].astype(np.int64)
         assert info[hub] == big.size, hub
-        assert info[seg] == int(((big + seg_edges - 1) // seg_edges).sum()), seg
+        assert info[seg] == int(((big + S - 1) // S).sum()), seg
     assert info["identity_eids"] == int(np.array_equal(ie, np.arange(p.o.n_edges, dtype=np.int32)))
     p.g.validate()

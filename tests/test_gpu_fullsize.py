@@ -48,7 +48,7 @@ def argmax_scatter_check(w, X, dm, ae_gpu, dXm_gpu, kind, name, seed=7):
     computed for every destination those sources' out-edges reach (the only
     ones the backward reads)."""
     rng = np.random.default_rng(seed)
-    seg = w.g.info()["seg_edges"]
+    seg = w.g.info()["seg_edges_out"]
     top = np.argsort(-w.outdeg, kind="stable")[:3]
     assert np.all(w.outdeg[top] > seg)
     big = np.nonzero((w.outdeg > 64) & (w.outdeg <= seg))[0]

@@ -204,13 +204,17 @@ def test_maximum_edge_count():
 
 
 def test_segment_size_follows_the_edge_count():
-    """seg_edges 0 (the default): the next power of two of E / 2048 within
-    [64, 2048]; a fixed option overrides it"""
-    for E, S in ((1000, 64), (200_000, 128), (1_000_000, 512), (9_000_000, 2048)):
+    """seg_edges 0 (the default): for the in-CSR the next power of two of
+    E / 8192 within [64, 512], for the reverse graph's CSR the next power of
+    two of E / 2048 within [64, 2048]; a fixed option sets both"""
+    for E, Si, So in ((1000, 64, 64), (200_000, 64, 128), (1_000_000, 128, 512), (3_000_000, 512, 2048),
+                      (9_000_000, 512, 2048)):
         src, dst = random_edges(E, 5000, 5000, E)
         p = Pair(src, dst, 5000, 5000)
-        assert p.g.info()["seg_edges"] == S, E
+        info = p.g.info()
+        assert (info["seg_edges"], info["seg_edges_out"]) == (Si, So), E
         check_formats(p)
     gnnk.set_option("seg_edges", 300)
     src, dst = random_edges(1, 50, 50, 1000)
-    assert Pair(src, dst, 50, 50).g.info()["seg_edges"] == 300
+    info = Pair(src, dst, 50, 50).g.info()
+    assert info["seg_edges"] == 300 and info["seg_edges_out"] == 300
