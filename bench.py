@@ -231,8 +231,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle's CPU timing")
     ap.add_argument("--no-c4", action="store_true", help="skip the 61.9M-edge HBM-bound reference rows")
     ap.add_argument("--mark", action="store_true",
-                    help="a one-element fill kernel before every operator of the first timed step, so that "
-                         "a counter run can tell which dispatches belong to which operator")
+                    help="a one-element fill kernel before every operator of the first timed step and after its "
+                         "last one, and around the 12 calls of each 61.9M-edge row, so that a counter run can tell "
+                         "which dispatches belong to which operator")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the library has no multi-GPU path (asked for --gpus {args.gpus}); "
@@ -321,6 +322,8 @@ def main():
             fn()
             if record:
                 evs[i + 1].record(stream)
+        if marked:
+            mark.fill_(len(ops) + 1)
 
     log(f"warmup {args.warmup} steps")
     for _ in range(args.warmup):
@@ -398,6 +401,8 @@ def main():
             if mark is not None:
                 mark.fill_(len(rows) + 1)
             t = timed_events(fn, stream, reps=10, warm=2)
+            if mark is not None:
+                mark.fill_(len(rows) + 1)
             rows.append(roofline_row(name, t * 1e3, bh, bg, traffic.get(name), ceil4, ceil4_what))
             log(f"  {name:48s} {t * 1e3:9.3f} ms")
         g4.destroy()

@@ -110,6 +110,8 @@ typedef struct {
     int64_t segments_in, segments_out;    /* segments of those rows */
     size_t workspace_bytes;
     int64_t seg_edges_out;  /* edges per segment of a hub row of the reverse graph's CSR */
+    int64_t seg_edges_gather; /* the same for the reverse passes that gather node rows */
+    int64_t segments_gather;  /* the segments of that finer table */
 } gnnk_graph_info;
 
 /* ------------------------------------------------------------------------ */
@@ -368,9 +370,10 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
  *   "seg_edges"   edges per hub-row segment: 0 (default) chooses per graph
  *                 the next power of two of num_edges / 8192 within [64, 512]
  *                 for the in-CSR and of num_edges / 2048 within [64, 2048]
- *                 for the reverse graph's CSR (small graphs split their long
- *                 rows across more wavefronts); otherwise a fixed value in
- *                 [32, 2^30] for both
+ *                 for the reverse graph's CSR, and for the reverse passes that
+ *                 gather node rows of num_edges / 16384 within [64, 256]
+ *                 (small graphs split their long rows across more
+ *                 wavefronts); otherwise a fixed value in [32, 2^30] for all
  *   "no_split"    1: never split a row across waves (hub rows run whole)
  *   "small_deg"   rows of at most this many edges take one lane group each
  *                 and share a wavefront (-1 = auto: 32, or the lane groups
@@ -385,6 +388,12 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
  *   "edge_chunk"  positions per lane group of edge-parallel walks (0 auto)
  *   "no_fast"     1: run every call on the kernels that read operand layouts
  *                 at run time (no compile-time specialised walks)
+ *   "fused_dw"    where the weight gradient of u_mul_e/sum (a per-head or
+ *                 per-edge weight, both gradients asked for) is formed:
+ *                 1: by the reverse pass that forms dX (one scattered record
+ *                 per edge); 0: by a g-SDDMM pass of its own over the in-CSR;
+ *                 -1 (default): fused for a weight of one column per edge,
+ *                 a pass of its own for per-head weights
  * Returns GNNK_EINVAL for an unknown key or value. */
 gnnk_status gnnk_set_option(const char* key, int64_t value);
 

@@ -520,7 +520,7 @@ gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags,
     if (flags & ~(GNNK_SCRATCH_ARGMAX | GNNK_SCRATCH_WIDE_SUMS)) return fail(GNNK_EINVAL, "unknown flags");
     auto al = [](size_t n) { return (n + 255) / 256 * 256; };
     const size_t C = (size_t)max_cols, E = (size_t)g->n_edges;
-    const size_t si = (size_t)g->in.n_seg, so = (size_t)g->out.n_seg;
+    const size_t si = (size_t)g->in.n_seg, so = (size_t)std::max(g->out.n_seg, g->out_fine.n_seg);
     // sums and their gradients: fp64 partials of hub segments (either CSR)
     size_t need = al(std::max(si, so) * C * 8);
     // max / min: value, edge and neighbour per segment and column
@@ -703,9 +703,17 @@ static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce redu
             A.mask_ld = words;
         }
         // u_mul_e/sum with a per-head or per-edge weight: the weight's
-        // gradient dZ[v] . X[u] in the same reverse pass (the pass has dZ[v]
-        // in its lanes and X[u] is the row's own), written at the edge id
-        const bool want_dw = grad_rhs && g->n_edges > 0 && op == GNNK_MUL && reduce == GNNK_SUM && rhs->feat == 1 &&
+        // gradient dZ[v] . X[u] can come from the same reverse pass (the
+        // pass has dZ[v] in its lanes and X[u] is the row's own), written at
+        // the edge id, one scattered record per edge.  A g-SDDMM of its own
+        // over the in-CSR writes the records in order but gathers X again.
+        // On the 114.6M-edge graph at 128 columns: with 8 heads the two
+        // passes take 5.06 + 3.76 ms against 9.26 ms fused (32-byte
+        // records); with one weight per edge 5.06 + 3.00 against 7.55 fused
+        // (4-byte records).  So by default only a one-column weight is fused.
+        const int64_t fz = options().fused_dw;
+        const bool want_dw = (fz == 1 || (fz < 0 && rhs && rhs->heads == 1)) && grad_rhs && g->n_edges > 0 &&
+                             op == GNNK_MUL && reduce == GNNK_SUM && rhs->feat == 1 &&
                              (rhs->heads == Hm || rhs->heads == 1) && lhs->heads == Hm && lhs->feat == Fm;
         if (want_dw) {
             A.x2 = lhs->data;
@@ -715,7 +723,9 @@ static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce redu
             A.per_head2 = rhs->heads > 1 ? 1 : 0;
             A.red2 = A.per_head2 ? Fm / geo.vec : (int32_t)geo.NV;
         }
-        st = run_spmm_sum(g, g->out, A, geo, dt, opk, stream, sc, want_dw ? &dw_done : nullptr);
+        // node rows gathered in the finer segments; the argmax scatter, which
+        // reads its masks in order and gathers few rows, keeps the coarse ones
+        st = run_spmm_sum(g, cmp ? g->out : g->out_fine, A, geo, dt, opk, stream, sc, want_dw ? &dw_done : nullptr);
         if (st != GNNK_OK) return st;
     }
     if (grad_rhs && g->n_edges > 0 && !dw_done) {
@@ -868,8 +878,13 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
         if (st != GNNK_OK) return st;
         A.flags = flags;
         Scratch sc = scratch_of(g, stream);
+        // a pass over the reverse graph that gathers node rows (the other
+        // operand of mul/div/dot) takes the finer segments; copy_e sums the
+        // coarse ones
+        const bool gathers = (A.a.target == T_NBR && A.a.full) || (A.b.data && A.b.target == T_NBR && A.b.full);
         if (tx == GNNK_EDGE) st = run_sddmm(g, A, geo, dt, opk, stream, sc);
-        else st = run_spmm_sum(g, tx == GNNK_SRC ? g->out : g->in, A, geo, dt, opk, stream, sc);
+        else st = run_spmm_sum(g, tx == GNNK_SRC ? (gathers ? g->out_fine : g->out) : g->in, A, geo, dt, opk, stream,
+                               sc);
         if (st != GNNK_OK) return st;
     }
     return GNNK_OK;
@@ -998,9 +1013,9 @@ static gnnk_status gat_bwd_run(gnnk_graph_t g, const gnnk_tensor* feat, const gn
     ain.csr = csr_of(g, g->in);
     set_geo(ain, geo);
     ain.sch = schedule(g->in, geo, true);
-    aout.csr = csr_of(g, g->out);
+    aout.csr = csr_of(g, g->out_fine);
     set_geo(aout, geo);
-    aout.sch = schedule(g->out, geo, true);
+    aout.sch = schedule(g->out_fine, geo, true);
     const size_t pa = (size_t)ain.sch.n_seg * 3 * H * 8, pb = (size_t)aout.sch.n_seg * (geo.D + H) * 8;
     double* part = reinterpret_cast<double*>(sc.take(std::max(pa, pb) + 8));
     if (!part) return scratch_fail(sc);

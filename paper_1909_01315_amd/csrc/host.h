@@ -41,7 +41,11 @@ struct gnnk_graph {
     int identity_eids = 1;
     int64_t seg_edges = 512;       // edges per segment of a hub row of the in-CSR
     int64_t seg_edges_out = 2048;  // the same for the reverse graph's CSR
+    int64_t seg_edges_fine = 256;  // the reverse graph's CSR for passes that gather node rows
     gnnk::Dir in, out;
+    // the reverse graph's CSR with segments of seg_edges_fine edges (its own
+    // hub tables and segment order, every other array shared with `out`)
+    gnnk::Dir out_fine;
     int32_t* flag = nullptr;  // device word for graph_validate
     size_t ws_used = 0;
     // scratch buffers the caller lent to the handle, one per stream
@@ -65,6 +69,7 @@ struct Options {
     int64_t no_fast = 0;  // 1: every call uses the runtime-layout kernels
     int64_t schedule = 0; // 0 auto, 1 row engine, 2 edge-parallel, 3 edge-parallel with atomics
     int64_t edge_chunk = 0; // positions per lane group of edge-parallel walks, 0 = auto
+    int64_t fused_dw = -1;  // u_mul_e/sum's weight gradient inside the reverse dX pass: 1 always, 0 never, -1 one-column weights
 };
 Options& options();
 
@@ -73,6 +78,10 @@ Options& options();
 // reverse graph's CSR the next power of two of E / 2048 within [64, 2048] --
 // small graphs split their long rows so that enough wavefronts share the work
 int64_t seg_edges_for(int64_t E, bool reverse);
+// the finer segment size of the reverse graph's CSR (passes that gather node
+// rows): the option when set, else the next power of two of E / 16384 within
+// [64, 256]
+int64_t seg_edges_fine_for(int64_t E);
 
 gnnk_status fail(gnnk_status st, const char* fmt, ...);
 gnnk_status hip_fail(hipError_t e, const char* what);

@@ -34,6 +34,7 @@ def reset_options():
     gnnk.set_option("seg_edges", 0)
     gnnk.set_option("no_split", 0)
     gnnk.set_option("small_deg", -1)
+    gnnk.set_option("fused_dw", -1)
 
 
 def feats(seed, name, shape, lo=None, hi=None):
@@ -251,11 +252,15 @@ def test_gsddmm_dot(c1, shape, lt, rt):
 
 @pytest.mark.parametrize("shapes", [((2, 32), (2, 1)), ((1, 64), (1, 1)), ((8, 16), (8, 1)), ((8, 16), (1, 1))])
 @pytest.mark.parametrize("seg", [2048, 64])
-def test_edge_gradient_in_the_reverse_pass_is_bit_identical(shapes, seg):
-    """u_mul_e/sum backward with both gradients computes the edge-weight
-    gradient inside the reverse pass (64+ columns); alone it is a g-SDDMM.
-    Both sum the same fp64 products in the same lane order: bit-identical."""
+@pytest.mark.parametrize("fused", [1, 0, -1])
+def test_edge_gradient_in_the_reverse_pass_is_bit_identical(shapes, seg, fused):
+    """u_mul_e/sum backward with both gradients: with the option fused_dw = 1
+    the edge-weight gradient is computed inside the reverse pass (64+
+    columns), with 0 (and alone) it is a g-SDDMM, with -1 (the default) the
+    first for one weight per edge and the second for per-head weights.  Both sum the same fp64 products
+    in the same lane order: bit-identical."""
     gnnk.set_option("seg_edges", seg)
+    gnnk.set_option("fused_dw", fused)
     sg = synth.graph_c2()
     p = Pair.of(sg)
     (xh, xf), (wh, wf) = shapes
