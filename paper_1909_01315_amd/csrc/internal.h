@@ -241,6 +241,22 @@ hipError_t launch_inverse(const int32_t* perm, int64_t n, int32_t* pos, hipStrea
 hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, int64_t ld,
                               const int32_t* pos_of_edge, uint32_t* bits, int64_t n_edges, int32_t words,
                               hipStream_t s);
+// The same masks built row by row (winner_rows_kernel) for a graph with
+// identity edge ids: units are the n_seg hub segments of the in-CSR, then its
+// rows perm[n_hub .. n_hub + n_small).  An arg names an edge of its own row
+// or nothing.
+struct WinnerRowsArgs {
+    const int32_t* arg;   // (n_dst rows, ld) winning edge ids
+    int64_t ld;
+    int32_t D, words;
+    const void* ptr;      // in-CSR row offsets (int32 or int64)
+    const int32_t* perm;  // rows by descending degree
+    const int4* seg;      // hub segments (row, begin, end, k)
+    int64_t n_seg, n_hub, n_small;
+    const int32_t* pos;   // reverse-CSR position of each edge id
+    uint32_t* bits;       // n_edges * words, zeroed here first
+};
+hipError_t launch_winner_rows(const WinnerRowsArgs& a, int ptr64, int64_t n_edges, hipStream_t s);
 hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int64_t n, hipStream_t s);
 
 // ----- device construction of the graph formats (build.hip) -----

@@ -135,6 +135,69 @@ __global__ __launch_bounds__(256) void winner_bits_kernel(const int32_t* arg_e, 
     }
 }
 
+// Winner masks by destination row, for identity edge ids (the in-CSR
+// position of an edge is its id): one wavefront per unit of the in-CSR (a hub
+// row's segment, or a whole smaller row), taking the unit's edges 64 at a
+// time, one per lane, with the edge's reverse-CSR position loaded first.  The
+// lanes scan the row's arg array, four 32-column words at a time: the winner
+// of a column less the chunk's first position is the lane of the edge that
+// won it, whose LDS word gets the column's bit.  Then every edge of the chunk
+// that won a column stores its words at its reverse-CSR position; the rest
+// stay as zeroed before.  An arg that names no edge of its own row matches
+// nothing, as the gradient's definition has it.  An edge's words are written
+// by the one wavefront that holds it and an OR does not depend on its order:
+// no global atomics, and the result is fixed.  Against winner_bits_kernel it
+// reads the positions of a row's edges in order and stores whole masks, where
+// that one looks up a position and stores a word per winning column; it
+// rescans the arg row for every 64 edges, so it suits rows short against D.
+constexpr int WIN_WB = 4;
+
+template <typename P>
+__global__ __launch_bounds__(64) void winner_rows_kernel(WinnerRowsArgs a) {
+    __shared__ uint4 lds[64];  // WIN_WB words per lane's edge
+    uint32_t* ldw = reinterpret_cast<uint32_t*>(lds);
+    const int lane = threadIdx.x;
+    const int64_t n_units = a.n_seg + a.n_small;
+    const P* ptr = static_cast<const P*>(a.ptr);
+    for (int64_t u = blockIdx.x; u < n_units; u += gridDim.x) {
+        int64_t v, b, e;
+        if (u < a.n_seg) {
+            const int4 sg = a.seg[u];
+            v = sg.x, b = sg.y, e = sg.z;
+        } else {
+            v = a.perm[a.n_hub + (u - a.n_seg)];
+            b = (int64_t)ptr[v], e = (int64_t)ptr[v + 1];
+        }
+        const int32_t* arow = a.arg + v * a.ld;
+        for (int64_t c0 = b; c0 < e; c0 += 64) {
+            const int nv = (int)(e - c0 < 64 ? e - c0 : 64);
+            const int32_t p = lane < nv ? a.pos[c0 + lane] : 0;
+            for (int w0 = 0; w0 < a.words; w0 += WIN_WB) {
+                const int wb = a.words - w0 < WIN_WB ? a.words - w0 : WIN_WB;
+                lds[lane] = make_uint4(0u, 0u, 0u, 0u);
+                __syncthreads();
+                const int cend = (w0 + wb) * 32 < a.D ? (w0 + wb) * 32 : a.D;
+                for (int c = w0 * 32 + lane; c < cend; c += 64) {
+                    const int64_t k = (int64_t)arow[c] - c0;
+                    if (k >= 0 && k < nv) atomicOr(&ldw[k * WIN_WB + ((c >> 5) - w0)], 1u << (c & 31));
+                }
+                __syncthreads();
+                const uint4 m = lds[lane];
+                if (lane < nv && (m.x | m.y | m.z | m.w) != 0u) {
+                    uint32_t* dst = a.bits + (int64_t)p * a.words + w0;
+                    if (wb == WIN_WB && (a.words & (WIN_WB - 1)) == 0) {
+                        *reinterpret_cast<uint4*>(dst) = m;
+                    } else {
+                        const uint32_t mw[WIN_WB] = {m.x, m.y, m.z, m.w};
+                        for (int i = 0; i < wb; ++i) dst[i] = mw[i];
+                    }
+                }
+                __syncthreads();
+            }
+        }
+    }
+}
+
 __global__ void iota_kernel(int32_t* out, int64_t n) {
     for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
         out[i] = (int32_t)i;
@@ -237,6 +300,16 @@ hipError_t launch_winner_bits(const int32_t* arg_e, int64_t n_rows, int32_t D, i
     if (n > 0)
         hipLaunchKernelGGL(winner_bits_kernel, dim3(grid_1d(n_rows * words * 32)), dim3(256), 0, s, arg_e, n_rows,
                            D, ld, pos_of_edge, bits, words, n_edges);
+    return hipGetLastError();
+}
+
+hipError_t launch_winner_rows(const WinnerRowsArgs& a, int ptr64, int64_t n_edges, hipStream_t s) {
+    const int64_t nw = n_edges * a.words, units = a.n_seg + a.n_small;
+    if (nw > 0) hipLaunchKernelGGL(zero_words_kernel, dim3(grid_1d(nw)), dim3(256), 0, s, a.bits, nw);
+    if (units <= 0 || a.D <= 0) return hipGetLastError();
+    const dim3 grid((unsigned)(units < 65536 ? units : 65536));
+    if (ptr64) hipLaunchKernelGGL(winner_rows_kernel<int64_t>, grid, dim3(64), 0, s, a);
+    else hipLaunchKernelGGL(winner_rows_kernel<int32_t>, grid, dim3(64), 0, s, a);
     return hipGetLastError();
 }
 

@@ -219,6 +219,31 @@ def test_max_ties_from_multi_edges(c1):
     assert_exact(ae, rae)
 
 
+@pytest.mark.parametrize("ident", [True, False])
+@pytest.mark.parametrize("seg", [0, 64])
+@pytest.mark.parametrize("D", [16, 100, 300, 512])
+def test_argmax_scatter_masks(hot, ident, seg, D):
+    """The max/min backward's winner masks, built row by row when edge ids are
+    the in-CSR positions (the hot graph's edges sorted by destination) and by
+    winning column otherwise: hub rows cut into 64-edge segments (seg 64) or
+    whole, and mask widths of one to sixteen words (partial blocks of four):
+    the gradient against the oracle."""
+    gnnk.set_option("seg_edges", seg)
+    src, dst = hot.o.src, hot.o.dst
+    if ident:
+        order = np.argsort(dst, kind="stable")
+        src, dst = src[order], dst[order]
+    p = Pair(src, dst, 300, 300)
+    assert p.g.info()["identity_eids"] == int(ident)
+    X = feats(S1, f"amX{D}", (300, 1, D))
+    dZ = feats(G1, f"amdZ{D}", (300, 1, D))
+    for red in ("max", "min"):
+        _, _, ae = orc.gspmm(p.o, "copy_lhs", red, X)
+        ref, _ = orc.gspmm_backward(p.o, "copy_lhs", red, X, None, dZ, arg_e=ae, want_rhs=False)
+        dX, _ = gnnk.gspmm_backward(p.g, "copy_lhs", red, dev(X), None, dev(dZ), arg_rhs=dev(ae))
+        assert_close(dX, ref, name=f"{red} D={D}")
+
+
 # ---------------------------------------------------------------------------
 # A3: g-SDDMM forward
 
