@@ -17,7 +17,8 @@
 //     sub-chunk order;
 //   mode 1 (atomic, order not fixed): fp64 atomic adds into a zeroed
 //     rows x D scratch, then spmm_edge_finish_kernel rounds the split rows.
-// g-SDDMM has no reduction: every position is independent, and both
+// g-SDDMM has no reduction: every position is independent, so the positions
+// are dealt out flat, consecutive ones to consecutive lane groups, and both
 // endpoints are read per edge (no row-level reuse of the destination
 // operand, which is what the row engine gains on CSR).
 #include "walk.h"
@@ -207,19 +208,37 @@ __global__ __launch_bounds__(256) void spmm_edge_finish_kernel(EngineArgs A, int
     }
 }
 
-// g-SDDMM, one output per position, both endpoints read per edge
+// ids of slot u of lane group g in a step of G * UNR positions from q: slot
+// u of every group lies on G consecutive positions q + u * G + g, so one
+// store instruction of the wavefront covers consecutive outputs; slots past
+// n_pos read position q (in bounds) and are dropped
+__device__ __forceinline__ void flat_ids(const CsrDev& C, int64_t q, int64_t n_pos, int G, int g, bool* ok,
+                                         int32_t* nb, int32_t* ed, int32_t* rw, int32_t* ps) {
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+        const int64_t p = q + (int64_t)u * G + g;
+        ok[u] = p < n_pos;
+        const int32_t pc = (int32_t)(ok[u] ? p : q);
+        ps[u] = pc;
+        nb[u] = C.idx[pc];
+        ed[u] = C.eid ? C.eid[pc] : pc;
+        rw[u] = C.row[pc];
+    }
+}
+
+// g-SDDMM, one output per position, both endpoints read per edge.  The
+// positions are dealt out flat: a wavefront takes G * UNR consecutive ones
+// per step (grid-stride), so every lane group has the same work and the
+// outputs of a step are written as one contiguous stretch (with identity
+// edge ids).  No reduction crosses lane groups, so no sub-chunks are needed.
 template <typename T, int VEC, int OPK, int EXT, int RM, class S>
 __global__ __launch_bounds__(256) void sddmm_edge_kernel(EngineArgs A, int64_t n_pos) {
     const GeomDev& geo = A.geo;
     const Lanes ln = lanes_of<S::GC>(geo);
     const int G = S::GC > 0 ? S::GC : geo.G;
     const int L = WAVE / G;
-    const int64_t k = (int64_t)wave_id() * G + ln.g;
-    // lane groups past the end still run the loop with no valid slot, so the
-    // lanes of a group stay together for the cross-lane sums
-    int32_t sb, se;
-    sub_range(A, k < A.n_sub ? k : A.n_sub - 1, n_pos, sb, se);
-    if (k >= A.n_sub) se = sb;
+    const int64_t per = (int64_t)G * UNR;
+    const int64_t stride = (int64_t)gridDim.x * WPB * per;
     using SN = Spec<S::AT, S::AK, S::BT, S::BK, S::GC, false, false>;
     const bool neg = (A.flags & F_NEGATE) != 0;
     for (int ch = 0; ch < geo.nchunk; ++ch) {
@@ -230,8 +249,8 @@ __global__ __launch_bounds__(256) void sddmm_edge_kernel(EngineArgs A, int64_t n
         Pre<VEC> pre;
         int32_t nb[UNR], ed[UNR], rw[UNR], ps[UNR];
         bool ok[UNR];
-        for (int32_t p0 = sb; p0 < se; p0 += UNR) {
-            coo_ids(A.csr, sb, se, p0, ok, nb, ed, rw, ps);
+        for (int64_t q = (int64_t)wave_id() * per; q < n_pos; q += stride) {
+            flat_ids(A.csr, q, n_pos, G, ln.g, ok, nb, ed, rw, ps);
             Raw<VEC> r[UNR];
 #pragma unroll
             for (int u = 0; u < UNR; ++u) fetch_bits<VEC, EXT>(A, ps[u], col0, r[u]);
@@ -372,10 +391,13 @@ hipError_t launch_spmm_edge(const EngineArgs& a, int64_t n_pos, int64_t n_rows, 
 
 hipError_t launch_sddmm_edge(const EngineArgs& a, int64_t n_pos, int dtype, int vec, int opk, int spec, int gc,
                              hipStream_t s) {
-    if (a.n_sub <= 0) return hipSuccess;
+    if (n_pos <= 0) return hipSuccess;
     const int ext = ext_of(a.flags);
     const dim3 block(WAVE * WPB);
-    const dim3 grid(blocks_for_waves((a.n_sub + a.geo.G - 1) / a.geo.G));
+    // one step of G * UNR positions per wavefront, at most 16384 blocks
+    // (grid-stride beyond)
+    const int64_t waves = (n_pos + (int64_t)a.geo.G * UNR - 1) / ((int64_t)a.geo.G * UNR);
+    const dim3 grid(blocks_for_waves(waves < 16384 * WPB ? waves : 16384 * WPB));
     if (dtype == 0) {
         GNNK_VEC_DISPATCH_F32(vec, sddmm_edge_t<float, V>(a, n_pos, opk, ext, spec, gc, grid, block, s))
     } else {
