@@ -166,11 +166,19 @@ __device__ __forceinline__ void softmax_pass_write(const EngineArgs& A, int64_t 
     }
 }
 
-// The same passes for a hub row with the first K unrolled steps of each lane
-// kept in registers between them: the write pass takes those edges' operands
-// (the backward's attention and its gradient) from the registers instead of
+// The same passes with the first K unrolled steps of each lane kept in
+// registers between them: the write pass takes those edges' operands (the
+// backward's attention and its gradient) from the registers instead of
 // reading them again.  A lane walks the same positions in the same order in
 // both passes, so the results are those of the uncached passes, bit for bit.
+// The backward (two operands, eight fp32 values per edge and lane at VEC = 4)
+// keeps two steps: c3 softmax backward 2.63 -> 2.53 ms on the hub rows, 2.54
+// -> 2.49 ms with the other rows too.  The forward keeps none: one to four
+// steps made it slower (1.80 -> 1.98-2.05 ms; the registers cost more
+// occupancy than the second read costs), and wider lanes (VEC = 8) would
+// spill.
+__host__ __device__ constexpr int hub_cache_steps(bool backward, int vec) { return backward && vec <= 4 ? 2 : 0; }
+
 template <typename T, int VEC, int K>
 struct RowCache {
     float s[K > 0 ? K : 1][SM_UNROLL][VEC];
@@ -221,13 +229,14 @@ __device__ __forceinline__ void softmax_pass_write_cached(const EngineArgs& A, i
     float inv[VEC];
 #pragma unroll
     for (int i = 0; i < VEC; ++i) inv[i] = backward ? 0.0f : (float)(1.0 / sum[i]);
+    const bool nt = stride > 1;
     int64_t p = b + start;
 #pragma unroll
     for (int k = 0; k < K; ++k) {
         if (k < c.n) {
 #pragma unroll
             for (int u = 0; u < U; ++u)
-                softmax_out<T, VEC>(A, edge_at(A, p + (int64_t)u * stride), col0, active, true, c.s[k][u], c.g[k][u],
+                softmax_out<T, VEC>(A, edge_at(A, p + (int64_t)u * stride), col0, active, nt, c.s[k][u], c.g[k][u],
                                     mx, sum, inv, backward);
             p += (int64_t)U * stride;
         }
@@ -268,6 +277,9 @@ __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
         double sum[VEC];
 #pragma unroll
         for (int i = 0; i < VEC; ++i) { mx[i] = -INFINITY; sum[i] = 0.0; }
+        constexpr int KC = hub_cache_steps(BWD, VEC);
+        RowCache<T, VEC, KC> rc;
+        if constexpr (KC > 0) softmax_pass_first_cached<T, VEC, KC, BWD>(A, b, e, start, stride, col0, mx, sum, rc);
         if (!BWD) {
             softmax_pass_online<T, VEC>(A, b, e, start, stride, col0, mx, sum);
             if (coop)
@@ -276,26 +288,21 @@ __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
                     for (int i = 0; i < VEC; ++i)
                         softmax_merge(mx[i], sum[i], __shfl_xor(mx[i], s, WAVE), shfl_xor_d(sum[i], s));
         } else {
-            softmax_pass_dot<T, VEC>(A, b, e, start, stride, col0, sum);
+            if constexpr (KC == 0) softmax_pass_dot<T, VEC>(A, b, e, start, stride, col0, sum);
             if (coop)
                 for (int s = geo.L; s < WAVE; s <<= 1)
 #pragma unroll
                     for (int i = 0; i < VEC; ++i) sum[i] += shfl_xor_d(sum[i], s);
         }
-        softmax_pass_write<T, VEC>(A, b, e, start, stride, col0, active, mx, sum, BWD);
+        if constexpr (KC > 0) softmax_pass_write_cached<T, VEC, KC>(A, b, e, start, stride, col0, active, mx, sum, BWD, rc);
+        else softmax_pass_write<T, VEC>(A, b, e, start, stride, col0, active, mx, sum, BWD);
     }
 }
 
 // wavefronts per hub row: c3 (114.6M edges, (E,8) fp32) softmax takes
 // 2.03 / 1.80 / 2.87 ms with 4 / 8 / 16 (backward 2.97 / 2.70 / 2.78 ms)
 constexpr int HUB_WAVES = 8;
-// Unrolled steps per lane held in registers between the two passes of a hub
-// row.  The backward (two operands, eight fp32 values per edge and lane at
-// VEC = 4) keeps two: c3 softmax backward 2.63 -> 2.53 ms.  The forward
-// keeps none: one to four steps made it slower (1.80 -> 1.98-2.05 ms; the
-// registers cost more occupancy than the second read costs), and wider
-// lanes (VEC = 8) would spill.
-__host__ __device__ constexpr int hub_cache_steps(bool backward, int vec) { return backward && vec <= 4 ? 2 : 0; }
+
 
 // hub row perm[blockIdx.x]: the lane groups of all HUB_WAVES wavefronts
 // stride over the row; each wavefront merges its lane groups by shuffles,
