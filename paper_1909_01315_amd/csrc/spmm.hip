@@ -172,7 +172,12 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
     }
 }
 
-// combine the segment partials of hub rows, in segment order
+// combine the segment partials of hub rows, in segment order.  A lane walks
+// its row's segments COMB_UNR at a time with the loads issued together: the
+// longest rows have hundreds of segments, and one load in flight per lane
+// left the combine waiting on each in turn.
+constexpr int COMB_UNR = 8;
+
 template <typename T, int VEC>
 __global__ __launch_bounds__(256) void spmm_sum_combine_kernel(EngineArgs A) {
     const int w = wave_id();
@@ -194,10 +199,23 @@ __global__ __launch_bounds__(256) void spmm_sum_combine_kernel(EngineArgs A) {
         double acc[VEC];
 #pragma unroll
         for (int i = 0; i < VEC; ++i) acc[i] = 0.0;
-        for (int s = s0; s < s1; ++s) {
-            const double* P = reinterpret_cast<const double*>(A.partial) + (int64_t)s * A.partial_stride + col0;
+        const double* P0 = reinterpret_cast<const double*>(A.partial) + col0;
+        int s = s0;
+        // COMB_UNR segments' loads in flight at once, added in segment order
+        for (; s + COMB_UNR <= s1; s += COMB_UNR) {
+            double v[COMB_UNR][VEC];
 #pragma unroll
-            for (int i = 0; i < VEC; ++i) acc[i] += P[i];
+            for (int u = 0; u < COMB_UNR; ++u)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) v[u][i] = P0[(int64_t)(s + u) * A.partial_stride + i];
+#pragma unroll
+            for (int u = 0; u < COMB_UNR; ++u)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) acc[i] += v[u][i];
+        }
+        for (; s < s1; ++s) {
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) acc[i] += P0[(int64_t)s * A.partial_stride + i];
         }
         write_sum_row<T, VEC>(A, r, active, ln.lig, col0, h, acc, deg, true, true, ch, &carry);
     }
@@ -412,19 +430,39 @@ __global__ __launch_bounds__(256) void spmm_cmp_combine_kernel(EngineArgs A) {
         int32_t be[VEC], bn[VEC];
 #pragma unroll
         for (int i = 0; i < VEC; ++i) { best[i] = 0.0f; be[i] = -1; bn[i] = -1; }
-        for (int s = s0; s < s1; ++s) {
-            const float* PV = reinterpret_cast<const float*>(A.partial) + (int64_t)s * D + col0;
-            const int32_t* PE = reinterpret_cast<const int32_t*>(A.partial) + (int64_t)A.sch.n_seg * D +
-                                (int64_t)s * D + col0;
-            const int32_t* PN = PE + (int64_t)A.sch.n_seg * D;
+        const float* PV0 = reinterpret_cast<const float*>(A.partial) + col0;
+        const int32_t* PE0 = reinterpret_cast<const int32_t*>(A.partial) + (int64_t)A.sch.n_seg * D + col0;
+        const int32_t* PN0 = PE0 + (int64_t)A.sch.n_seg * D;
+        auto take = [&](float pv, int32_t pe, int32_t pn, int i) {
+            const bool upd = (pe >= 0) & better(pv, pe, best[i], be[i], is_min);
+            best[i] = upd ? pv : best[i];
+            be[i] = upd ? pe : be[i];
+            bn[i] = upd ? pn : bn[i];
+        };
+        int s = s0;
+        // COMB_UNR segments' loads in flight at once, compared in segment order
+        for (; s + COMB_UNR <= s1; s += COMB_UNR) {
+            float pv[COMB_UNR][VEC];
+            int32_t pe[COMB_UNR][VEC], pn[COMB_UNR][VEC];
+#pragma unroll
+            for (int u = 0; u < COMB_UNR; ++u)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) {
+                    const int64_t o = (int64_t)(s + u) * D + i;
+                    pv[u][i] = PV0[o];
+                    pe[u][i] = PE0[o];
+                    pn[u][i] = PN0[o];
+                }
+#pragma unroll
+            for (int u = 0; u < COMB_UNR; ++u)
+#pragma unroll
+                for (int i = 0; i < VEC; ++i) take(pv[u][i], pe[u][i], pn[u][i], i);
+        }
+        for (; s < s1; ++s) {
 #pragma unroll
             for (int i = 0; i < VEC; ++i) {
-                const float pv = PV[i];
-                const int32_t pe = PE[i], pn = PN[i];
-                const bool upd = (pe >= 0) & better(pv, pe, best[i], be[i], is_min);
-                best[i] = upd ? pv : best[i];
-                be[i] = upd ? pe : be[i];
-                bn[i] = upd ? pn : bn[i];
+                const int64_t o = (int64_t)s * D + i;
+                take(PV0[o], PE0[o], PN0[o], i);
             }
         }
         write_cmp_row<T, VEC>(A, r, active, col0, best, be, bn, row_ok ? row_ptr(A.csr, r) : -1);
