@@ -22,6 +22,44 @@ struct SddmmSink {
     const EngineArgs& A;
     int lig, col0, h, ch;
     bool active;
+
+    // Runs of four lanes and batches of four edges per lane group (a per-head
+    // dot of 16 fp32 columns): a full batch's four partial sums are reduced
+    // and scattered together, a 4 x 4 transpose in two DPP steps after which
+    // lane q of a run holds the total of slot q, and one store instruction
+    // writes the four outputs.  Per batch that is 3 fp64 additions and 6
+    // lane moves per lane instead of 8 and 16, and one store path instead of
+    // four (c3 u_dot_v and the d attention pass were bound by VALU issue).
+    // The sums pair up as run_sum_c<4> pairs them for each slot, lanes {0, 1}
+    // and {2, 3} and then the two pairs, so the results are bit-identical.
+    static constexpr bool kBatch = RM == 4 && UNR == 4;
+
+    __device__ __forceinline__ void batch(const Raw<VEC>* rw, const int32_t* ed) {
+        double s[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+            double m[VEC];
+            combine_f64<VEC, OPK, EXT>(A, rw[u], ed[u], m);
+            double t = 0.0;
+#pragma unroll
+            for (int i = 0; i < VEC; ++i) t += m[i];
+            s[u] = active ? t : 0.0;
+        }
+        const int q = lig & 3;
+        const bool odd = (q & 1) != 0, hi = (q & 2) != 0;
+        // with lane q ^ 1: keep the two slots of q's parity, hand over the others
+        const double k0 = (odd ? s[1] : s[0]) + dpp_d<DPP_QUAD_1032>(odd ? s[0] : s[1]);
+        const double k1 = (odd ? s[3] : s[2]) + dpp_d<DPP_QUAD_1032>(odd ? s[2] : s[3]);
+        // with lane q ^ 2: keep slot q
+        const double tot = (hi ? k1 : k0) + dpp_d<DPP_QUAD_2301>(hi ? k0 : k1);
+        if (active) {
+            const int32_t e = q == 0 ? ed[0] : (q == 1 ? ed[1] : (q == 2 ? ed[2] : ed[3]));
+            T* row = reinterpret_cast<T*>(A.out.data) + (uint64_t)(uint32_t)e * (uint32_t)A.out.stride;
+            const bool neg = (A.flags & F_NEGATE) != 0;
+            IO<T, VEC>::store1(row + (A.out.per_head ? h : 0), (float)(neg ? -tot : tot));
+        }
+    }
+
     __device__ __forceinline__ void operator()(const Raw<VEC>& rw, int32_t ed, int32_t, bool ok) {
         double m[VEC];
         combine_f64<VEC, OPK, EXT>(A, rw, ed, m);

@@ -22,6 +22,8 @@
 // for every edge of the lane group in ascending position order.
 #pragma once
 
+#include <type_traits>
+
 #include "device.h"
 
 namespace gnnk {
@@ -128,6 +130,14 @@ __device__ __forceinline__ void vload_ids(const CsrDev& C, int64_t q, int g, int
     }
 }
 
+// A consumer that takes a whole full batch at once says so with a constant
+// member kBatch = true and a method batch(r, ed) (partial batches still go
+// edge by edge).
+template <class F, class = void>
+struct TakesBatch : std::false_type {};
+template <class F>
+struct TakesBatch<F, std::void_t<decltype(F::kBatch)>> : std::integral_constant<bool, F::kBatch> {};
+
 // Hand the edges of a full batch to consume (b of a CB spec arrives by
 // ds_bpermute from the coalesced load).
 template <int VEC, int OPK, class S, class F>
@@ -141,7 +151,12 @@ __device__ __forceinline__ void take_batch(const EngineArgs& A, Raw<VEC>* r, con
 #pragma unroll
             for (int i = 0; i < VEC; ++i) r[u].b[i] = x;
         }
-        consume(r[u], ed[u], nb[u], true);
+    }
+    if constexpr (TakesBatch<F>::value) {
+        consume.batch(r, ed);
+    } else {
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) consume(r[u], ed[u], nb[u], true);
     }
 }
 
