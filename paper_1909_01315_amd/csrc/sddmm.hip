@@ -52,8 +52,10 @@ struct SddmmSink {
         const double k1 = (odd ? s[3] : s[2]) + dpp_d<DPP_QUAD_1032>(odd ? s[2] : s[3]);
         // with lane q ^ 2: keep slot q
         const double tot = (hi ? k1 : k0) + dpp_d<DPP_QUAD_2301>(hi ? k0 : k1);
+        // slot q's edge by two selects (no branches)
+        const int32_t e01 = odd ? ed[1] : ed[0], e23 = odd ? ed[3] : ed[2];
+        const int32_t e = hi ? e23 : e01;
         if (active) {
-            const int32_t e = q == 0 ? ed[0] : (q == 1 ? ed[1] : (q == 2 ? ed[2] : ed[3]));
             T* row = reinterpret_cast<T*>(A.out.data) + (uint64_t)(uint32_t)e * (uint32_t)A.out.stride;
             const bool neg = (A.flags & F_NEGATE) != 0;
             IO<T, VEC>::store1(row + (A.out.per_head ? h : 0), (float)(neg ? -tot : tot));
