@@ -55,6 +55,28 @@ __device__ __forceinline__ void online_step(float* mx, double* sum, const float*
     }
 }
 
+// U scores at once: the running sum is rescaled once to the new maximum
+// (the batch's and the old one's), then the batch's terms are added, about
+// 60% of the instructions of U single steps (c3 softmax forward ran close to
+// its VALU issue limit).  A column whose scores are all -inf so far keeps
+// (-inf, 0).
+template <int VEC, int U>
+__device__ __forceinline__ void online_batch(float* mx, double* sum, const float (*s)[VEC]) {
+#pragma unroll
+    for (int i = 0; i < VEC; ++i) {
+        float mb = s[0][i];
+#pragma unroll
+        for (int u = 1; u < U; ++u) mb = fmaxf(mb, s[u][i]);
+        const float mn = fmaxf(mx[i], mb);
+        double acc = mx[i] == -INFINITY ? 0.0 : sum[i] * (double)exp_le0(mx[i] - mn);
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc += (double)exp_le0(s[u][i] - mn);
+        const bool live = mn != -INFINITY;
+        sum[i] = live ? acc : sum[i];
+        mx[i] = mn;
+    }
+}
+
 // running (max, sum of exp(s - max)) over the edges of a lane group
 template <typename T, int VEC>
 __device__ __forceinline__ void softmax_pass_online(const EngineArgs& A, int64_t b, int64_t e, int start, int stride,
@@ -65,8 +87,7 @@ __device__ __forceinline__ void softmax_pass_online(const EngineArgs& A, int64_t
         float s[U][VEC];
 #pragma unroll
         for (int u = 0; u < U; ++u) ld_edge<T, VEC>(A.a, edge_at(A, p + (int64_t)u * stride), col0, s[u]);
-#pragma unroll
-        for (int u = 0; u < U; ++u) online_step<VEC>(mx, sum, s[u]);
+        online_batch<VEC, U>(mx, sum, s);
     }
     for (; p < e; p += stride) {
         float s[VEC];
