@@ -43,7 +43,10 @@ struct SddmmSink {
             double t = 0.0;
 #pragma unroll
             for (int i = 0; i < VEC; ++i) t += m[i];
-            s[u] = active ? t : 0.0;
+            // no masking of inactive lanes: a run is active or inactive as a
+            // whole (the row's lanes come in whole heads of four), its lanes
+            // only exchange among themselves, and inactive runs store nothing
+            s[u] = t;
         }
         const int q = lig & 3;
         const bool odd = (q & 1) != 0, hi = (q & 2) != 0;
