@@ -225,9 +225,11 @@ gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags,
 gnnk_status graph_attach_scratch(gnnk_graph_t g, hipStream_t stream, void* buf, size_t bytes);
 
 /* Bytes of scratch the last call on this thread that returned GNNK_ENOMEM for
- * lack of scratch asked for (0 after any other outcome).  A call that needs
- * several parts asks for them in turn, so a call retried with that many
- * bytes may ask for more. */
+ * lack of scratch asked for (0 after any other outcome): the whole call's
+ * need, so the same call with a buffer of that many bytes gets its scratch.
+ * A call made of several passes (gradient pairs, the max/min backward, slices
+ * of heads, the fused attention backward) is checked whole, arguments and
+ * scratch, before its first pass is launched. */
 gnnk_status gnnk_scratch_needed(size_t* bytes);
 
 /* ------------------------------------------------------------------------ */

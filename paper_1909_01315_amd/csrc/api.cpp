@@ -203,6 +203,9 @@ int64_t rows_of_target(const gnnk_graph* g, int t) {
 
 gnnk_status launch_status(hipError_t e, const char* what) { return e == hipSuccess ? GNNK_OK : hip_fail(e, what); }
 
+// a kernel launch, skipped (and not evaluated) while a call is being planned
+#define GNNK_LAUNCH(call, what) (planning() ? GNNK_OK : launch_status((call), (what)))
+
 // A node table addressed with 32-bit byte offsets by the fast kernels.
 bool fits32(const OperandDev& o, int64_t rows, int es) {
     if (!o.data) return false;
@@ -330,7 +333,7 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
             A.partial = sc.take(need);
             if (!A.partial) return scratch_fail(sc);
         }
-        gnnk_status st = launch_status(launch_spmm_edge(A, g->n_edges, d.n_rows, dtype, geo.vec, opk, pk.spec, pk.gc,
+        gnnk_status st = GNNK_LAUNCH(launch_spmm_edge(A, g->n_edges, d.n_rows, dtype, geo.vec, opk, pk.spec, pk.gc,
                                                         walk == 3 ? 1 : 0, s),
                                        "edge-parallel g-SpMM launch");
         if (st != GNNK_OK) return st;
@@ -344,19 +347,19 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
         sc.w_small_end = 0;
         sc.w_total = (int32_t)((d.n_rows - d.n_nz + (int64_t)geo.G * sc.fill_rows_per_group - 1) /
                                ((int64_t)geo.G * sc.fill_rows_per_group));
-        return launch_status(launch_spmm(F, dtype, geo.vec, false, opk, SP_DYN, 0, s), "empty-row fill launch");
+        return GNNK_LAUNCH(launch_spmm(F, dtype, geo.vec, false, opk, SP_DYN, 0, s), "empty-row fill launch");
     }
     if (A.sch.n_seg > 0) {
         A.partial = sc.take((size_t)A.sch.n_seg * geo.D * 8);
         if (!A.partial) return scratch_fail(sc);
     }
     gnnk_status st = (fused_dw && *fused_dw)
-                         ? launch_status(launch_spmm_dw(A, dtype, geo.vec, pk.spec, pk.gc, s),
+                         ? GNNK_LAUNCH(launch_spmm_dw(A, dtype, geo.vec, pk.spec, pk.gc, s),
                                          "g-SpMM launch (with the edge gradient)")
-                         : launch_status(launch_spmm(A, dtype, geo.vec, false, opk, pk.spec, pk.gc, s),
+                         : GNNK_LAUNCH(launch_spmm(A, dtype, geo.vec, false, opk, pk.spec, pk.gc, s),
                                          "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
-        st = launch_status(launch_spmm_combine(A, dtype, geo.vec, false, s), "g-SpMM combine launch");
+        st = GNNK_LAUNCH(launch_spmm_combine(A, dtype, geo.vec, false, s), "g-SpMM combine launch");
     return st;
 }
 
@@ -373,10 +376,10 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
     }
     if (pick_walk(g->in, multi)) {
         set_edge_chunks(A, g->n_edges, geo);
-        return launch_status(launch_sddmm_edge(A, g->n_edges, dtype, geo.vec, opk, pk.spec, pk.gc, s),
+        return GNNK_LAUNCH(launch_sddmm_edge(A, g->n_edges, dtype, geo.vec, opk, pk.spec, pk.gc, s),
                              "edge-parallel g-SDDMM launch");
     }
-    return launch_status(launch_sddmm(A, dtype, geo.vec, opk, pk.spec, pk.gc, s), "g-SDDMM launch");
+    return GNNK_LAUNCH(launch_sddmm(A, dtype, geo.vec, opk, pk.spec, pk.gc, s), "g-SDDMM launch");
 }
 
 int32_t tgt_in(int t) { return t == GNNK_SRC ? T_NBR : (t == GNNK_EDGE ? T_EDGE : T_SELF); }   // in-CSR walk
@@ -477,9 +480,9 @@ gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const 
         if (!A.partial) return scratch_fail(sc);
     }
     const Pick pk = pick_spmm(g, g->in, A, geo, dtype_code(out), opk, true);
-    st = launch_status(launch_spmm(A, dtype_code(out), geo.vec, true, opk, pk.spec, pk.gc, stream), "g-SpMM launch");
+    st = GNNK_LAUNCH(launch_spmm(A, dtype_code(out), geo.vec, true, opk, pk.spec, pk.gc, stream), "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
-        st = launch_status(launch_spmm_combine(A, dtype_code(out), geo.vec, true, stream), "g-SpMM combine launch");
+        st = GNNK_LAUNCH(launch_spmm_combine(A, dtype_code(out), geo.vec, true, stream), "g-SpMM combine launch");
     return st;
 }
 
@@ -694,8 +697,10 @@ static gnnk_status spmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce redu
             const int32_t words = (int32_t)((geo.D + 31) / 32);
             uint32_t* bits = reinterpret_cast<uint32_t*>(sc.take((size_t)g->n_edges * words * 4));
             if (!bits) return scratch_fail(sc);
-            hipError_t le;
-            if (g->identity_eids && g->n_edges <= 64 * g->in.n_nz) {
+            hipError_t le = hipSuccess;
+            if (planning()) {
+                // nothing is launched while planning
+            } else if (g->identity_eids && g->n_edges <= 64 * g->in.n_nz) {
                 // rows of the in-CSR (mean in-degree up to 64): the positions
                 // of a row's edges are read in order and each edge's mask is
                 // stored whole.  Longer rows win few of their columns per
@@ -795,13 +800,14 @@ gnnk_status gspmm_backward(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, co
                            hipStream_t stream) {
     clear_error();
     (void)arg_lhs;
-    return spmm_backward(g, op, reduce, lhs, rhs, arg_rhs, grad_out, grad_lhs, grad_rhs, stream, -1);
+    return planned(g, stream, [&] {
+        return spmm_backward(g, op, reduce, lhs, rhs, arg_rhs, grad_out, grad_lhs, grad_rhs, stream, -1);
+    });
 }
 
-gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
-                            const gnnk_tensor* rhs, gnnk_target rhs_target, const gnnk_tensor* grad_out,
-                            gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs, hipStream_t stream) {
-    clear_error();
+static gnnk_status sddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
+                                  const gnnk_tensor* rhs, gnnk_target rhs_target, const gnnk_tensor* grad_out,
+                                  gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs, hipStream_t stream) {
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
     if (op < GNNK_COPY_LHS || op > GNNK_DOT) return fail(GNNK_EINVAL, "bad op");
     if (lhs_target < GNNK_SRC || lhs_target > GNNK_DST || rhs_target < GNNK_SRC || rhs_target > GNNK_DST)
@@ -837,9 +843,9 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
             gnnk_tensor go = head_slice(grad_out, Hm, h0, hc);
             gnnk_tensor gl = grad_lhs ? head_slice(grad_lhs, Hm, h0, hc) : gnnk_tensor{};
             gnnk_tensor gr = grad_rhs ? head_slice(grad_rhs, Hm, h0, hc) : gnnk_tensor{};
-            gnnk_status st = gsddmm_backward(g, op, use_l ? &l : nullptr, lhs_target, use_r ? &r : nullptr,
-                                             rhs_target, &go, grad_lhs ? &gl : nullptr, grad_rhs ? &gr : nullptr,
-                                             stream);
+            gnnk_status st = sddmm_backward(g, op, use_l ? &l : nullptr, lhs_target, use_r ? &r : nullptr,
+                                            rhs_target, &go, grad_lhs ? &gl : nullptr, grad_rhs ? &gr : nullptr,
+                                            stream);
             if (st != GNNK_OK) return st;
         }
         return GNNK_OK;
@@ -915,6 +921,15 @@ gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lh
     return GNNK_OK;
 }
 
+gnnk_status gsddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tensor* lhs, gnnk_target lhs_target,
+                            const gnnk_tensor* rhs, gnnk_target rhs_target, const gnnk_tensor* grad_out,
+                            gnnk_tensor* grad_lhs, gnnk_tensor* grad_rhs, hipStream_t stream) {
+    clear_error();
+    return planned(g, stream, [&] {
+        return sddmm_backward(g, op, lhs, lhs_target, rhs, rhs_target, grad_out, grad_lhs, grad_rhs, stream);
+    });
+}
+
 static gnnk_status softmax_common(gnnk_graph_t g, const gnnk_tensor* a, const gnnk_tensor* b, gnnk_tensor* out,
                                   bool backward, hipStream_t stream) {
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
@@ -944,7 +959,7 @@ static gnnk_status softmax_common(gnnk_graph_t g, const gnnk_tensor* a, const gn
     // the graph's segment size, when larger); shorter rows by one wavefront
     // or lane group, whatever the segment size
     A.sch = schedule(g->in, geo, false, std::max<int64_t>(g->seg_edges, 2048));
-    return launch_status(launch_softmax(A, dtype_code(a), geo.vec, backward, stream), "edge softmax launch");
+    return GNNK_LAUNCH(launch_softmax(A, dtype_code(a), geo.vec, backward, stream), "edge softmax launch");
 }
 
 gnnk_status edge_softmax(gnnk_graph_t g, const gnnk_tensor* score, gnnk_tensor* out, hipStream_t stream) {
@@ -1008,7 +1023,7 @@ gnnk_status gat_aggregate(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_te
     const int es = dt == 1 ? 2 : 4;
     const bool fast = !options().no_fast && fast_geo(geo, dt) && fits32(A.a, g->n_src, es) &&
                       fits32(A.b, g->n_src, es);
-    return launch_status(launch_gat(A, er->data, er->row_stride, attn ? attn->data : nullptr,
+    return GNNK_LAUNCH(launch_gat(A, er->data, er->row_stride, attn ? attn->data : nullptr,
                                     attn ? attn->row_stride : 0, slope, row_ml,
                                     stats ? reinterpret_cast<float*>(stats->data) : nullptr,
                                     stats ? stats->row_stride : 0, dt, geo.vec, fast ? geo.G : 0, stream),
@@ -1072,7 +1087,7 @@ static gnnk_status gat_bwd_run(gnnk_graph_t g, const gnnk_tensor* feat, const gn
     const int es = dt == 1 ? 2 : 4;
     const bool fast = !options().no_fast && fast_geo(geo, dt) && fits32(ain.a, g->n_src, es) &&
                       fits32(ain.b, g->n_src, es);
-    return launch_status(launch_gat_backward(ain, aout, B, dt, geo.vec, fast ? geo.G : 0, stream),
+    return GNNK_LAUNCH(launch_gat_backward(ain, aout, B, dt, geo.vec, fast ? geo.G : 0, stream),
                          "fused attention backward launch");
 }
 
@@ -1086,11 +1101,10 @@ static gnnk_tensor col_slice(const gnnk_tensor* t, int c0, int cw) {
     return s;
 }
 
-gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
-                                   const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
-                                   const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,
-                                   gnnk_tensor* grad_er, hipStream_t stream) {
-    clear_error();
+static gnnk_status gat_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
+                                const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
+                                const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,
+                                gnnk_tensor* grad_er, hipStream_t stream) {
     if (!g) return fail(GNNK_EINVAL, "NULL graph");
     if (!tensor_ok(feat) || !tensor_ok(el) || !tensor_ok(er) || !tensor_ok(grad_out) || !stats ||
         (grad_feat && !tensor_ok(grad_feat)) || (grad_el && !tensor_ok(grad_el)) || (grad_er && !tensor_ok(grad_er)))
@@ -1169,6 +1183,16 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
         }
     }
     return GNNK_OK;
+}
+
+gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, const gnnk_tensor* el,
+                                   const gnnk_tensor* er, float slope, const gnnk_tensor* stats,
+                                   const gnnk_tensor* grad_out, gnnk_tensor* grad_feat, gnnk_tensor* grad_el,
+                                   gnnk_tensor* grad_er, hipStream_t stream) {
+    clear_error();
+    return planned(g, stream, [&] {
+        return gat_backward(g, feat, el, er, slope, stats, grad_out, grad_feat, grad_el, grad_er, stream);
+    });
 }
 
 static gnnk_status leaky_common(const gnnk_tensor* x, const gnnk_tensor* dy, gnnk_tensor* y, float slope,

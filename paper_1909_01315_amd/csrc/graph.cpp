@@ -22,6 +22,8 @@ namespace gnnk {
 static thread_local char g_err[512];
 // bytes of scratch the last call on this thread that ran short asked for
 static thread_local size_t g_need = 0;
+static thread_local bool g_plan = false;
+static thread_local size_t g_plan_peak = 0;
 
 gnnk_status fail(gnnk_status st, const char* fmt, ...) {
     va_list ap;
@@ -79,6 +81,10 @@ int64_t Dir::count_above(int64_t t) const {
 void* Scratch::take(size_t n) {
     const size_t at = used;
     used += (n + 255) / 256 * 256;
+    if (g_plan) {
+        if (used > g_plan_peak) g_plan_peak = used;
+        return base + at;
+    }
     if (used > bytes) {
         g_need = used;
         return nullptr;
@@ -88,6 +94,12 @@ void* Scratch::take(size_t n) {
 
 Scratch scratch_of(gnnk_graph* g, hipStream_t s) {
     Scratch sc;
+    if (g_plan) {
+        // a stand-in that no kernel sees: nothing is launched while planning
+        sc.base = reinterpret_cast<char*>((uintptr_t)1 << 20);
+        sc.bytes = SIZE_MAX;
+        return sc;
+    }
     std::lock_guard<std::mutex> lk(g->lent_mu);
     for (int k = 0; k < g->n_lent; ++k)
         if (g->lent[k].stream == s) {
@@ -95,6 +107,23 @@ Scratch scratch_of(gnnk_graph* g, hipStream_t s) {
             sc.bytes = g->lent[k].bytes;
         }
     return sc;
+}
+
+bool planning() { return g_plan; }
+
+gnnk_status planned(gnnk_graph* g, hipStream_t s, const std::function<gnnk_status()>& run) {
+    if (g_plan) return run();
+    g_plan = true;
+    g_plan_peak = 0;
+    const gnnk_status st = run();
+    g_plan = false;
+    if (st != GNNK_OK) return st;
+    Scratch have = g ? scratch_of(g, s) : Scratch{};
+    if (g_plan_peak > have.bytes) {
+        g_need = g_plan_peak;
+        return scratch_fail(have);
+    }
+    return run();
 }
 
 gnnk_status scratch_fail(const Scratch& sc) {

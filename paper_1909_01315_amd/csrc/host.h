@@ -4,6 +4,7 @@
 #include <stdarg.h>
 #include <stdint.h>
 
+#include <functional>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -104,6 +105,15 @@ Scratch scratch_of(gnnk_graph* g, hipStream_t s);
 
 // status and message of a call that did not get the scratch it needs
 gnnk_status scratch_fail(const Scratch& sc);
+
+// A call made of several passes (a gradient pair, the max/min backward's
+// masks and the walk that reads them, slices of heads) runs twice: first as a
+// plan, with every launch skipped and its scratch only counted, so that an
+// argument error or a scratch shortfall (its whole need) comes back before
+// anything runs on the GPU; then for real.  While planning, scratch_of()
+// hands out an unbounded buffer whose addresses are never used.
+bool planning();
+gnnk_status planned(gnnk_graph* g, hipStream_t s, const std::function<gnnk_status()>& run);
 
 // gspmm with its scratch from sc (api.cpp)
 gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const gnnk_tensor* lhs,

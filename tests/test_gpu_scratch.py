@@ -71,6 +71,88 @@ def test_call_without_scratch_fails_before_launching(sg2):
     p.g.destroy()
 
 
+@pytest.mark.parametrize("kind", ["max", "mul_sum", "dot"])
+def test_multi_pass_call_short_of_scratch_runs_nothing(sg2, kind):
+    """Calls made of several passes (the max backward's winner masks and the
+    walk that reads them; dX and the edge gradient of u_mul_e/sum; the two
+    node gradients of a dot) with a lent buffer too small for a later pass:
+    GNNK_ENOMEM, the buffer untouched (no pass ran), and gnnk_scratch_needed()
+    the whole call's need, with which the same call then succeeds."""
+    p = hub_pair(sg2)
+    lib = gnnk.load()
+    s = torch.cuda.Stream()
+    S = synth.feat_seed(32)
+    X = synth.normal(S, "mX", (p.o.n_src, 1, 64))
+    Y = synth.normal(S, "mY", (p.o.n_dst, 1, 64))
+    W = synth.uniform(S, "mW", (p.o.n_edges, 1, 1), 0.5, 1.5)
+    dZ = synth.normal(synth.grad_seed(32), "mdZ", (p.o.n_dst, 1, 64))
+    dM = synth.normal(synth.grad_seed(32), "mdM", (p.o.n_edges, 1, 1))
+    if kind == "max":
+        _, _, ae = orc.gspmm(p.o, "copy_lhs", "max", X)
+        ref, _ = orc.gspmm_backward(p.o, "copy_lhs", "max", X, None, dZ, arg_e=ae, want_rhs=False)
+    elif kind == "mul_sum":
+        ref = orc.gspmm_backward(p.o, "mul", "sum", X, W, dZ)
+    else:
+        ref = orc.gsddmm_backward(p.o, "dot", X, "u", Y, "v", dM)
+    # the need of the whole call, from a call without any buffer
+    lib.graph_attach_scratch(p.g.handle, s.cuda_stream, None, 0)
+    g_handle = p.g.handle
+    need = ctypes.c_size_t(0)
+    if kind == "dot":
+        Xd, Yd, dMd = dev(X), dev(Y), dev(dM)
+        gl, gr = torch.empty_like(Xd), torch.empty_like(Yd)
+        d = [gnnk._desc(t) for t in (Xd, Yd, dMd, gl, gr)]
+        call = lambda: lib.gsddmm_backward(g_handle, gnnk.OPS["dot"], gnnk._ref(d[0]), gnnk.TARGETS["u"],
+                                           gnnk._ref(d[1]), gnnk.TARGETS["v"], gnnk._ref(d[2]), gnnk._ref(d[3]),
+                                           gnnk._ref(d[4]), s.cuda_stream)
+    else:
+        Xd, dZd = dev(X), dev(dZ)
+        gl = torch.empty_like(Xd)
+        if kind == "max":
+            aed = dev(ae)
+            d = [gnnk._desc(t) for t in (Xd, dZd, gl)]
+            call = lambda: lib.gspmm_backward(g_handle, gnnk.OPS["copy_lhs"], gnnk.REDUCES["max"], gnnk._ref(d[0]),
+                                              None, None, aed.data_ptr(), gnnk._ref(d[1]), gnnk._ref(d[2]), None,
+                                              s.cuda_stream)
+        else:
+            Wd = dev(W)
+            gw = torch.empty_like(Wd)
+            d = [gnnk._desc(t) for t in (Xd, Wd, dZd, gl, gw)]
+            call = lambda: lib.gspmm_backward(g_handle, gnnk.OPS["mul"], gnnk.REDUCES["sum"], gnnk._ref(d[0]),
+                                              gnnk._ref(d[1]), None, None, gnnk._ref(d[2]), gnnk._ref(d[3]),
+                                              gnnk._ref(d[4]), s.cuda_stream)
+    torch.cuda.synchronize()
+    assert call() == gnnk.ENOMEM
+    assert lib.gnnk_scratch_needed(ctypes.byref(need)) == gnnk.OK
+    assert need.value > 0
+    # a buffer short by 4 KiB, filled with a pattern that no pass may touch
+    short = need.value - 4096 if need.value > 4096 else 0
+    if short > 0:
+        buf = torch.full((short,), 0x5A, dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        assert lib.graph_attach_scratch(g_handle, s.cuda_stream, buf.data_ptr(), short) == gnnk.OK
+        assert call() == gnnk.ENOMEM
+        n2 = ctypes.c_size_t(0)
+        assert lib.gnnk_scratch_needed(ctypes.byref(n2)) == gnnk.OK and n2.value == need.value
+        s.synchronize()
+        assert bool((buf == 0x5A).all()), "no pass may run when the call is short of scratch"
+    # exactly the reported need suffices, in one go
+    full = torch.empty(need.value, dtype=torch.uint8, device="cuda")
+    assert lib.graph_attach_scratch(g_handle, s.cuda_stream, full.data_ptr(), need.value) == gnnk.OK
+    assert call() == gnnk.OK
+    s.synchronize()
+    if kind == "max":
+        assert_close(gl, ref, name="max backward")
+    elif kind == "mul_sum":
+        assert_close(gl, ref[0], name="dX")
+        assert_close(gw, ref[1], name="dW")
+    else:
+        assert_close(gl, ref[0], name="dX")
+        assert_close(gr, ref[1], name="dY")
+    lib.graph_attach_scratch(g_handle, s.cuda_stream, None, 0)
+    p.g.destroy()
+
+
 def test_one_handle_on_two_streams_at_once(sg2):
     """Calls of every scratch-using kind queued on two streams without any
     synchronisation between them (so their kernels overlap), each stream
