@@ -21,6 +21,7 @@ its backward, and the fused attention layer with its backward.  Tolerances are t
 max/min values and their arg edges compare bit for bit.  The case number,
 seed and draws are printed before the GPU work of a case."""
 import contextlib
+import os
 import sys
 
 import numpy as np
@@ -34,7 +35,9 @@ from test_gpu_gat import oracle_gat, oracle_gat_backward
 
 pytestmark = pytest.mark.gpu
 
-N_CASES = 400
+# other seed ranges and counts: GNNK_RANDOM_SEED0, GNNK_RANDOM_CASES
+SEED0 = int(os.environ.get("GNNK_RANDOM_SEED0", "90000"))
+N_CASES = int(os.environ.get("GNNK_RANDOM_CASES", "400"))
 OPS = ["copy_lhs", "copy_rhs", "add", "sub", "mul", "div"]
 TARGETS = ["u", "e", "v"]
 
@@ -149,7 +152,7 @@ def check_bound(gpu, ref, bound, name, rel=1e-5):
 
 @pytest.mark.parametrize("case", range(N_CASES))
 def test_random_case(case):
-    rng = np.random.default_rng(90_000 + case)
+    rng = np.random.default_rng(SEED0 + case)
     src, dst, n_src, n_dst, ptr64 = draw_graph(rng)
     opts = draw_options(rng)
     build = ["coo", "coo", "csr", "csr_eids"][int(rng.integers(4))]
