@@ -281,8 +281,13 @@ __device__ __forceinline__ void walk_winners(const EngineArgs& A, int32_t self, 
     for (int32_t p0 = b; p0 < e; p0 += WAVE) {
         const int32_t p = p0 + lane;
         uint32_t any = 0u;
+        // the position's ids load with its mask words, so that the kept
+        // positions' gathers wait on one round trip, not two
+        int32_t pn = 0, pe = 0;
         if (p < e) {
             const uint32_t* w = M + (uint64_t)(uint32_t)p * words;
+            pn = A.csr.idx[p];
+            pe = A.csr.eid ? A.csr.eid[p] : p;
             for (uint32_t j = 0; j < words; ++j) any |= w[j];
         }
         const uint64_t m = __ballot(any != 0u);
@@ -294,6 +299,8 @@ __device__ __forceinline__ void walk_winners(const EngineArgs& A, int32_t self, 
                                                          __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
         const int dst = any != 0u ? below : n + (lane - below);
         const int32_t cpos = __builtin_amdgcn_ds_permute(dst << 2, p);
+        const int32_t cnb = __builtin_amdgcn_ds_permute(dst << 2, pn);
+        const int32_t ced = __builtin_amdgcn_ds_permute(dst << 2, pe);
         for (int k = 0; k < n; k += G * UNR) {
             int32_t nb[UNR], ed[UNR], ps[UNR];
             bool ok[UNR];
@@ -301,10 +308,13 @@ __device__ __forceinline__ void walk_winners(const EngineArgs& A, int32_t self, 
             for (int u = 0; u < UNR; ++u) {
                 const int q = k + g + G * u;
                 ok[u] = q < n;
-                const int32_t pq = __shfl(cpos, ok[u] ? q : 0, WAVE);
+                // a slot past the kept positions takes kept position 0 (n > 0
+                // here), whose ids are in range; it is dropped by ok
+                const int qs = ok[u] ? q : 0;
+                const int32_t pq = __shfl(cpos, qs, WAVE);
                 ps[u] = ok[u] ? pq : b;
-                nb[u] = A.csr.idx[ps[u]];
-                ed[u] = A.csr.eid ? A.csr.eid[ps[u]] : ps[u];
+                nb[u] = __shfl(cnb, qs, WAVE);
+                ed[u] = __shfl(ced, qs, WAVE);
             }
             Raw<VEC> r[UNR];
 #pragma unroll
