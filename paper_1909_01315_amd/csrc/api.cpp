@@ -145,6 +145,8 @@ CsrDev csr_of(const gnnk_graph* g, const Dir& d) {
     c.seg_order = d.seg_order;
     c.hub_off = d.hub_off;
     c.row = d.row;
+    c.segw = d.segw;
+    c.rowt = d.rowt;
     c.ptr64 = g->ptr64;
     return c;
 }

@@ -379,6 +379,46 @@ hipError_t launch_seg_keys(const int4* seg, int64_t n_seg, const int32_t* idx, u
     return hipGetLastError();
 }
 
+namespace {
+
+// the segment of each hub-segment wavefront, with its table index: the walk
+// then finds its segment with one load instead of two dependent ones
+__global__ void seg_wave_kernel(const int4* seg, const int32_t* order, int64_t n_seg, int4* segw) {
+    for (int64_t w = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; w < n_seg; w += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t si = order[w];
+        const int4 t = seg[si];
+        segw[w] = make_int4(t.x, t.y, t.z, si);
+    }
+}
+
+// {row, begin, end, 0} of every row in degree order
+template <typename P>
+__global__ void row_table_kernel(const P* ptr, const int32_t* perm, int64_t n_rows, int4* rowt) {
+    for (int64_t k = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; k < n_rows; k += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t r = perm[k];
+        rowt[k] = make_int4(r, (int32_t)ptr[r], (int32_t)ptr[r + 1], 0);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_seg_wave(const int4* seg, const int32_t* order, int64_t n_seg, int4* segw, hipStream_t s) {
+    if (n_seg <= 0) return hipSuccess;
+    hipLaunchKernelGGL(seg_wave_kernel, dim3(grid_1d(n_seg)), dim3(256), 0, s, seg, order, n_seg, segw);
+    return hipGetLastError();
+}
+
+hipError_t launch_row_table(const void* ptr, int ptr64, const int32_t* perm, int64_t n_rows, int4* rowt,
+                            hipStream_t s) {
+    if (n_rows <= 0) return hipSuccess;
+    dim3 grid(grid_1d(n_rows)), block(256);
+    if (ptr64)
+        hipLaunchKernelGGL(row_table_kernel<int64_t>, grid, block, 0, s, (const int64_t*)ptr, perm, n_rows, rowt);
+    else
+        hipLaunchKernelGGL(row_table_kernel<int32_t>, grid, block, 0, s, (const int32_t*)ptr, perm, n_rows, rowt);
+    return hipGetLastError();
+}
+
 hipError_t launch_hub_segments(const void* ptr, int ptr64, const int32_t* perm, const int32_t* hub_off, int64_t n_hub,
                                int64_t seg_edges, int4* seg, hipStream_t s) {
     if (n_hub <= 0) return hipSuccess;

@@ -132,13 +132,11 @@ __global__ __launch_bounds__(256) void gat_kernel(EngineArgs A, GatArgs G) {
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int si = A.csr.seg_order[w];
-            const int4 s = A.csr.seg[si];
-            r = s.x; b = s.y; e = s.z; slot = si;
+            const int4 s = A.csr.segw[w];
+            r = s.x; b = s.y; e = s.z; slot = s.w;
         } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+            r = t.x; b = t.y; e = t.z;
         }
         r = uniform64(r);
         b = uniform64(b);
@@ -187,9 +185,8 @@ __global__ __launch_bounds__(256) void gat_kernel(EngineArgs A, GatArgs G) {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * Gn + ln.g;
         int64_t r = -1, b = 0, e = 0;
         if (k < A.sch.n_nz) {
-            r = A.csr.perm[k];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[k];
+            r = t.x; b = t.y; e = t.z;
         }
         const int32_t self = r >= 0 ? (int32_t)r : 0;
         for (int ch = 0; ch < geo.nchunk; ++ch) {
@@ -432,22 +429,19 @@ __global__ __launch_bounds__(256) void gat_bwd_dst_kernel(EngineArgs A, GatBwdAr
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int si = A.csr.seg_order[w];
-            const int4 sg = A.csr.seg[si];
-            r = sg.x; b = sg.y; e = sg.z; slot = si;
+            const int4 sg = A.csr.segw[w];
+            r = sg.x; b = sg.y; e = sg.z; slot = sg.w;
         } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+            r = t.x; b = t.y; e = t.z;
         }
         gat_bwd_dst_row<T, VEC, S, true, RED>(A, B, ln, Gn, uniform64(r), uniform64(b), uniform64(e), slot);
     } else if (w < A.sch.w_small_end) {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * Gn + ln.g;
         int64_t r = -1, b = 0, e = 0;
         if (k < A.sch.n_nz) {
-            r = A.csr.perm[k];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[k];
+            r = t.x; b = t.y; e = t.z;
         }
         gat_bwd_dst_row<T, VEC, S, false, RED>(A, B, ln, Gn, r, b, e, -1);
     } else if (B.d_er) {
@@ -623,22 +617,19 @@ __global__ __launch_bounds__(256) void gat_bwd_src_kernel(EngineArgs A, GatBwdAr
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int si = A.csr.seg_order[w];
-            const int4 sg = A.csr.seg[si];
-            r = sg.x; b = sg.y; e = sg.z; slot = si;
+            const int4 sg = A.csr.segw[w];
+            r = sg.x; b = sg.y; e = sg.z; slot = sg.w;
         } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+            r = t.x; b = t.y; e = t.z;
         }
         gat_bwd_src_row<T, VEC, true, RED>(A, B, ln, uniform64(r), uniform64(b), uniform64(e), slot);
     } else if (w < A.sch.w_small_end) {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + ln.g;
         int64_t r = -1, b = 0, e = 0;
         if (k < A.sch.n_nz) {
-            r = A.csr.perm[k];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[k];
+            r = t.x; b = t.y; e = t.z;
         }
         gat_bwd_src_row<T, VEC, false, RED>(A, B, ln, r, b, e, -1);
     } else {

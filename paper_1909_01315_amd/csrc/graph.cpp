@@ -154,6 +154,7 @@ struct Layout {
     size_t tmp = 0, tmp_words = 0;  // the build's temporaries (radix-sort counts, degree and segment sort keys)
     size_t in_hub = 0, out_hub = 0, in_seg = 0, out_seg = 0, in_sego = 0, out_sego = 0, total = 0;
     size_t fine_hub = 0, fine_seg = 0, fine_sego = 0;  // the reverse CSR's finer hub tables
+    size_t in_rowt = 0, out_rowt = 0, in_segw = 0, out_segw = 0, fine_segw = 0;  // per-wavefront lookup tables
 };
 
 struct Bump {
@@ -201,6 +202,8 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t S
     L.out_row = b.take((size_t)E * 4);
     L.out_pos = b.take((size_t)E * 4);
     L.flag = b.take(ALIGN);
+    L.in_rowt = b.take((size_t)n_dst * 16);
+    L.out_rowt = b.take((size_t)n_src * 16);
     L.tmp_words = build_tmp_words(n_src, n_dst, E, S);
     L.tmp = b.take(L.tmp_words * 4);
     L.in_hub = b.take((size_t)(hub_in + 1) * 4);
@@ -212,6 +215,9 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t S
     L.fine_hub = b.take((size_t)(hub_fine + 1) * 4);
     L.fine_seg = b.take((size_t)seg_fine * 16);
     L.fine_sego = b.take((size_t)seg_fine * 4);
+    L.in_segw = b.take((size_t)seg_in * 16);
+    L.out_segw = b.take((size_t)seg_out * 16);
+    L.fine_segw = b.take((size_t)seg_fine * 16);
     L.total = b.off;
     return L;
 }
@@ -373,21 +379,32 @@ struct Builder {
         out.seg = at<int4>(L.out_seg);
         in.seg_order = at<int32_t>(L.in_sego);
         out.seg_order = at<int32_t>(L.out_sego);
+        in.segw = at<int4>(L.in_segw);
+        out.segw = at<int4>(L.out_segw);
+        in.rowt = at<int4>(L.in_rowt);
+        out.rowt = at<int4>(L.out_rowt);
+        chk(launch_row_table(in.ptr, g->ptr64, in.perm, in.n_rows, in.rowt, s));
+        chk(launch_row_table(out.ptr, g->ptr64, out.perm, out.n_rows, out.rowt, s));
         chk(hipMemcpyAsync(in.hub_off, hin.data(), hin.size() * 4, hipMemcpyHostToDevice, s));
         chk(hipMemcpyAsync(out.hub_off, hout.data(), hout.size() * 4, hipMemcpyHostToDevice, s));
         chk(launch_hub_segments(in.ptr, g->ptr64, in.perm, in.hub_off, in.n_hub, g->seg_edges, in.seg, s));
         chk(launch_hub_segments(out.ptr, g->ptr64, out.perm, out.hub_off, out.n_hub, g->seg_edges_out, out.seg, s));
         order_segments(in, g->n_src);
         order_segments(out, g->n_dst);
+        chk(launch_seg_wave(in.seg, in.seg_order, in.n_seg, in.segw, s));
+        chk(launch_seg_wave(out.seg, out.seg_order, out.n_seg, out.segw, s));
         if (finer) {
             fine.hub_off = at<int32_t>(L.fine_hub);
             fine.seg = at<int4>(L.fine_seg);
             fine.seg_order = at<int32_t>(L.fine_sego);
+            fine.segw = at<int4>(L.fine_segw);
+            fine.rowt = out.rowt;
             chk(hipMemcpyAsync(fine.hub_off, fine.hub_host.data(), fine.hub_host.size() * 4, hipMemcpyHostToDevice,
                                s));
             chk(launch_hub_segments(fine.ptr, g->ptr64, fine.perm, fine.hub_off, fine.n_hub, g->seg_edges_fine,
                                     fine.seg, s));
             order_segments(fine, g->n_dst);
+            chk(launch_seg_wave(fine.seg, fine.seg_order, fine.n_seg, fine.segw, s));
         } else {
             fine = out;
         }

@@ -25,6 +25,8 @@ struct Dir {
     int32_t* perm = nullptr;       // device rows by descending degree
     int4* seg = nullptr;           // device segments of hub rows
     int32_t* seg_order = nullptr;  // device segment of each hub-segment wavefront
+    int4* segw = nullptr;          // device seg[seg_order[w]] with the table index in .w
+    int4* rowt = nullptr;          // device {perm[k], begin, end, 0} per degree-order position
     int32_t* hub_off = nullptr;    // device first segment per hub row (n_hub + 1)
     int32_t* row = nullptr;        // device row of each position (COO form)
     int32_t* pos = nullptr;        // device position of each edge id in this CSR

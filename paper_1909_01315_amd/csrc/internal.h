@@ -72,6 +72,8 @@ struct CsrDev {
     const int32_t* seg_order;
     const int32_t* hub_off; // first segment of each hub row (hub rows = perm[0, n_hub)), n_hub + 1 entries
     const int32_t* row;     // row of each position (the COO form of the same CSR)
+    const int4* segw;       // seg[seg_order[w]] with its table index: {row, begin, end, seg_order[w]}
+    const int4* rowt;       // {perm[k], begin, end, 0}: the rows in degree order with their positions
     int32_t ptr64;
     int32_t pad;
 };
@@ -262,6 +264,9 @@ hipError_t launch_copy_ptr(const void* src, int src64, void* dst, int dst64, int
 // ----- device construction of the graph formats (build.hip) -----
 // key[k] = idx[seg[k].begin] / 2 + idx[seg[k].end - 1] / 2 for k < n_seg
 hipError_t launch_seg_keys(const int4* seg, int64_t n_seg, const int32_t* idx, uint32_t* key, hipStream_t s);
+hipError_t launch_seg_wave(const int4* seg, const int32_t* order, int64_t n_seg, int4* segw, hipStream_t s);
+hipError_t launch_row_table(const void* ptr, int ptr64, const int32_t* perm, int64_t n_rows, int4* rowt,
+                            hipStream_t s);
 // bits needed for keys in [0, max_key]
 int key_bits(uint64_t max_key);
 // uint32 words of scratch radix_sort_pairs needs for n pairs

@@ -143,21 +143,19 @@ __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
     if (w < A.sch.w_big_end) {
         int64_t r, b, e;
         if (w < A.sch.n_seg) {
-            const int4 s = A.csr.seg[A.csr.seg_order[w]];
+            const int4 s = A.csr.segw[w];
             r = s.x; b = s.y; e = s.z;
         } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+            r = t.x; b = t.y; e = t.z;
         }
         sddmm_row<T, VEC, OPK, EXT, RM, S, true>(A, ln, G, L, uniform64(r), uniform64(b), uniform64(e));
     } else {
         int64_t r = -1, b = 0, e = 0;
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * G + ln.g;
         if (k < A.sch.n_nz) {
-            r = A.csr.perm[k];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[k];
+            r = t.x; b = t.y; e = t.z;
         }
         sddmm_row<T, VEC, OPK, EXT, RM, S, false>(A, ln, G, L, r, b, e);
     }

@@ -278,15 +278,13 @@ __global__ __launch_bounds__(256) void softmax_kernel(EngineArgs A) {
     const bool coop = w < A.sch.w_big_end;
     int64_t r = -1, b = 0, e = 0;
     if (coop) {
-        r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-        b = row_ptr(A.csr, r);
-        e = row_ptr(A.csr, r + 1);
+        const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+        r = t.x; b = t.y; e = t.z;
     } else {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * geo.G + g;
         if (k < A.sch.n_nz) {
-            r = A.csr.perm[k];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[k];
+            r = t.x; b = t.y; e = t.z;
         }
     }
     const int start = coop ? g : 0, stride = coop ? geo.G : 1;
@@ -336,8 +334,8 @@ __global__ __launch_bounds__(WAVE * HUB_WAVES) void softmax_hub_kernel(EngineArg
     const GeomDev& geo = A.geo;
     const Lanes ln = lanes_of(geo);
     const int wv = threadIdx.x >> 6;
-    const int64_t r = A.csr.perm[blockIdx.x];
-    const int64_t b = uniform64(row_ptr(A.csr, r)), e = uniform64(row_ptr(A.csr, r + 1));
+    const int4 t = A.csr.rowt[blockIdx.x];
+    const int64_t b = uniform64(t.y), e = uniform64(t.z);
     const int start = wv * geo.G + ln.g, stride = HUB_WAVES * geo.G;
     for (int ch = 0; ch < geo.nchunk; ++ch) {
         const int j = ch * geo.L + ln.lig;

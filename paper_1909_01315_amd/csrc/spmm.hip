@@ -59,13 +59,11 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int si = A.csr.seg_order[w];
-            const int4 s = A.csr.seg[si];
-            r = s.x; b = s.y; e = s.z; slot = si;
+            const int4 s = A.csr.segw[w];
+            r = s.x; b = s.y; e = s.z; slot = s.w;
         } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+            r = t.x; b = t.y; e = t.z;
         }
         r = uniform64(r);
         b = uniform64(b);
@@ -113,9 +111,8 @@ __global__ __launch_bounds__(256) void spmm_sum_kernel(EngineArgs A) {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * G + ln.g;
         int64_t r = -1, b = 0, e = 0;
         if (k < A.sch.n_nz) {
-            r = A.csr.perm[k];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[k];
+            r = t.x; b = t.y; e = t.z;
         }
         const int32_t self = r >= 0 ? (int32_t)r : 0;
         double carry = 0.0;
@@ -372,22 +369,19 @@ __global__ __launch_bounds__(256) void spmm_cmp_kernel(EngineArgs A) {
         int64_t r, b, e;
         int slot = -1;
         if (w < A.sch.n_seg) {
-            const int si = A.csr.seg_order[w];
-            const int4 s = A.csr.seg[si];
-            r = s.x; b = s.y; e = s.z; slot = si;
+            const int4 s = A.csr.segw[w];
+            r = s.x; b = s.y; e = s.z; slot = s.w;
         } else {
-            r = A.csr.perm[A.sch.n_hub + (w - A.sch.n_seg)];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+            r = t.x; b = t.y; e = t.z;
         }
         cmp_row<T, VEC, OPK, S, true>(A, ln, G, L, uniform64(r), uniform64(b), uniform64(e), slot);
     } else if (w < A.sch.w_small_end) {
         const int64_t k = A.sch.n_big + (int64_t)(w - A.sch.w_big_end) * G + ln.g;
         int64_t r = -1, b = 0, e = 0;
         if (k < A.sch.n_nz) {
-            r = A.csr.perm[k];
-            b = row_ptr(A.csr, r);
-            e = row_ptr(A.csr, r + 1);
+            const int4 t = A.csr.rowt[k];
+            r = t.x; b = t.y; e = t.z;
         }
         cmp_row<T, VEC, OPK, S, false>(A, ln, G, L, r, b, e, -1);
     } else {
