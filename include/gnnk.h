@@ -112,6 +112,8 @@ typedef struct {
     int64_t seg_edges_out;  /* edges per segment of a hub row of the reverse graph's CSR */
     int64_t seg_edges_gather; /* the same for the reverse passes that gather node rows */
     int64_t segments_gather;  /* the segments of that finer table */
+    int64_t seg_edges_in_gather; /* the in-CSR's finer segments, for the passes that gather node rows */
+    int64_t segments_in_gather;  /* the segments of that table */
 } gnnk_graph_info;
 
 /* ------------------------------------------------------------------------ */

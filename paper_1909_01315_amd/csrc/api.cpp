@@ -217,7 +217,7 @@ bool fits32(const OperandDev& o, int64_t rows, int es) {
 
 // rows of the table an operand reads during a walk over `d`
 int64_t table_rows(const gnnk_graph* g, const Dir& d, int32_t target) {
-    const bool in = &d == &g->in;
+    const bool in = &d == &g->in || &d == &g->in_fine;
     if (target == T_EDGE) return g->n_edges;
     if (target == T_NBR) return in ? g->n_src : g->n_dst;
     return in ? g->n_dst : g->n_src;
@@ -366,9 +366,12 @@ gnnk_status run_spmm_sum(gnnk_graph* g, const Dir& d, EngineArgs& A, const Geo& 
 }
 
 gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, int opk, hipStream_t s, Scratch& sc) {
-    A.csr = csr_of(g, g->in);
+    // the in-CSR's finer segments (c3 u_dot_v 3.33 -> 3.19 ms): a g-SDDMM
+    // leaves no partials, and more of each hub row runs in narrow pieces
+    const Dir& d = g->in_fine;
+    A.csr = csr_of(g, d);
     set_geo(A, geo);
-    A.sch = schedule(g->in, geo, false);
+    A.sch = schedule(d, geo, false);
     const Pick pk = pick_sddmm(g, A, geo, dtype, opk);
     const bool multi = A.out.reduce && geo.nchunk > 1;
     if (multi) {
@@ -376,7 +379,7 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
         A.xacc = reinterpret_cast<double*>(sc.take((size_t)g->n_edges * 8));
         if (!A.xacc) return scratch_fail(sc);
     }
-    if (pick_walk(g->in, multi)) {
+    if (pick_walk(d, multi)) {
         set_edge_chunks(A, g->n_edges, geo);
         return GNNK_LAUNCH(launch_sddmm_edge(A, g->n_edges, dtype, geo.vec, opk, pk.spec, pk.gc, s),
                              "edge-parallel g-SDDMM launch");
@@ -471,7 +474,13 @@ gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const 
     A.out.red = 1;
     A.out.reduce = 0;
     A.flags = (reduce == GNNK_MEAN ? F_OWN_MEAN : 0) | (reduce == GNNK_MIN ? F_IS_MIN : 0);
-    if (!cmp) return run_spmm_sum(g, g->in, A, geo, dtype_code(out), opk, stream, sc);
+    if (!cmp) {
+        // sums that gather node rows take the in-CSR's finer segments
+        // (c3 copy_u/mean 2.59 -> 2.46 ms, c4 copy_u/sum 3.59 -> 3.24 ms);
+        // copy_e sums keep the coarser ones, on which they run faster
+        const bool gathers = (A.a.target == T_NBR && A.a.full) || (A.b.data && A.b.target == T_NBR && A.b.full);
+        return run_spmm_sum(g, gathers ? g->in_fine : g->in, A, geo, dtype_code(out), opk, stream, sc);
+    }
     A.arg_nbr = arg_lhs;
     A.arg_edge = arg_rhs;
     A.csr = csr_of(g, g->in);
@@ -526,8 +535,9 @@ gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags,
     auto al = [](size_t n) { return (n + 255) / 256 * 256; };
     const size_t C = (size_t)max_cols, E = (size_t)g->n_edges;
     const size_t si = (size_t)g->in.n_seg, so = (size_t)std::max(g->out.n_seg, g->out_fine.n_seg);
-    // sums and their gradients: fp64 partials of hub segments (either CSR)
-    size_t need = al(std::max(si, so) * C * 8);
+    const size_t sif = (size_t)g->in_fine.n_seg;
+    // sums and their gradients: fp64 partials of hub segments (any table)
+    size_t need = al(std::max({si, sif, so}) * C * 8);
     // max / min: value, edge and neighbour per segment and column
     need = std::max(need, al(si * C * 12));
     // fused attention: partial states of segments, and the row state of hub
@@ -911,13 +921,12 @@ static gnnk_status sddmm_backward(gnnk_graph_t g, gnnk_binop op, const gnnk_tens
         if (st != GNNK_OK) return st;
         A.flags = flags;
         Scratch sc = scratch_of(g, stream);
-        // a pass over the reverse graph that gathers node rows (the other
-        // operand of mul/div/dot) takes the finer segments; copy_e sums the
-        // coarse ones
+        // a pass that gathers node rows (the other operand of mul/div/dot)
+        // takes its CSR's finer segments; copy_e sums the coarse ones
         const bool gathers = (A.a.target == T_NBR && A.a.full) || (A.b.data && A.b.target == T_NBR && A.b.full);
         if (tx == GNNK_EDGE) st = run_sddmm(g, A, geo, dt, opk, stream, sc);
-        else st = run_spmm_sum(g, tx == GNNK_SRC ? (gathers ? g->out_fine : g->out) : g->in, A, geo, dt, opk, stream,
-                               sc);
+        else st = run_spmm_sum(g, tx == GNNK_SRC ? (gathers ? g->out_fine : g->out) : (gathers ? g->in_fine : g->in),
+                               A, geo, dt, opk, stream, sc);
         if (st != GNNK_OK) return st;
     }
     return GNNK_OK;

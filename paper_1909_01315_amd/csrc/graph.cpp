@@ -155,6 +155,7 @@ struct Layout {
     size_t in_hub = 0, out_hub = 0, in_seg = 0, out_seg = 0, in_sego = 0, out_sego = 0, total = 0;
     size_t fine_hub = 0, fine_seg = 0, fine_sego = 0;  // the reverse CSR's finer hub tables
     size_t in_rowt = 0, out_rowt = 0, in_segw = 0, out_segw = 0, fine_segw = 0;  // per-wavefront lookup tables
+    size_t ifine_hub = 0, ifine_seg = 0, ifine_sego = 0, ifine_segw = 0;  // the in-CSR's finer hub tables
 };
 
 struct Bump {
@@ -171,7 +172,9 @@ struct Bump {
 int64_t max_segments(int64_t E, int64_t S) { return 2 * E / S + 2; }
 
 // the smallest segment size of a graph's tables (the most segments)
-int64_t min_seg_edges(const gnnk_graph* g) { return std::min({g->seg_edges, g->seg_edges_out, g->seg_edges_fine}); }
+int64_t min_seg_edges(const gnnk_graph* g) {
+    return std::min({g->seg_edges, g->seg_edges_out, g->seg_edges_fine, g->seg_edges_in_fine});
+}
 
 // uint32 words of build temporaries: the radix sort of the edges, or four
 // row-sized arrays plus the sort of the degree keys, or the same for the
@@ -185,7 +188,8 @@ size_t build_tmp_words(int64_t n_src, int64_t n_dst, int64_t E, int64_t S) {
 }
 
 Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t S, int64_t hub_in, int64_t hub_out,
-                   int64_t seg_in, int64_t seg_out, int64_t hub_fine = 0, int64_t seg_fine = 0) {
+                   int64_t seg_in, int64_t seg_out, int64_t hub_fine = 0, int64_t seg_fine = 0,
+                   int64_t hub_ifine = 0, int64_t seg_ifine = 0) {
     Layout L;
     Bump b;
     L.in_ptr = b.take((size_t)(n_dst + 1) * ps);
@@ -218,6 +222,10 @@ Layout make_layout(int64_t n_src, int64_t n_dst, int64_t E, size_t ps, int64_t S
     L.in_segw = b.take((size_t)seg_in * 16);
     L.out_segw = b.take((size_t)seg_out * 16);
     L.fine_segw = b.take((size_t)seg_fine * 16);
+    L.ifine_hub = b.take((size_t)(hub_ifine + 1) * 4);
+    L.ifine_seg = b.take((size_t)seg_ifine * 16);
+    L.ifine_sego = b.take((size_t)seg_ifine * 4);
+    L.ifine_segw = b.take((size_t)seg_ifine * 16);
     L.total = b.off;
     return L;
 }
@@ -368,8 +376,13 @@ struct Builder {
         const bool finer = g->seg_edges_fine < g->seg_edges_out;
         fine = out;
         if (finer) schedule_host(fine, g->seg_edges_fine, fine.hub_host);
+        Dir& ifine = g->in_fine;
+        const bool ifiner = g->seg_edges_in_fine < g->seg_edges;
+        ifine = in;
+        if (ifiner) schedule_host(ifine, g->seg_edges_in_fine, ifine.hub_host);
         L = make_layout(g->n_src, g->n_dst, E, g->ptr64 ? 8 : 4, min_seg_edges(g), in.n_hub, out.n_hub, in.n_seg,
-                        out.n_seg, finer ? fine.n_hub : 0, finer ? fine.n_seg : 0);
+                        out.n_seg, finer ? fine.n_hub : 0, finer ? fine.n_seg : 0, ifiner ? ifine.n_hub : 0,
+                        ifiner ? ifine.n_seg : 0);
         if (ws_bytes < L.total)
             return fail(GNNK_ENOMEM, "workspace of %zu bytes is smaller than the %zu bytes this graph needs",
                         ws_bytes, L.total);
@@ -408,6 +421,21 @@ struct Builder {
         } else {
             fine = out;
         }
+        if (ifiner) {
+            ifine.hub_off = at<int32_t>(L.ifine_hub);
+            ifine.seg = at<int4>(L.ifine_seg);
+            ifine.seg_order = at<int32_t>(L.ifine_sego);
+            ifine.segw = at<int4>(L.ifine_segw);
+            ifine.rowt = in.rowt;
+            chk(hipMemcpyAsync(ifine.hub_off, ifine.hub_host.data(), ifine.hub_host.size() * 4,
+                               hipMemcpyHostToDevice, s));
+            chk(launch_hub_segments(ifine.ptr, g->ptr64, ifine.perm, ifine.hub_off, ifine.n_hub,
+                                    g->seg_edges_in_fine, ifine.seg, s));
+            order_segments(ifine, g->n_src);
+            chk(launch_seg_wave(ifine.seg, ifine.seg_order, ifine.n_seg, ifine.segw, s));
+        } else {
+            ifine = in;
+        }
         chk(hipMemsetAsync(g->flag, 0, 4, s));
         // the host copies of the hub offsets stay with the handle, so the
         // copies above may still be in flight when the call returns
@@ -431,6 +459,7 @@ gnnk_graph* new_graph(int64_t num_src, int64_t num_dst, int64_t num_edges, gnnk_
     g->seg_edges = seg_edges_for(num_edges, false);
     g->seg_edges_out = seg_edges_for(num_edges, true);
     g->seg_edges_fine = seg_edges_fine_for(num_edges);
+    g->seg_edges_in_fine = seg_edges_fine_for(num_edges);
     return g;
 }
 
@@ -531,11 +560,12 @@ gnnk_status graph_workspace_bytes(int64_t num_src, int64_t num_dst, int64_t num_
     // hub rows have more than S edges: at most E / S of them, and at most
     // E / S + (hub rows) <= 2 E / S segments
     const int64_t Si = seg_edges_for(num_edges, false), So = seg_edges_for(num_edges, true);
-    const int64_t Sf = seg_edges_fine_for(num_edges);
+    const int64_t Sf = seg_edges_fine_for(num_edges);  // both CSRs' finer tables
     Layout L = make_layout(num_src, num_dst, num_edges, ptr_t == GNNK_I64 ? 8 : 4, std::min({Si, So, Sf}),
                            num_edges / Si + 1, num_edges / So + 1, max_segments(num_edges, Si),
                            max_segments(num_edges, So), Sf < So ? num_edges / Sf + 1 : 0,
-                           Sf < So ? max_segments(num_edges, Sf) : 0);
+                           Sf < So ? max_segments(num_edges, Sf) : 0, Sf < Si ? num_edges / Sf + 1 : 0,
+                           Sf < Si ? max_segments(num_edges, Sf) : 0);
     *bytes = L.total;
     return GNNK_OK;
 }
@@ -594,6 +624,8 @@ gnnk_status graph_info(gnnk_graph_t g, gnnk_graph_info* info) {
     info->seg_edges_out = g->seg_edges_out;
     info->seg_edges_gather = g->seg_edges_fine;
     info->segments_gather = g->out_fine.n_seg;
+    info->seg_edges_in_gather = g->seg_edges_in_fine;
+    info->segments_in_gather = g->in_fine.n_seg;
     info->hub_dst_rows = g->in.n_hub;
     info->hub_src_rows = g->out.n_hub;
     info->segments_in = g->in.n_seg;

@@ -45,7 +45,11 @@ struct gnnk_graph {
     int64_t seg_edges = 512;       // edges per segment of a hub row of the in-CSR
     int64_t seg_edges_out = 2048;  // the same for the reverse graph's CSR
     int64_t seg_edges_fine = 256;  // the reverse graph's CSR for passes that gather node rows
+    int64_t seg_edges_in_fine = 256;  // the in-CSR for passes that gather node rows
     gnnk::Dir in, out;
+    // the in-CSR with segments of seg_edges_in_fine edges (its own hub tables
+    // and segment order, every other array shared with `in`)
+    gnnk::Dir in_fine;
     // the reverse graph's CSR with segments of seg_edges_fine edges (its own
     // hub tables and segment order, every other array shared with `out`)
     gnnk::Dir out_fine;

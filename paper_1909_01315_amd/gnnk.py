@@ -50,7 +50,8 @@ class _Info(ctypes.Structure):
                 ("seg_edges", ctypes.c_int64), ("hub_dst_rows", ctypes.c_int64), ("hub_src_rows", ctypes.c_int64),
                 ("segments_in", ctypes.c_int64), ("segments_out", ctypes.c_int64),
                 ("workspace_bytes", ctypes.c_size_t), ("seg_edges_out", ctypes.c_int64),
-                ("seg_edges_gather", ctypes.c_int64), ("segments_gather", ctypes.c_int64)]
+                ("seg_edges_gather", ctypes.c_int64), ("segments_gather", ctypes.c_int64),
+                ("seg_edges_in_gather", ctypes.c_int64), ("segments_in_gather", ctypes.c_int64)]
 
 
 SYMBOLS = {

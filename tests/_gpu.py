@@ -102,6 +102,7 @@ def check_formats(p, seg_edges=None):
     seg_in = seg_edges if seg_edges is not None else info["seg_edges"]
     seg_out = seg_edges if seg_edges is not None else info["seg_edges_out"]
     seg_g = seg_edges if seg_edges is not None else info["seg_edges_gather"]
+    seg_gi = seg_edges if seg_edges is not None else info["seg_edges_in_gather"]
     assert info["max_in_degree"] == (ind.max() if ind.size else 0)
     assert info["max_out_degree"] == (outd.max() if outd.size else 0)
     assert info["empty_dst_rows"] == int((ind == 0).sum())
@@ -113,5 +114,7 @@ def check_formats(p, seg_edges=None):
         assert info[seg] == int(((big + S - 1) // S).sum()), seg
     big = outd[outd > seg_g].astype(np.int64)
     assert info["segments_gather"] == int(((big + seg_g - 1) // seg_g).sum()), "segments_gather"
+    big = ind[ind > seg_gi].astype(np.int64)
+    assert info["segments_in_gather"] == int(((big + seg_gi - 1) // seg_gi).sum()), "segments_in_gather"
     assert info["identity_eids"] == int(np.array_equal(ie, np.arange(p.o.n_edges, dtype=np.int32)))
     p.g.validate()

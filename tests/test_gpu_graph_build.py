@@ -206,16 +206,19 @@ def test_maximum_edge_count():
 def test_segment_size_follows_the_edge_count():
     """seg_edges 0 (the default): for the in-CSR the next power of two of
     E / 8192 within [64, 512], for the reverse graph's CSR the next power of
-    two of E / 2048 within [64, 2048] and, for its passes that gather node
-    rows, of E / 16384 within [64, 256]; a fixed option sets all three"""
+    two of E / 2048 within [64, 2048] and, for the passes of either CSR that
+    gather node rows, of E / 16384 within [64, 256]; a fixed option sets all
+    four"""
     for E, Si, So, Sg in ((1000, 64, 64, 64), (200_000, 64, 128, 64), (1_000_000, 128, 512, 64),
                           (3_000_000, 512, 2048, 256), (9_000_000, 512, 2048, 256)):
         src, dst = random_edges(E, 5000, 5000, E)
         p = Pair(src, dst, 5000, 5000)
         info = p.g.info()
-        assert (info["seg_edges"], info["seg_edges_out"], info["seg_edges_gather"]) == (Si, So, Sg), E
+        assert (info["seg_edges"], info["seg_edges_out"], info["seg_edges_gather"],
+                info["seg_edges_in_gather"]) == (Si, So, Sg, Sg), E
         check_formats(p)
     gnnk.set_option("seg_edges", 300)
     src, dst = random_edges(1, 50, 50, 1000)
     info = Pair(src, dst, 50, 50).g.info()
     assert info["seg_edges"] == 300 and info["seg_edges_out"] == 300 and info["seg_edges_gather"] == 300
+    assert info["seg_edges_in_gather"] == 300
