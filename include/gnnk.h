@@ -374,8 +374,9 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
  *   "seg_edges"   edges per hub-row segment: 0 (default) chooses per graph
  *                 the next power of two of num_edges / 8192 within [64, 512]
  *                 for the in-CSR and of num_edges / 2048 within [64, 2048]
- *                 for the reverse graph's CSR, and for the reverse passes that
- *                 gather node rows of num_edges / 16384 within [64, 256]
+ *                 for the reverse graph's CSR, and for the passes of either
+ *                 CSR that gather node rows (and every g-SDDMM) of
+ *                 num_edges / 16384 within [64, 256]
  *                 (small graphs split their long rows across more
  *                 wavefronts); otherwise a fixed value in [32, 2^30] for all
  *   "no_split"    1: never split a row across waves (hub rows run whole)
