@@ -380,6 +380,10 @@ gnnk_status gat_aggregate_backward(gnnk_graph_t g, const gnnk_tensor* feat, cons
  *                 (small graphs split their long rows across more
  *                 wavefronts); otherwise a fixed value in [32, 2^30] for all
  *   "no_split"    1: never split a row across waves (hub rows run whole)
+ *   "sddmm_split" wavefronts per hub-row segment of a g-SDDMM, each taking
+ *                 whole batches of it: 0 (default) two where a batch holds
+ *                 64 or more edges (16 or more lane groups), else one;
+ *                 otherwise 1-8 (results do not depend on it)
  *   "small_deg"   rows of at most this many edges take one lane group each
  *                 and share a wavefront (-1 = auto: 32, or the lane groups
  *                 per wavefront if more; none when a wavefront is one group)

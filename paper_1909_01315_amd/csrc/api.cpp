@@ -372,6 +372,22 @@ gnnk_status run_sddmm(gnnk_graph* g, EngineArgs& A, const Geo& geo, int dtype, i
     A.csr = csr_of(g, d);
     set_geo(A, geo);
     A.sch = schedule(d, geo, false);
+    // narrow rows (16 or more lane groups, a batch of 64 or more edges) put
+    // two wavefronts on each hub segment: it holds few batches, and a
+    // wavefront's fixed start (segment, row value, first ids) then overlaps
+    // with another's gathers
+    {
+        const int64_t o = options().sddmm_split;
+        const int ks = (int)(o > 0 ? o : (geo.G >= 16 ? 2 : 1));
+        if (ks > 1 && A.sch.n_seg > 0) {
+            const int64_t extra = (int64_t)A.sch.n_seg * (ks - 1);
+            if ((int64_t)A.sch.w_total + extra > INT32_MAX) return fail(GNNK_EUNSUPPORTED, "too many wavefronts");
+            A.sch.seg_split = ks;
+            A.sch.w_big_end += (int32_t)extra;
+            A.sch.w_small_end += (int32_t)extra;
+            A.sch.w_total += (int32_t)extra;
+        }
+    }
     const Pick pk = pick_sddmm(g, A, geo, dtype, opk);
     const bool multi = A.out.reduce && geo.nchunk > 1;
     if (multi) {

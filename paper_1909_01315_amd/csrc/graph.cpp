@@ -745,6 +745,9 @@ gnnk_status gnnk_set_option(const char* key, int64_t value) {
     } else if (k == "fused_dw") {
         if (value < -1 || value > 1) return fail(GNNK_EINVAL, "fused_dw is -1 (auto), 0 or 1");
         options().fused_dw = value;
+    } else if (k == "sddmm_split") {
+        if (value < 0 || value > 8) return fail(GNNK_EINVAL, "sddmm_split is 0 (auto) or in [1, 8]");
+        options().sddmm_split = value;
     } else if (k == "no_fast") {
         if (value != 0 && value != 1) return fail(GNNK_EINVAL, "no_fast is 0 or 1");
         options().no_fast = value;

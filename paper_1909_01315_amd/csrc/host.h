@@ -77,6 +77,7 @@ struct Options {
     int64_t schedule = 0; // 0 auto, 1 row engine, 2 edge-parallel, 3 edge-parallel with atomics
     int64_t edge_chunk = 0; // positions per lane group of edge-parallel walks, 0 = auto
     int64_t fused_dw = -1;  // u_mul_e/sum's weight gradient inside the reverse dX pass: 1 always, 0 never, -1 one-column weights
+    int64_t sddmm_split = 0;  // wavefronts per hub segment of a g-SDDMM, 0 = auto
 };
 Options& options();
 

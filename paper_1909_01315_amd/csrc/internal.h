@@ -88,7 +88,7 @@ struct SchedDev {
     int32_t w_small_end;    // wave index where small rows end
     int32_t w_total;        // total waves
     int32_t fill_rows_per_group;
-    int32_t pad;
+    int32_t seg_split;      // g-SDDMM: wavefronts per hub segment (0 or 1: one); n_seg counts segments
 };
 
 struct GeomDev {

@@ -142,11 +142,21 @@ __global__ __launch_bounds__(256) void sddmm_kernel(EngineArgs A) {
     const int L = WAVE / G;
     if (w < A.sch.w_big_end) {
         int64_t r, b, e;
-        if (w < A.sch.n_seg) {
-            const int4 s = A.csr.segw[w];
+        const int ks = A.sch.seg_split > 1 ? A.sch.seg_split : 1;
+        const int nsw = A.sch.n_seg * ks;  // hub-segment wavefronts
+        if (w < nsw) {
+            const int4 s = A.csr.segw[w / ks];
             r = s.x; b = s.y; e = s.z;
+            if (ks > 1) {
+                // part w % ks of the segment, cut at whole batches
+                const int64_t nbt = (int64_t)G * ENGINE_UNR;
+                const int64_t step = ((e - b + ks - 1) / ks + nbt - 1) / nbt * nbt;
+                const int64_t b2 = b + (int64_t)(w % ks) * step;
+                b = b2 < e ? b2 : e;
+                e = b2 + step < e ? b2 + step : e;
+            }
         } else {
-            const int4 t = A.csr.rowt[A.sch.n_hub + (w - A.sch.n_seg)];
+            const int4 t = A.csr.rowt[A.sch.n_hub + (w - nsw)];
             r = t.x; b = t.y; e = t.z;
         }
         sddmm_row<T, VEC, OPK, EXT, RM, S, true>(A, ln, G, L, uniform64(r), uniform64(b), uniform64(e));

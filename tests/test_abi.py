@@ -55,6 +55,8 @@ def test_host_side_errors(lib):
     assert lib.gnnk_set_option(b"seg_edges", 0) == gnnk.OK  # per graph (the default)
     assert lib.gnnk_set_option(b"fused_dw", 2) == gnnk.EINVAL
     assert lib.gnnk_set_option(b"fused_dw", -1) == gnnk.OK  # the default
+    assert lib.gnnk_set_option(b"sddmm_split", 9) == gnnk.EINVAL
+    assert lib.gnnk_set_option(b"sddmm_split", 0) == gnnk.OK  # the default
     assert lib.edge_leaky_relu(None, None, ctypes.c_float(0.2), None) == gnnk.EINVAL
     n = ctypes.c_size_t(7)
     assert lib.graph_scratch_bytes(None, 64, 0, ctypes.byref(n)) == gnnk.EINVAL

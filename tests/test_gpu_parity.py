@@ -35,6 +35,7 @@ def reset_options():
     gnnk.set_option("no_split", 0)
     gnnk.set_option("small_deg", -1)
     gnnk.set_option("fused_dw", -1)
+    gnnk.set_option("sddmm_split", 0)
 
 
 def feats(seed, name, shape, lo=None, hi=None):
@@ -299,6 +300,27 @@ def test_edge_gradient_in_the_reverse_pass_is_bit_identical(shapes, seg, fused):
     assert_close(dW, ref, name="edge gradient")
     gl, _ = orc.gspmm_backward(p.o, "mul", "sum", X, W, dZ, want_rhs=False)
     assert_close(dX, gl, name="dX")
+
+
+@pytest.mark.parametrize("split", [1, 2, 3, 4, 8])
+@pytest.mark.parametrize("seg", [512, 64])
+def test_gsddmm_hub_segments_split_across_wavefronts(hot, split, seg):
+    """A hub segment of a g-SDDMM shared by several wavefronts, each taking
+    whole batches of it (the parts past the segment's end are empty): the
+    same results as one wavefront per segment, bit for bit where the oracle's
+    result is one rounding"""
+    gnnk.set_option("seg_edges", seg)
+    p = Pair(hot.o.src, hot.o.dst, 300, 300)
+    gnnk.set_option("sddmm_split", split)
+    el = feats(S1, "el", (300, 8, 1))
+    er = feats(S1, "er", (300, 8, 1))
+    assert_exact(gnnk.gsddmm(p.g, "add", dev(el), "u", dev(er), "v"), orc.gsddmm(p.o, "add", el, "u", er, "v"),
+                 "u_add_v")
+    X = feats(S1, "X", (300, 2, 32))
+    Y = feats(S1, "Y", (300, 2, 32))
+    assert_exact(gnnk.gsddmm(p.g, "mul", dev(X), "u", dev(Y), "v"), orc.gsddmm(p.o, "mul", X, "u", Y, "v"), "u_mul_v")
+    assert_close(gnnk.gsddmm(p.g, "dot", dev(X), "u", dev(Y), "v"), orc.gsddmm(p.o, "dot", X, "u", Y, "v"),
+                 name="u_dot_v")
 
 
 def test_gsddmm_u_add_v_scores(c1):
