@@ -8,7 +8,8 @@ are still covered.  Each case draws
     from the in-CSR (with or without explicit edge ids);
   - library options: hub segment size, small-row threshold, schedule
     (row engine, edge-parallel ordered, edge-parallel with atomics), the
-    edge-parallel chunk and the runtime-layout kernels;
+    edge-parallel chunk, the runtime-layout kernels and the wavefronts per
+    hub segment of a g-SDDMM;
   - shapes: H in {1, 2, 4, 8}, F from 1 to 40 (now and then a row wider than
     one pass of the wavefront: F of 100-300), each operand full (H, F), per
     head (H, 1) or one value (1, 1); fp32 or bf16; node tables with a padded
@@ -46,7 +47,7 @@ TARGETS = ["u", "e", "v"]
 def reset_options():
     yield
     for k, v in (("seg_edges", 0), ("small_deg", -1), ("schedule", 0), ("no_fast", 0), ("no_split", 0),
-                 ("edge_chunk", 0)):
+                 ("edge_chunk", 0), ("sddmm_split", 0)):
         gnnk.set_option(k, v)
 
 
@@ -155,6 +156,9 @@ def test_random_case(case):
     rng = np.random.default_rng(SEED0 + case)
     src, dst, n_src, n_dst, ptr64 = draw_graph(rng)
     opts = draw_options(rng)
+    # drawn from a stream of its own, so that the other draws of a case stay
+    # those of the seed
+    opts["sddmm_split"] = int(np.random.default_rng([SEED0 + case, 1]).choice([0, 0, 1, 2, 3]))
     build = ["coo", "coo", "csr", "csr_eids"][int(rng.integers(4))]
     side = bool(rng.random() < 0.3)
     if rng.random() < 0.1:
