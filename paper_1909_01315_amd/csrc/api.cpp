@@ -490,23 +490,22 @@ gnnk_status gspmm_impl(gnnk_graph_t g, gnnk_binop op, gnnk_reduce reduce, const 
     A.out.red = 1;
     A.out.reduce = 0;
     A.flags = (reduce == GNNK_MEAN ? F_OWN_MEAN : 0) | (reduce == GNNK_MIN ? F_IS_MIN : 0);
-    if (!cmp) {
-        // sums that gather node rows take the in-CSR's finer segments
-        // (c3 copy_u/mean 2.59 -> 2.46 ms, c4 copy_u/sum 3.59 -> 3.24 ms);
-        // copy_e sums keep the coarser ones, on which they run faster
-        const bool gathers = (A.a.target == T_NBR && A.a.full) || (A.b.data && A.b.target == T_NBR && A.b.full);
-        return run_spmm_sum(g, gathers ? g->in_fine : g->in, A, geo, dtype_code(out), opk, stream, sc);
-    }
+    // passes that gather node rows take the in-CSR's finer segments (c3
+    // copy_u/mean 2.59 -> 2.46 ms, c4 copy_u/sum 3.59 -> 3.24 ms); copy_e
+    // reductions keep the coarser ones, on which they run faster
+    const bool gathers = (A.a.target == T_NBR && A.a.full) || (A.b.data && A.b.target == T_NBR && A.b.full);
+    const Dir& d = gathers ? g->in_fine : g->in;
+    if (!cmp) return run_spmm_sum(g, d, A, geo, dtype_code(out), opk, stream, sc);
     A.arg_nbr = arg_lhs;
     A.arg_edge = arg_rhs;
-    A.csr = csr_of(g, g->in);
+    A.csr = csr_of(g, d);
     set_geo(A, geo);
-    A.sch = schedule(g->in, geo, true);
+    A.sch = schedule(d, geo, true);
     if (A.sch.n_seg > 0) {
         A.partial = sc.take((size_t)A.sch.n_seg * geo.D * 12);
         if (!A.partial) return scratch_fail(sc);
     }
-    const Pick pk = pick_spmm(g, g->in, A, geo, dtype_code(out), opk, true);
+    const Pick pk = pick_spmm(g, d, A, geo, dtype_code(out), opk, true);
     st = GNNK_LAUNCH(launch_spmm(A, dtype_code(out), geo.vec, true, opk, pk.spec, pk.gc, stream), "g-SpMM launch");
     if (st == GNNK_OK && A.sch.n_hub > 0)
         st = GNNK_LAUNCH(launch_spmm_combine(A, dtype_code(out), geo.vec, true, stream), "g-SpMM combine launch");
@@ -555,7 +554,7 @@ gnnk_status graph_scratch_bytes(gnnk_graph_t g, int64_t max_cols, int32_t flags,
     // sums and their gradients: fp64 partials of hub segments (any table)
     size_t need = al(std::max({si, sif, so}) * C * 8);
     // max / min: value, edge and neighbour per segment and column
-    need = std::max(need, al(si * C * 12));
+    need = std::max(need, al(std::max(si, sif) * C * 12));
     // fused attention: partial states of segments, and the row state of hub
     // rows when the attention is written
     need = std::max(need, al(si * 3 * C * 8 + (size_t)g->in.n_hub * 2 * C * 8));
