@@ -68,9 +68,13 @@ __device__ __forceinline__ int32_t pick(const int32_t* v, int u, int g) {
     if constexpr (GC == 1) {
         return __builtin_amdgcn_readfirstlane(v[u]);
     } else if constexpr (GC == 2) {
-        const int32_t x0 = __builtin_amdgcn_readfirstlane(v[2 * u]);
-        const int32_t x1 = __builtin_amdgcn_readfirstlane(v[2 * u + 1]);
-        return (g & 1) ? x1 : x0;
+        // the two candidates as one 64-bit scalar shifted by 0 or 32 bits in
+        // each lane: one VALU instruction with one scalar operand, where a
+        // select between two scalars first moves both into the lanes
+        const uint32_t x0 = (uint32_t)__builtin_amdgcn_readfirstlane(v[2 * u]);
+        const uint32_t x1 = (uint32_t)__builtin_amdgcn_readfirstlane(v[2 * u + 1]);
+        const uint64_t pr = ((uint64_t)x1 << 32) | x0;
+        return (int32_t)(uint32_t)(pr >> ((g & 1) << 5));
     } else {
         static_assert(GC == 4, "scalar id batches serve 1, 2 or 4 lane groups");
         const int32_t x0 = __builtin_amdgcn_readfirstlane(v[4 * u]);
