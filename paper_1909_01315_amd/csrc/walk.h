@@ -77,12 +77,13 @@ __device__ __forceinline__ int32_t pick(const int32_t* v, int u, int g) {
         return (int32_t)(uint32_t)(pr >> ((g & 1) << 5));
     } else {
         static_assert(GC == 4, "scalar id batches serve 1, 2 or 4 lane groups");
-        const int32_t x0 = __builtin_amdgcn_readfirstlane(v[4 * u]);
-        const int32_t x1 = __builtin_amdgcn_readfirstlane(v[4 * u + 1]);
-        const int32_t x2 = __builtin_amdgcn_readfirstlane(v[4 * u + 2]);
-        const int32_t x3 = __builtin_amdgcn_readfirstlane(v[4 * u + 3]);
-        const int32_t lo = (g & 1) ? x1 : x0;
-        const int32_t hi = (g & 1) ? x3 : x2;
+        const uint32_t x0 = (uint32_t)__builtin_amdgcn_readfirstlane(v[4 * u]);
+        const uint32_t x1 = (uint32_t)__builtin_amdgcn_readfirstlane(v[4 * u + 1]);
+        const uint32_t x2 = (uint32_t)__builtin_amdgcn_readfirstlane(v[4 * u + 2]);
+        const uint32_t x3 = (uint32_t)__builtin_amdgcn_readfirstlane(v[4 * u + 3]);
+        const int sh = (g & 1) << 5;
+        const int32_t lo = (int32_t)(uint32_t)((((uint64_t)x1 << 32) | x0) >> sh);
+        const int32_t hi = (int32_t)(uint32_t)((((uint64_t)x3 << 32) | x2) >> sh);
         return (g & 2) ? hi : lo;
     }
 }
