@@ -43,10 +43,16 @@ struct SddmmSink {
             double t = 0.0;
 #pragma unroll
             for (int i = 0; i < VEC; ++i) t += m[i];
-            // no masking of inactive lanes: a run is active or inactive as a
-            // whole (the row's lanes come in whole heads of four), its lanes
-            // only exchange among themselves, and inactive runs store nothing
             s[u] = t;
+        }
+        // Where the row's vectors come in whole runs of four (per-head dots,
+        // rows of a multiple of four vectors) every run is active or inactive
+        // as a whole and needs no masking.  A whole-row sum of three vectors
+        // (runs of four lanes, the fourth outside the row) zeroes the lane
+        // outside the row, whose loads repeat the row's first vector.
+        if ((A.geo.NV & 3) != 0) {
+#pragma unroll
+            for (int u = 0; u < UNR; ++u) s[u] = active ? s[u] : 0.0;
         }
         const int q = lig & 3;
         const bool odd = (q & 1) != 0, hi = (q & 2) != 0;
@@ -58,7 +64,10 @@ struct SddmmSink {
         // slot q's edge by two selects (no branches)
         const int32_t e01 = odd ? ed[1] : ed[0], e23 = odd ? ed[3] : ed[2];
         const int32_t e = hi ? e23 : e01;
-        if (active) {
+        // every lane of a run that holds a vector of the row stores its slot,
+        // also a lane outside the row in a partly active run
+        const bool run_active = ch * A.geo.L + (lig & ~3) < A.geo.NV;
+        if (run_active) {
             T* row = reinterpret_cast<T*>(A.out.data) + (uint64_t)(uint32_t)e * (uint32_t)A.out.stride;
             const bool neg = (A.flags & F_NEGATE) != 0;
             IO<T, VEC>::store1(row + (A.out.per_head ? h : 0), (float)(neg ? -tot : tot));

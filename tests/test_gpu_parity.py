@@ -323,6 +323,22 @@ def test_gsddmm_hub_segments_split_across_wavefronts(hot, split, seg):
                  name="u_dot_v")
 
 
+@pytest.mark.parametrize("H,F", [(4, 3), (1, 12), (2, 6), (3, 4), (1, 3), (2, 8), (1, 20)])
+@pytest.mark.parametrize("fused", [0, -1])
+def test_whole_row_sums_of_a_partial_run(hot, H, F, fused):
+    """The gradient of a one-value edge weight sums dZ[v] . X[u] over the whole
+    row.  Rows of three vectors (12 fp32 columns, 3 columns) fill three lanes
+    of a run of four: the fourth lane must add nothing and still store its
+    slot's edge (a case found by the random cases)"""
+    gnnk.set_option("fused_dw", fused)
+    X = feats(S1, "X", (300, H, F))
+    W = feats(S1, "W", (hot.o.n_edges, 1, 1), 0.5, 1.5)
+    dZ = feats(S1, "dZ", (300, H, F))
+    _, gr = orc.gspmm_backward(hot.o, "mul", "sum", X, W, dZ, want_lhs=False)
+    _, dr = gnnk.gspmm_backward(hot.g, "mul", "sum", dev(X), dev(W), dev(dZ), want_lhs=False)
+    assert_close(dr, gr, name=f"dW ({H}, {F})")
+
+
 def test_gsddmm_u_add_v_scores(c1):
     el = feats(S1, "el", (c1.o.n_src, 4, 1))
     er = feats(S1, "er", (c1.o.n_dst, 4, 1))
